@@ -1,0 +1,320 @@
+"""Pins for the CPU oracle: checks against things other than the oracle itself.
+
+Each pin takes the oracle's attention module `A` (and, where needed, its SP
+module `S`) as an argument, so the mutation test can run the same pins
+against deliberately broken copies of the oracle source.
+
+Sources of truth used here:
+  * closed forms (single visible key; all-zero queries give a uniform
+    softmax over the visible keys);
+  * a library routine: torch float64 scaled_dot_product_attention on the CPU
+    with an explicit boolean mask, and torch autograd through it;
+  * central finite differences of sum(dO * O);
+  * the gradient identities sum_j dK_j = 0 and sum_j dV_j = sum_i dO_i that
+    follow from softmax rows summing to one;
+  * exact-decomposition invariants the paper relies on: the ring fold equals
+    monolithic attention (Section 2.1), a packed batch equals its sequences
+    run one by one (Section 3.2), and Dummy-Head Ulysses over all ranks
+    equals attention without SP (Sections 4.1 and 6.1).
+"""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+from workloads import padded_heads
+
+
+def _kw(T, H, Hkv, cu=None, pos_q=None, pos_k=None, head_offset=0, num_real=None,
+        gqa=None, kv_off=0, scale=0.37, causal=True, Tk=None):
+    Tk = T if Tk is None else Tk
+    cu_q = np.array([0, T]) if cu is None else np.asarray(cu)
+    cu_k = np.array([0, Tk]) if cu is None else np.asarray(cu)
+    if pos_q is None:
+        pos_q = np.zeros(T, np.int64)
+        for s in range(len(cu_q) - 1):
+            pos_q[cu_q[s]:cu_q[s + 1]] = np.arange(cu_q[s + 1] - cu_q[s])
+    if pos_k is None:
+        pos_k = np.zeros(Tk, np.int64)
+        for s in range(len(cu_k) - 1):
+            pos_k[cu_k[s]:cu_k[s + 1]] = np.arange(cu_k[s + 1] - cu_k[s])
+    num_real = H if num_real is None else num_real
+    gqa = (num_real // Hkv if num_real >= Hkv else 1) if gqa is None else gqa
+    return dict(cu_q=cu_q, cu_k=cu_k, pos_q=pos_q, pos_k=pos_k, H_loc=H,
+                head_offset=head_offset, num_real_heads=num_real, gqa_group=gqa,
+                kv_head_offset=kv_off, scale=scale, causal=causal)
+
+
+def _rand(rng, *shape):
+    return rng.standard_normal(shape)
+
+
+# ---------------------------------------------------------------- closed forms
+def pin_single_visible_key(A):
+    """Row 0 of a causal segment sees only key 0: O_0 = v_0, LSE_0 = s q0.k0."""
+    rng = np.random.default_rng(1)
+    T, H, D = 9, 2, 5
+    q, k, v = _rand(rng, T, H, D), _rand(rng, T, 1, D), _rand(rng, T, 1, D)
+    kw = _kw(T, H, 1)
+    O, L = A.attn_forward(q, k, v, **kw)
+    for h in range(H):
+        assert np.allclose(O[0, h], v[0, 0], rtol=0, atol=1e-14)
+        assert np.isclose(L[h, 0], kw["scale"] * q[0, h] @ k[0, 0], rtol=0, atol=1e-14)
+
+
+def pin_zero_query_uniform(A):
+    """Q = 0 makes every visible score 0: O_i = mean of visible v_j and
+    LSE_i = log(number visible).  Varlen, offsets and padding rows included."""
+    rng = np.random.default_rng(2)
+    T, Tk, H, D = 23, 23, 3, 4
+    cu = np.array([0, 7, 7, 16, 20])
+    pos = np.zeros(T, np.int64)
+    pos[0:7] = 5 + np.arange(7)       # segment 0 starts at position 5
+    pos[7:16] = np.arange(9)
+    pos[16:20] = 2 + np.arange(4)
+    posk = pos.copy()
+    posk[0:7] = 3 + np.arange(7)      # keys start two positions earlier
+    q = np.zeros((T, H, D))
+    k, v = _rand(rng, Tk, 1, D), _rand(rng, Tk, 1, D)
+    kw = _kw(T, H, 1, cu=cu, pos_q=pos, pos_k=posk)
+    O, L = A.attn_forward(q, k, v, **kw)
+    seg = np.full(T, -1)
+    for s in range(len(cu) - 1):
+        seg[cu[s]:cu[s + 1]] = s
+    for i in range(T):
+        vis = [j for j in range(Tk) if seg[i] >= 0 and seg[j] == seg[i] and posk[j] <= pos[i]]
+        for h in range(H):
+            if vis:
+                assert np.allclose(O[i, h], v[vis, 0].mean(axis=0), atol=1e-13)
+                assert np.isclose(L[h, i], np.log(len(vis)), atol=1e-13)
+            else:
+                assert np.all(O[i, h] == 0) and L[h, i] == -np.inf
+
+
+# ------------------------------------------------------------ library routine
+def _torch_ref(q, k, v, do, kw):
+    """torch float64 SDPA with an explicit boolean mask, plus autograd."""
+    T, H, D = q.shape
+    Tk = k.shape[0]
+    seg_q = np.full(T, -1)
+    seg_k = np.full(Tk, -1)
+    for s in range(len(kw["cu_q"]) - 1):
+        seg_q[kw["cu_q"][s]:kw["cu_q"][s + 1]] = s
+        seg_k[kw["cu_k"][s]:kw["cu_k"][s + 1]] = s
+    mask = (seg_q[:, None] >= 0) & (seg_q[:, None] == seg_k[None, :])
+    if kw["causal"]:
+        mask &= np.asarray(kw["pos_k"])[None, :] <= np.asarray(kw["pos_q"])[:, None]
+    has = mask.any(axis=1)
+    O = np.zeros_like(q)
+    dq, dk, dv = np.zeros_like(q), np.zeros_like(k), np.zeros_like(v)
+    for h in range(H):
+        g = kw["head_offset"] + h
+        if g >= kw["num_real_heads"]:
+            continue
+        kv = g // kw["gqa_group"] - kw["kv_head_offset"]
+        tq = torch.tensor(q[has, h][None, None], requires_grad=True)
+        tk = torch.tensor(k[:, kv][None, None], requires_grad=True)
+        tv = torch.tensor(v[:, kv][None, None], requires_grad=True)
+        m = torch.tensor(mask[has][None, None])
+        o = torch.nn.functional.scaled_dot_product_attention(tq, tk, tv, attn_mask=m,
+                                                             scale=kw["scale"])
+        (o * torch.tensor(do[has, h][None, None])).sum().backward()
+        O[has, h] = o[0, 0].detach().numpy()
+        dq[has, h] = tq.grad[0, 0].numpy()
+        dk[:, kv] += tk.grad[0, 0].numpy()
+        dv[:, kv] += tv.grad[0, 0].numpy()
+    return O, dq, dk, dv
+
+
+def pin_torch_sdpa(A):
+    """Forward and backward equal torch fp64 SDPA + autograd (GQA, dummy
+    heads, varlen with padding rows, position offsets, non-causal)."""
+    rng = np.random.default_rng(3)
+    cases = [
+        dict(T=37, H=4, Hkv=1, D=8, cu=[0, 37], num_real=4, gqa=4, kv_off=0, ho=0),
+        dict(T=50, H=4, Hkv=2, D=6, cu=[0, 13, 13, 40, 47], num_real=7, gqa=2, kv_off=2, ho=4),
+        dict(T=41, H=3, Hkv=3, D=5, cu=[0, 20, 41], num_real=5, gqa=1, kv_off=3, ho=3),
+    ]
+    for c in cases:
+        T, H, Hkv, D = c["T"], c["H"], c["Hkv"], c["D"]
+        q, k, v, do = _rand(rng, T, H, D), _rand(rng, T, Hkv, D), _rand(rng, T, Hkv, D), _rand(rng, T, H, D)
+        for causal in (True, False):
+            kw = _kw(T, H, Hkv, cu=c["cu"], head_offset=c["ho"], num_real=c["num_real"],
+                     gqa=c["gqa"], kv_off=c["kv_off"], causal=causal)
+            O, _ = A.attn_forward(q, k, v, **kw)
+            dq, dk, dv = A.attn_backward(q, k, v, do, **kw)
+            rO, rdq, rdk, rdv = _torch_ref(q, k, v, do, kw)
+            for a, b in ((O, rO), (dq, rdq), (dk, rdk), (dv, rdv)):
+                assert np.allclose(a, b, rtol=0, atol=1e-12), np.abs(a - b).max()
+    # ring-style offsets: Q chunk at positions 40.., K chunk at 20..
+    T = 24
+    q, k, v, do = _rand(rng, T, 2, 4), _rand(rng, T, 1, 4), _rand(rng, T, 1, 4), _rand(rng, T, 2, 4)
+    kw = _kw(T, 2, 1, pos_q=40 + np.arange(T), pos_k=30 + np.arange(T))
+    O, _ = A.attn_forward(q, k, v, **kw)
+    rO, rdq, rdk, rdv = _torch_ref(q, k, v, do, kw)
+    dq, dk, dv = A.attn_backward(q, k, v, do, **kw)
+    for a, b in ((O, rO), (dq, rdq), (dk, rdk), (dv, rdv)):
+        assert np.allclose(a, b, rtol=0, atol=1e-12)
+
+
+# ------------------------------------------------------- finite differences
+def pin_finite_differences(A):
+    """Central differences of sum(dO * O) match the analytic backward."""
+    rng = np.random.default_rng(4)
+    T, H, Hkv, D = 11, 2, 1, 4
+    cu = [0, 6, 11]
+    q, k, v, do = _rand(rng, T, H, D), _rand(rng, T, Hkv, D), _rand(rng, T, Hkv, D), _rand(rng, T, H, D)
+    kw = _kw(T, H, Hkv, cu=cu, gqa=2)
+    dq, dk, dv = A.attn_backward(q, k, v, do, **kw)
+
+    def loss(qq, kk, vv):
+        return float((A.attn_forward(qq, kk, vv, **kw)[0] * do).sum())
+
+    h = 1e-6
+    for arr, grad, which in ((q, dq, 0), (k, dk, 1), (v, dv, 2)):
+        num = np.zeros_like(arr)
+        for idx in np.ndindex(arr.shape):
+            args = [q.copy(), k.copy(), v.copy()]
+            args[which][idx] += h
+            fp = loss(*args)
+            args[which][idx] -= 2 * h
+            fm = loss(*args)
+            num[idx] = (fp - fm) / (2 * h)
+        err = np.abs(num - grad).max() / max(1e-12, np.abs(grad).max())
+        assert err < 1e-6, (which, err)
+
+
+# ------------------------------------------------------ gradient identities
+def pin_gradient_sums(A):
+    """Per KV head: sum_j dK_j = 0 and sum_j dV_j = sum over rows with keys
+    of dO_i, for each segment separately."""
+    rng = np.random.default_rng(5)
+    T, H, Hkv, D = 45, 4, 2, 6
+    cu = [0, 17, 30, 45]
+    q, k, v, do = _rand(rng, T, H, D), _rand(rng, T, Hkv, D), _rand(rng, T, Hkv, D), _rand(rng, T, H, D)
+    kw = _kw(T, H, Hkv, cu=cu, gqa=2)
+    _, dk, dv = A.attn_backward(q, k, v, do, **kw)
+    for s in range(3):
+        a, b = cu[s], cu[s + 1]
+        for kv in range(Hkv):
+            assert np.allclose(dk[a:b, kv].sum(axis=0), 0, atol=1e-12)
+            want = do[a:b, 2 * kv:2 * kv + 2].sum(axis=(0, 1))
+            assert np.allclose(dv[a:b, kv].sum(axis=0), want, atol=1e-12)
+
+
+# -------------------------------------------------------- SP decompositions
+def pin_packed_equals_separate(A):
+    """A packed batch equals its sequences run one by one (fwd and bwd)."""
+    rng = np.random.default_rng(6)
+    lens = [9, 1, 14, 6]
+    T = sum(lens)
+    cu = np.concatenate([[0], np.cumsum(lens)])
+    H, Hkv, D = 2, 1, 4
+    q, k, v, do = _rand(rng, T, H, D), _rand(rng, T, Hkv, D), _rand(rng, T, Hkv, D), _rand(rng, T, H, D)
+    kw = _kw(T, H, Hkv, cu=cu)
+    O, L = A.attn_forward(q, k, v, **kw)
+    g = A.attn_backward(q, k, v, do, **kw)
+    for s, n in enumerate(lens):
+        a, b = cu[s], cu[s + 1]
+        kws = _kw(n, H, Hkv)
+        Os, Ls = A.attn_forward(q[a:b], k[a:b], v[a:b], **kws)
+        gs = A.attn_backward(q[a:b], k[a:b], v[a:b], do[a:b], **kws)
+        assert np.allclose(O[a:b], Os, atol=1e-13) and np.allclose(L[:, a:b], Ls, atol=1e-13)
+        for x, y in zip(g, gs):
+            assert np.allclose(x[a:b], y, atol=1e-13)
+
+
+def pin_ring_fold(A, S):
+    """Ring rank r: folding chunk partials with the LSE merge equals
+    monolithic causal attention over the concatenated keys; its backward
+    (per-chunk, with the final O/LSE) equals the monolithic backward."""
+    rng = np.random.default_rng(7)
+    C, n, r, H, Hkv, D = 8, 4, 2, 4, 2, 5
+    L = C * n
+    q_full, k_full, v_full, do_full = (_rand(rng, L, H, D), _rand(rng, L, Hkv, D),
+                                       _rand(rng, L, Hkv, D), _rand(rng, L, H, D))
+    q = q_full[r * C:(r + 1) * C]
+    do = do_full[r * C:(r + 1) * C]
+    chunks = [(k_full[c * C:(c + 1) * C], v_full[c * C:(c + 1) * C]) for c in range(r + 1)]
+    pos = [c * C + np.arange(C) for c in range(r + 1)]
+    common = dict(H_loc=H, head_offset=0, num_real_heads=H, gqa_group=2, kv_head_offset=0, scale=0.41)
+    o, lse = S.ring_forward(q, chunks, q_pos=r * C + np.arange(C), kv_pos=pos, **common)
+    Kc = k_full[:(r + 1) * C]
+    Vc = v_full[:(r + 1) * C]
+    mono = dict(cu_q=np.array([0, C]), cu_k=np.array([0, (r + 1) * C]),
+                pos_q=r * C + np.arange(C), pos_k=np.arange((r + 1) * C), **common)
+    Om, Lm = A.attn_forward(q, Kc, Vc, **mono)
+    assert np.allclose(o, Om, atol=1e-12) and np.allclose(lse, Lm, atol=1e-12)
+    dq, dks, dvs = S.ring_backward(q, chunks, do, o, lse, q_pos=r * C + np.arange(C), kv_pos=pos, **common)
+    dqm, dkm, dvm = A.attn_backward(q, Kc, Vc, do, **mono)
+    assert np.allclose(dq, dqm, atol=1e-12)
+    assert np.allclose(np.concatenate(dks), dkm, atol=1e-12)
+    assert np.allclose(np.concatenate(dvs), dvm, atol=1e-12)
+
+
+def pin_merge_identity(S):
+    """(0, -inf) is the merge identity; the merge is commutative; two
+    all-masked partials give (0, -inf) without NaN."""
+    rng = np.random.default_rng(8)
+    T, H, D = 6, 2, 3
+    o, l = _rand(rng, T, H, D), _rand(rng, H, T)
+    z, zl = np.zeros((T, H, D)), np.full((H, T), -np.inf)
+    a, b = S.lse_merge(o, l, z, zl)
+    assert np.array_equal(a, o) and np.array_equal(b, l)
+    a, b = S.lse_merge(z, zl, o, l)
+    assert np.allclose(a, o, atol=1e-15) and np.array_equal(b, l)
+    o2, l2 = _rand(rng, T, H, D), _rand(rng, H, T)
+    a1, b1 = S.lse_merge(o, l, o2, l2)
+    a2, b2 = S.lse_merge(o2, l2, o, l)
+    assert np.allclose(a1, a2, atol=1e-14) and np.allclose(b1, b2, atol=1e-14)
+    a, b = S.lse_merge(z, zl, z, zl)
+    assert np.all(a == 0) and np.all(b == -np.inf)
+    # weights: merging a partial with itself doubles the mass but keeps O
+    a, b = S.lse_merge(o, l, o, l)
+    assert np.allclose(a, o, atol=1e-14) and np.allclose(b, l + np.log(2), atol=1e-14)
+
+
+def pin_ulysses_equals_no_sp(A, S):
+    """Dummy-Head Ulysses over all ranks equals attention without SP, for MHA
+    with hs % sp != 0 and for GQA (the paper's forward-exactness check)."""
+    rng = np.random.default_rng(9)
+    for L, hs, hkv, sp, D in ((16, 7, 7, 2, 4), (24, 7, 1, 4, 3), (16, 6, 2, 4, 4), (8, 3, 3, 4, 2)):
+        q, k, v = _rand(rng, L, hs, D), _rand(rng, L, hkv, D), _rand(rng, L, hkv, D)
+        cu = np.array([0, L // 2 + 1, L])
+        pos = np.concatenate([np.arange(L // 2 + 1), np.arange(L - L // 2 - 1)])
+        o, lses = S.ulysses_simulate(q, k, v, sp, scale=0.5, cu=cu, pos=pos, gqa_group=hs // hkv)
+        ref, _ = A.attn_forward(q, k, v, cu_q=cu, cu_k=cu, pos_q=pos, pos_k=pos, H_loc=hs,
+                                head_offset=0, num_real_heads=hs, gqa_group=hs // hkv,
+                                kv_head_offset=0, scale=0.5)
+        assert o.shape == (L, hs, D)
+        assert np.allclose(o, ref, atol=1e-13)
+        hs_new = padded_heads(hs, sp)
+        hloc = hs_new // sp
+        for j in range(sp):  # dummy slots carry LSE = -inf
+            for h in range(hloc):
+                if j * hloc + h >= hs:
+                    assert np.all(lses[j][h] == -np.inf)
+
+
+def pin_pack_unpack(S):
+    """unpack(pack(x)) = x bit for bit; pack(x)[j] holds heads j*H.. with
+    zero dummies (closed form of the sequential split + head slicing)."""
+    rng = np.random.default_rng(10)
+    for T, hs, sp, D in ((12, 7, 2, 4), (8, 28, 8, 2), (6, 40, 16, 3)):
+        bits = rng.integers(0, 65536, size=(T, hs, D), dtype=np.uint16)
+        hs_new = padded_heads(hs, sp)
+        hloc = hs_new // sp
+        hm = np.array([h if h < hs else -1 for h in range(hs_new)])
+        packed = S.ulysses_pack(bits, sp, hloc, hm)
+        assert packed.shape == (sp, T, hloc, D)
+        padded = S.pad_heads(bits[None], sp)[0]
+        for j in range(sp):
+            assert np.array_equal(packed[j], padded[:, j * hloc:(j + 1) * hloc])
+        back = S.ulysses_unpack(packed, np.where(hm >= 0, hm, -1), hs)
+        assert back.dtype == bits.dtype and np.array_equal(back, bits)
+
+
+ATTN_PINS = [pin_single_visible_key, pin_zero_query_uniform, pin_torch_sdpa,
+             pin_finite_differences, pin_gradient_sums, pin_packed_equals_separate]
+SP_PINS = [pin_merge_identity, pin_pack_unpack]
+BOTH_PINS = [pin_ring_fold, pin_ulysses_equals_no_sp]
