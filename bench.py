@@ -1,0 +1,370 @@
+#!/usr/bin/env python3
+"""Benchmark of one sequence-parallel rank's attention shard on MI355X.
+
+Metric: attention forward+backward TFLOP/s counting real heads only
+(14 * D * allowed_pairs * H_real per step), and its fraction of the MI355X
+bf16 dense MFMA peak (2.5 PFLOP/s).
+
+A step is one pass of the rank's hot path over one batch of synthetic input
+already resident in HBM:
+  Ulysses shard: pack Q, K, V (dummy-head zero fill) -> attention forward ->
+      unpack O -> pack dO -> attention backward -> unpack dQ (MHA: dK, dV too)
+  packed varlen shard: attention forward -> backward
+  ring rank r: r+1 fused ring steps (LSE merge in the epilogue, bf16 O on the
+      last) -> per-chunk backward into an fp32 dQ accumulator -> dQ to bf16
+The all-to-all itself is not run (one GPU).
+
+Output: ONE JSON line on stdout (driver contract), with a `roofline` object
+for the dominant kernel (HIP-event timed on the library's stream) and a
+`cpu_baseline` object (the fp64 oracle on a bounded sample on host cores).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+from workloads import (allowed_pairs, ring_chunk_positions, shard_inputs, randn_bf16_bits,  # noqa: E402
+                       ulysses_kv_head_map, ulysses_q_head_map, workload, WORKLOADS)
+
+METRIC = "attn fwd+bwd TFLOP/s (real heads) per SP-rank shard; % of bf16 MFMA peak"
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA, published
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E, published
+DEFAULT_WORKLOAD = "ulysses_7b_L32768_q28kv4_sp8_r6_d128"
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+class KernelTimers:
+    """Event pairs armed around individual library kernels (sp_profile_events)."""
+
+    def __init__(self, sp, torch):
+        self.sp, self.torch = sp, torch
+        self.pool, self.used, self.on = [], [], False
+
+    def arm(self, kid, flops):
+        if not self.on:
+            return
+        if len(self.used) >= len(self.pool):
+            a = self.torch.cuda.Event(enable_timing=True)
+            b = self.torch.cuda.Event(enable_timing=True)
+            a.record()
+            b.record()
+            self.pool.append((a, b))
+        pair = self.pool[len(self.used)]
+        self.used.append((kid, flops, pair))
+        self.sp.sp_profile_events(kid, *pair)
+
+    def disarm(self):
+        for kid in (1, 2, 3, 4, 5, 6):
+            self.sp.sp_profile_events(kid, None, None)
+
+    def summary(self):
+        out = {}
+        for kid, flops, (a, b) in self.used:
+            ms = a.elapsed_time(b)
+            s = out.setdefault(kid, {"ms": 0.0, "n": 0, "flops": 0.0})
+            s["ms"] += ms
+            s["n"] += 1
+            s["flops"] += flops
+        return out
+
+
+KNAMES = {1: "attn_fwd_kernel", 2: "attn_dq_kernel", 3: "attn_dkdv_kernel", 4: "pack_kernel",
+          5: "unpack_kernel", 6: "merge_kernel"}
+
+
+def lib_desc(sp, sh, pos_k=None):
+    return sp.Desc(T_q=sh.T_q, T_k=sh.T_k, head_dim=sh.D, H_loc=sh.H_loc,
+                   head_offset=sh.head_offset, num_real_heads=sh.num_real_heads,
+                   num_padded_heads=sh.num_padded_heads, gqa_group=sh.gqa_group,
+                   Hkv_loc=sh.Hkv_loc, kv_head_offset=sh.kv_head_offset,
+                   cu_seqlens_q=sh.cu_q, cu_seqlens_k=sh.cu_k, position_ids_q=sh.pos_q,
+                   position_ids_k=sh.pos_k if pos_k is None else pos_k, causal=sh.causal,
+                   softmax_scale=sh.scale)
+
+
+def to_dev(torch, bits):
+    return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).cuda()
+
+
+class Step:
+    """Buffers and the launch sequence of one step for a workload."""
+
+    def __init__(self, sp, torch, sh, timers):
+        self.sp, self.torch, self.sh, self.t = sp, torch, sh, timers
+        dev = "cuda"
+        D = sh.D
+        self.ring = sh.ring_chunks > 0
+        nr = sh.n_real_loc
+        if self.ring:
+            self.descs = [lib_desc(sp, sh, ring_chunk_positions(sh, c)) for c in range(sh.ring_chunks)]
+            self.pairs = [allowed_pairs(sh.cu_q, sh.cu_k, sh.pos_q, ring_chunk_positions(sh, c))
+                          for c in range(sh.ring_chunks)]
+            q, _, _, do = shard_inputs(sh, chunk=0)
+            self.q, self.do = to_dev(torch, q), to_dev(torch, do)
+            self.k, self.v = [], []
+            for c in range(sh.ring_chunks):
+                _, k, v, _ = shard_inputs(sh, chunk=c)
+                self.k.append(to_dev(torch, k))
+                self.v.append(to_dev(torch, v))
+            self.o_acc = torch.empty((sh.T_q, sh.H_loc, D), dtype=torch.float32, device=dev)
+            self.lse_acc = torch.empty((sh.H_loc, sh.T_q), dtype=torch.float32, device=dev)
+            self.o = torch.empty((sh.T_q, sh.H_loc, D), dtype=torch.bfloat16, device=dev)
+            self.dq_acc = torch.empty((sh.T_q, sh.H_loc, D), dtype=torch.float32, device=dev)
+            self.dq = torch.empty((sh.T_q, sh.H_loc, D), dtype=torch.bfloat16, device=dev)
+            self.dk = [torch.empty_like(x) for x in self.k]
+            self.dv = [torch.empty_like(x) for x in self.v]
+            self.ws_f = torch.empty(sp.sp_attn_workspace_size(self.descs[0], sp.SP_OP_RING_STEP),
+                                    dtype=torch.uint8, device=dev)
+            self.ws_b = torch.empty(sp.sp_attn_workspace_size(self.descs[0], sp.SP_OP_BWD),
+                                    dtype=torch.uint8, device=dev)
+        else:
+            self.desc = lib_desc(sp, sh)
+            self.pairs = [allowed_pairs(sh.cu_q, sh.cu_k, sh.pos_q, sh.pos_k)]
+            q, k, v, do = shard_inputs(sh)
+            self.q, self.k, self.v, self.do = (to_dev(torch, x) for x in (q, k, v, do))
+            self.o = torch.empty_like(self.q)
+            self.lse = torch.empty((sh.H_loc, sh.T_q), dtype=torch.float32, device=dev)
+            self.dq = torch.empty_like(self.q)
+            self.dk = torch.empty_like(self.k)
+            self.dv = torch.empty_like(self.v)
+            self.ws_f = torch.empty(sp.sp_attn_workspace_size(self.desc, sp.SP_OP_FWD),
+                                    dtype=torch.uint8, device=dev)
+            self.ws_b = torch.empty(sp.sp_attn_workspace_size(self.desc, sp.SP_OP_BWD),
+                                    dtype=torch.uint8, device=dev)
+            self.ulysses = sh.sp > 1
+            if self.ulysses:
+                Tl = sh.T_q // sh.sp
+                self.Tl = Tl
+                sb = sh.seed_base + 50
+                # the rank's pre-all-to-all token slice of every head
+                self.q_pre = to_dev(torch, randn_bf16_bits((Tl, sh.hs, D), sb))
+                self.do_pre = to_dev(torch, randn_bf16_bits((Tl, sh.hs, D), sb + 1))
+                self.k_pre = to_dev(torch, randn_bf16_bits((Tl, sh.hkv, D), sb + 2))
+                self.v_pre = to_dev(torch, randn_bf16_bits((Tl, sh.hkv, D), sb + 3))
+                self.qmap = ulysses_q_head_map(sh.hs, sh.sp)
+                self.mha = sh.hkv == sh.hs
+                self.kmap = self.qmap if self.mha else ulysses_kv_head_map(sh.hs, sh.hkv, sh.sp)
+                self.kw = len(self.kmap) // sh.sp
+                self.send_q = torch.empty((sh.sp, Tl, sh.H_loc, D), dtype=torch.bfloat16, device=dev)
+                self.send_do = torch.empty_like(self.send_q)
+                self.send_k = torch.empty((sh.sp, Tl, self.kw, D), dtype=torch.bfloat16, device=dev)
+                self.send_v = torch.empty_like(self.send_k)
+                self.o_pre = torch.empty((Tl, sh.hs, D), dtype=torch.bfloat16, device=dev)
+                self.dq_pre = torch.empty_like(self.o_pre)
+                if self.mha:
+                    self.dk_pre = torch.empty((Tl, sh.hkv, D), dtype=torch.bfloat16, device=dev)
+                    self.dv_pre = torch.empty_like(self.dk_pre)
+        H = nr * D
+        self.flops_fwd = [4.0 * H * p for p in self.pairs]
+        self.flops_dq = [6.0 * H * p for p in self.pairs]
+        self.flops_dkdv = [8.0 * H * p for p in self.pairs]
+        self.flops_metric = 14.0 * H * sum(self.pairs)
+        self.flops_strict = 12.0 * H * sum(self.pairs)
+        sh_ = sh
+        self.pack_bytes = 0
+        if not self.ring and self.ulysses:
+            el = 2 * sh_.D
+            Tl = self.Tl
+            self.pack_bytes = Tl * sh_.hs * el + sh_.sp * Tl * sh_.H_loc * el
+
+    def run(self):
+        sp, t = self.sp, self.t
+        if self.ring:
+            n = len(self.descs)
+            for c in range(n):
+                t.arm(sp.SP_KERNEL_ATTN_FWD, self.flops_fwd[c])
+                sp.sp_ring_step(self.descs[c], self.q, self.k[c], self.v[c], self.o_acc,
+                                self.lse_acc, init=(c == 0), o_out=self.o if c == n - 1 else None,
+                                workspace=self.ws_f)
+            self.dq_acc.zero_()
+            for c in range(n):
+                t.arm(sp.SP_KERNEL_ATTN_DQ, self.flops_dq[c])
+                t.arm(sp.SP_KERNEL_ATTN_DKDV, self.flops_dkdv[c])
+                sp.sp_attn_bwd(self.descs[c], self.q, self.k[c], self.v[c], self.o, self.lse_acc,
+                               self.do, dq_acc=self.dq_acc, dk=self.dk[c], dv=self.dv[c],
+                               workspace=self.ws_b)
+            sp.sp_f32_to_bf16(self.dq_acc, self.dq)
+            return
+        sh = self.sh
+        if self.ulysses:
+            t.arm(sp.SP_KERNEL_PACK, 0.0)
+            sp.sp_ulysses_pack(self.q_pre, sh.sp, sh.H_loc, self.qmap, dst=self.send_q)
+            sp.sp_ulysses_pack(self.k_pre, sh.sp, self.kw, self.kmap, dst=self.send_k)
+            sp.sp_ulysses_pack(self.v_pre, sh.sp, self.kw, self.kmap, dst=self.send_v)
+        t.arm(sp.SP_KERNEL_ATTN_FWD, self.flops_fwd[0])
+        sp.sp_attn_fwd(self.desc, self.q, self.k, self.v, self.o, self.lse, workspace=self.ws_f)
+        if self.ulysses:
+            t.arm(sp.SP_KERNEL_UNPACK, 0.0)
+            sp.sp_ulysses_unpack(self.o.view(sh.sp, self.Tl, sh.H_loc, sh.D), self.qmap, sh.hs,
+                                 dst=self.o_pre)
+            sp.sp_ulysses_pack(self.do_pre, sh.sp, sh.H_loc, self.qmap, dst=self.send_do)
+        t.arm(sp.SP_KERNEL_ATTN_DQ, self.flops_dq[0])
+        t.arm(sp.SP_KERNEL_ATTN_DKDV, self.flops_dkdv[0])
+        sp.sp_attn_bwd(self.desc, self.q, self.k, self.v, self.o, self.lse, self.do, dq=self.dq,
+                       dk=self.dk, dv=self.dv, workspace=self.ws_b)
+        if self.ulysses:
+            sp.sp_ulysses_unpack(self.dq.view(sh.sp, self.Tl, sh.H_loc, sh.D), self.qmap, sh.hs,
+                                 dst=self.dq_pre)
+            if self.mha:
+                sp.sp_ulysses_unpack(self.dk.view(sh.sp, self.Tl, sh.H_loc, sh.D), self.qmap,
+                                     sh.hkv, dst=self.dk_pre)
+                sp.sp_ulysses_unpack(self.dv.view(sh.sp, self.Tl, sh.H_loc, sh.D), self.qmap,
+                                     sh.hkv, dst=self.dv_pre)
+
+
+def cpu_baseline(sh, budget_s=15.0):
+    """The fp64 oracle, as it stands, on a causal prefix of the workload's first
+    segment (all real heads), sized for ~budget_s of CPU work."""
+    import oracle
+    from threadpoolctl import threadpool_info
+    seg0 = int(sh.cu_q[1] - sh.cu_q[0])
+    rng_bits = shard_inputs(sh, chunk=0 if sh.ring_chunks else None)
+
+    def run(L):
+        q, k, v, do = (oracle.bf16_bits_to_f64(x[:L]) for x in rng_bits)
+        cu = np.array([0, L])
+        pos = np.arange(L)
+        kw = dict(cu_q=cu, cu_k=cu, pos_q=pos, pos_k=pos, H_loc=sh.H_loc,
+                  head_offset=sh.head_offset, num_real_heads=sh.num_real_heads,
+                  gqa_group=sh.gqa_group, kv_head_offset=sh.kv_head_offset, scale=sh.scale)
+        t0 = time.perf_counter()
+        o, lse = oracle.attn_forward(q, k, v, **kw)
+        oracle.attn_backward(q, k, v, do, o=o, lse=lse, **kw)
+        return time.perf_counter() - t0
+
+    L0 = min(1024, seg0)
+    t0 = run(L0)
+    L = int(min(seg0, L0 * math.sqrt(max(1.0, budget_s / max(t0, 1e-3)))))
+    L = max(L0, L // 256 * 256)
+    dt = run(L)
+    pairs = L * (L + 1) // 2
+    flops = 14.0 * sh.D * pairs * sh.n_real_loc
+    threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
+            "sample": (f"fp64 oracle fwd+bwd on the causal prefix L={L} of the first segment, "
+                       f"{sh.n_real_loc} real heads, D={sh.D}; {dt:.1f} s"),
+            "seconds": round(dt, 2)}
+
+
+def measure(sp, torch, name, steps, warmup, per_kernel=True):
+    sh = workload(name)
+    timers = KernelTimers(sp, torch)
+    st = Step(sp, torch, sh, timers)
+    for _ in range(warmup):
+        st.run()
+    torch.cuda.synchronize()
+    timers.on = per_kernel
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        st.run()
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    timers.on = False
+    timers.disarm()
+    ms = dt * 1e3 / steps
+    return sh, st, ms, timers.summary()
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD, choices=WORKLOADS)
+    ap.add_argument("--all", action="store_true", help="one JSON line per workload")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--dummy-overhead", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path "
+              "(one SP rank's shard per GPU); run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import paper_2505_22296_amd as sp
+    sp.load()
+    names = WORKLOADS if args.all else [args.workload]
+    for name in names:
+        sh, st, ms, ks = measure(sp, torch, name, args.steps, args.warmup)
+        value = st.flops_metric / (ms * 1e-3) / 1e12
+        # dominant kernel: most time per step
+        dom = max(ks.items(), key=lambda kv: kv[1]["ms"]) if ks else None
+        roof = None
+        kern = {}
+        for kid, s in ks.items():
+            avg = s["ms"] / s["n"]
+            kern[KNAMES[kid]] = {"avg_ms": round(avg, 4), "launches_per_step": s["n"] / args.steps,
+                                 "tflops": round(s["flops"] / s["n"] / (avg * 1e-3) / 1e12, 1)
+                                 if s["flops"] else None}
+        if dom:
+            kid, s = dom
+            avg_s = s["ms"] / s["n"] * 1e-3
+            ach = s["flops"] / s["n"] / avg_s / 1e12
+            roof = {"bound": "mfma", "kernel": KNAMES[kid], "achieved": round(ach, 1),
+                    "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                    "frac": round(ach / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                    "avg_launch_ms": round(s["ms"] / s["n"], 4),
+                    "flops_per_launch": s["flops"] / s["n"]}
+        out = {
+            "metric": METRIC, "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1,
+            "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
+            "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+            "data": "synthetic (seeded N(0,1) bf16; shapes of the paper's workloads)",
+            "config": {"workload": name, "T_q": sh.T_q, "T_k": sh.T_k, "D": sh.D,
+                       "H_loc": sh.H_loc, "H_real": sh.n_real_loc, "Hkv_loc": sh.Hkv_loc,
+                       "segments": int(len(sh.cu_q) - 1), "ring_chunks": sh.ring_chunks,
+                       "sp": sh.sp, "rank": sh.rank, "pairs_per_head": int(sum(st.pairs)),
+                       "flops_per_step": st.flops_metric},
+            "pct_of_bf16_peak": round(100.0 * value / PEAK_BF16_TFLOPS, 2),
+            "strict_12D_tflops": round(st.flops_strict / (ms * 1e-3) / 1e12, 2),
+            "kernels": kern,
+            "roofline": roof,
+        }
+        if args.dummy_overhead and sh.n_real_loc < sh.H_loc:
+            out["dummy_overhead"] = dummy_overhead(sp, torch, sh, args.steps)
+        if not args.no_cpu_baseline and name == names[0]:
+            log("timing the CPU oracle baseline ...")
+            out["cpu_baseline"] = cpu_baseline(sh)
+        print(json.dumps(out), flush=True)
+
+
+def dummy_overhead(sp, torch, sh, steps):
+    """fwd+bwd time with dummy slots vs the same real heads without them."""
+    res = {}
+    for tag, s in (("with_dummies", sh), ("without", sh.without_dummies())):
+        desc = lib_desc(sp, s)
+        q, k, v, do = (to_dev(torch, x) for x in shard_inputs(s))
+        o, lse = torch.empty_like(q), torch.empty((s.H_loc, s.T_q), dtype=torch.float32, device="cuda")
+        dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+        wf = torch.empty(sp.sp_attn_workspace_size(desc, sp.SP_OP_FWD), dtype=torch.uint8, device="cuda")
+        wb = torch.empty(sp.sp_attn_workspace_size(desc, sp.SP_OP_BWD), dtype=torch.uint8, device="cuda")
+
+        def run():
+            sp.sp_attn_fwd(desc, q, k, v, o, lse, workspace=wf)
+            sp.sp_attn_bwd(desc, q, k, v, o, lse, do, dq=dq, dk=dk, dv=dv, workspace=wb)
+
+        run()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            run()
+        torch.cuda.synchronize()
+        res[tag + "_ms"] = round((time.perf_counter() - t0) * 1e3 / steps, 4)
+    res["overhead_pct"] = round(100.0 * (res["with_dummies_ms"] / res["without_ms"] - 1.0), 2)
+    return res
+
+
+if __name__ == "__main__":
+    main()

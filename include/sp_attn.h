@@ -1,0 +1,263 @@
+/*
+ * sp_attn.h -- C ABI of the per-rank sequence-parallel attention library
+ * (MI355X / gfx950).
+ *
+ * The library computes one sequence-parallel (SP) rank's share of a causal,
+ * packed-varlen attention layer, forward and backward, for the two SP modes
+ * of arXiv 2505.22296:
+ *
+ *   - Dummy-Head Ulysses (Section 4, Listing 1).  Query heads are padded at
+ *     the END of the head axis with zero "dummy" heads up to a multiple of
+ *     the SP size; after the all-to-all a rank holds the full sequence over
+ *     H_loc = hs_new / sp head slots.  Dummy slots are never computed: their
+ *     outputs and gradients are written as +0.0 (LSE -inf).
+ *   - Ring-Attention (Section 2.1, Table 1).  A rank's Q chunk is run against
+ *     successive KV chunks and partial results are combined through
+ *     log-sum-exp.
+ *
+ * Conventions shared by every entry point
+ *   Memory      All tensor pointers are DEVICE pointers owned by the caller;
+ *               the library allocates no device memory.  Scratch space is a
+ *               caller-provided workspace of the size sp_attn_workspace_size
+ *               reports (256-byte aligned).  Arrays documented as HOST are
+ *               read during the call only.
+ *   Layout      Activations are contiguous [T, H, D] (token-major, D
+ *               innermost), bf16 stored as uint16 bit patterns, 16-byte
+ *               aligned.  LSE arrays are float32 [H, T] (head-major), natural
+ *               logarithm.
+ *   Streams     `stream` is a hipStream_t (NULL = the default stream).  Calls
+ *               enqueue work and return; results are ready when the stream
+ *               reaches them.  Host arrays may be freed on return.
+ *   Errors      Every call returns sp_status.  Arguments are validated before
+ *               anything is enqueued; on error nothing is launched and no
+ *               output is touched.  SP_ERR_HIP reports a failed launch or copy.
+ *               No C++ exception crosses this interface.
+ *   Threading   The library holds no state; calls are reentrant.  Calls that
+ *               share a workspace must be ordered on one stream.
+ *
+ * Numerics: bf16 operands, float32 accumulation, float32 softmax statistics,
+ * outputs rounded to bf16 with round-to-nearest-even.
+ */
+#ifndef SP_ATTN_H
+#define SP_ATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum sp_status {
+  SP_OK = 0,
+  SP_ERR_INVALID_ARG = 1, /* inconsistent shapes, heads, segments, positions, pointers */
+  SP_ERR_UNSUPPORTED = 2, /* valid but not implemented (e.g. head_dim not 64/128) */
+  SP_ERR_WORKSPACE = 3,   /* workspace missing, misaligned or too small */
+  SP_ERR_HIP = 4          /* a HIP launch or copy failed */
+} sp_status;
+
+/* Operation selector for sp_attn_workspace_size / sp_attn_schedule. */
+enum { SP_OP_FWD = 0, SP_OP_BWD = 1, SP_OP_RING_STEP = 2 };
+
+/*
+ * One rank's attention problem.
+ *
+ * Heads.  Global query heads 0..num_padded_heads-1 exist after dummy-head
+ * padding (Listing 1: hs_new = hs + (sp - hs % sp) % sp); heads >= hs =
+ * num_real_heads are dummies.  This rank holds the H_loc consecutive slots
+ * starting at global head head_offset (Ulysses: rank * H_loc; ring: 0).
+ * Real query head g reads KV head g / gqa_group; the rank holds the Hkv_loc
+ * consecutive KV heads starting at kv_head_offset.  Requirements:
+ * num_padded_heads % H_loc == 0, head_offset % H_loc == 0,
+ * num_padded_heads - num_real_heads < num_padded_heads / H_loc (fewer dummies
+ * than ranks), num_real_heads % gqa_group == 0, and every real local head's KV
+ * head lies in the local KV range.
+ *
+ * Segments (neat packing, Section 3.2).  num_seqs segments; query rows
+ * [cu_seqlens_q[s], cu_seqlens_q[s+1]) attend to keys
+ * [cu_seqlens_k[s], cu_seqlens_k[s+1]) only.  Rows/keys past the last
+ * segment are padding: they attend to nothing (O = 0, LSE = -inf) and are
+ * attended by nothing.  cu arrays start at 0, are non-decreasing, and end at
+ * or below T.
+ *
+ * Positions (Section 5.2: explicit global position IDs).  When causal, key j
+ * is visible to row i iff position_ids_k[j] <= position_ids_q[i] (diagonal
+ * included).  Inside each segment positions must be a +1 ramp; only each
+ * segment's first position matters, so ring chunks express their global
+ * offsets here (Q chunk r at r*C.., KV chunk c at c*C..).  NULL means
+ * positions 0,1,.. restarting at every segment.
+ */
+typedef struct sp_attn_desc {
+  int32_t T_q;              /* query tokens at this rank (rows of q, o, dq)         */
+  int32_t T_k;              /* key tokens (rows of k, v, dk, dv)                     */
+  int32_t head_dim;         /* D: 64 or 128                                          */
+  int32_t H_loc;            /* query-head slots at this rank, real and dummy        */
+  int32_t head_offset;      /* global index of local query slot 0                    */
+  int32_t num_real_heads;   /* hs                                                    */
+  int32_t num_padded_heads; /* hs_new                                                */
+  int32_t gqa_group;        /* real query heads per KV head (1 = MHA)                */
+  int32_t Hkv_loc;          /* KV heads at this rank                                 */
+  int32_t kv_head_offset;   /* global index of local KV head 0                       */
+  int32_t num_seqs;         /* segments (>= 0)                                       */
+  int32_t causal;           /* 1 = causal by position inside a segment, 0 = full     */
+  float softmax_scale;      /* multiplies q.k (callers pass 1/sqrt(D))               */
+  int32_t reserved;         /* must be 0                                             */
+  const int32_t* cu_seqlens_q;   /* HOST, num_seqs + 1                               */
+  const int32_t* cu_seqlens_k;   /* HOST, num_seqs + 1                               */
+  const int32_t* position_ids_q; /* HOST, T_q, or NULL                               */
+  const int32_t* position_ids_k; /* HOST, T_k, or NULL                               */
+} sp_attn_desc;
+
+/* Human-readable name of a status code (static storage). */
+const char* sp_status_string(sp_status s);
+
+/* Library version as major*10000 + minor*100 + patch. */
+int32_t sp_version(void);
+
+/*
+ * Dummy-head padding + Ulysses send-side pack (Section 4.1, Listing 1, and
+ * the [L/sp, hs, d] -> [L, hs/sp, d] all-to-all layout of Section 4):
+ *
+ *   dst[j, t, h, :] = src[t, head_map[j*H_dst_loc + h], :]   (map entry >= 0)
+ *   dst[j, t, h, :] = 0                                       (map entry == -1)
+ *
+ * src: [T_loc, H_src, D] bf16; dst: [sp, T_loc, H_dst_loc, D] bf16, where
+ * chunk j is what goes to rank j.  head_map: HOST, sp*H_dst_loc entries in
+ * [-1, H_src); a source head may appear several times (GQA K/V replicated to
+ * two ranks).  For Ulysses Q (and MHA K/V) the map is
+ * j*H_loc + h if < hs else -1, which is Listing 1's pad followed by the even
+ * head split.  Bit copy: the output is exact.  D must be a multiple of 8.
+ * T_loc == 0 is a no-op.
+ */
+sp_status sp_ulysses_pack(const void* src, int32_t T_loc, int32_t H_src, int32_t head_dim,
+                          int32_t sp, int32_t H_dst_loc, const int32_t* head_map, void* dst,
+                          void* stream);
+
+/*
+ * Ulysses receive-side unpack + unpad (Listing 1 unpad_heads, after the
+ * reverse all-to-all):
+ *
+ *   dst[t, head_map[j*H_src_loc + h], :] = src[j, t, h, :]   (map entry >= 0)
+ *
+ * src: [sp, T_loc, H_src_loc, D] bf16; dst: [T_loc, H_dst, D] bf16.
+ * Entries equal to -1 (dummy slots) are dropped.  Every destination head
+ * 0..H_dst-1 must be named exactly once (otherwise SP_ERR_INVALID_ARG).
+ * Bit copy.
+ */
+sp_status sp_ulysses_unpack(const void* src, int32_t T_loc, int32_t H_src_loc, int32_t head_dim,
+                            int32_t sp, const int32_t* head_map, int32_t H_dst, void* dst,
+                            void* stream);
+
+/* Workspace bytes needed by `op` (SP_OP_FWD, SP_OP_BWD, SP_OP_RING_STEP) for
+ * this problem.  Validates the descriptor. */
+sp_status sp_attn_workspace_size(const sp_attn_desc* desc, int32_t op, size_t* bytes);
+
+/*
+ * Attention forward over the rank's real heads (the FlashAttention-style
+ * fused kernel: bf16 MFMA for QK^T and PV, fp32 online softmax, causal and
+ * varlen block skipping; dummy slots are not computed).
+ *
+ * q: [T_q, H_loc, D]; k, v: [T_k, Hkv_loc, D]   (bf16, inputs, not modified)
+ * o: [T_q, H_loc, D] bf16 output; lse: [H_loc, T_q] float32 output.
+ * Real head rows: O = softmax(scale q k^T + mask) v, LSE = log-sum-exp of the
+ * masked scaled scores.  Rows without visible keys and all dummy slots:
+ * O = +0.0, LSE = -inf.
+ */
+sp_status sp_attn_fwd(const sp_attn_desc* desc, const void* q, const void* k, const void* v,
+                      void* o, float* lse, void* workspace, size_t workspace_bytes,
+                      void* stream);
+
+/*
+ * Attention backward (gradients of sum(dO * O)), with P recomputed from LSE:
+ * dV = P^T dO, dP = dO V^T, dS = P (dP - rowsum(dO o O)), dQ = scale dS K,
+ * dK = scale dS^T Q.  dK/dV of a KV head sum over its real query heads.
+ *
+ * o, lse: the forward's outputs (for ring: the FINAL merged O and LSE).
+ * dout: [T_q, H_loc, D] bf16.
+ * dq: bf16 [T_q, H_loc, D], written; or NULL when dq_acc is given.
+ * dq_acc: float32 [T_q, H_loc, D], dQ is ADDED to it (ring: accumulate over
+ *         KV chunks); or NULL.  Exactly one of dq / dq_acc must be non-NULL.
+ * dk, dv: bf16 [T_k, Hkv_loc, D], written.
+ * Dummy slots: dq = +0.0 (dq_acc untouched); KV heads read by no real query
+ * head get dk = dv = +0.0.  Deterministic: no atomics.
+ */
+sp_status sp_attn_bwd(const sp_attn_desc* desc, const void* q, const void* k, const void* v,
+                      const void* o, const float* lse, const void* dout, void* dq,
+                      float* dq_acc, void* dk, void* dv, void* workspace,
+                      size_t workspace_bytes, void* stream);
+
+/*
+ * One Ring-Attention step (Section 2.1): attention of the rank's Q chunk
+ * against one KV chunk, merged into running float32 accumulators:
+ *   (O, L) <- (O, L) (+) (O_c, L_c),  L = logaddexp(L, L_c),
+ *   O = e^(L_old - L) O + e^(L_c - L) O_c.
+ * desc positions carry the chunk offsets.  init = 1 on the first chunk:
+ * the accumulators are overwritten with this chunk's partial (rows that see
+ * no key: O = 0, L = -inf).  init = 0: rows that see no key of this chunk are
+ * left untouched (the merge identity).
+ * o_acc: float32 [T_q, H_loc, D] in/out; lse_acc: float32 [H_loc, T_q] in/out.
+ * o_out: optional bf16 [T_q, H_loc, D]; when non-NULL the merged O is also
+ * written there rounded to bf16 (use on the last chunk).  Dummy slots: with
+ * init the accumulators get (0, -inf); o_out gets +0.0.
+ */
+sp_status sp_ring_step(const sp_attn_desc* desc, const void* q, const void* k_chunk,
+                       const void* v_chunk, float* o_acc, float* lse_acc, int32_t init,
+                       void* o_out, void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Standalone log-sum-exp merge of two partial attention results over disjoint
+ * key sets (the ring combine, Section 2.1), in float32:
+ *   L = logaddexp(L_acc, L_part); O_acc = e^(L_acc-L) O_acc + e^(L_part-L) O_part;
+ *   both -inf gives (0, -inf).
+ * o_acc: float32 [T, H, D] in/out; lse_acc: float32 [H, T] in/out.
+ * o_part: [T, H, D], bf16 when o_part_is_bf16 else float32; lse_part: [H, T].
+ * o_out_bf16: optional bf16 [T, H, D] copy of the merged O (RNE), or NULL.
+ * D must be a multiple of 8.
+ */
+sp_status sp_lse_merge(float* o_acc, float* lse_acc, const void* o_part, int32_t o_part_is_bf16,
+                       const float* lse_part, int32_t T, int32_t H, int32_t head_dim,
+                       void* o_out_bf16, void* stream);
+
+/* dst[i] = bf16_rne(src[i]) for i < n (e.g. a ring dQ accumulator). */
+sp_status sp_f32_to_bf16(const float* src, void* dst, int64_t n, void* stream);
+
+/*
+ * Introspection of the block-skip scheduler (host only, no GPU work): the
+ * work items `op` would launch, SP_SCHED_ITEM_INTS int32 each, longest first:
+ *   SP_OP_FWD / SP_OP_RING_STEP (init=1): {q_begin, q_end, k_begin, k_end,
+ *       delta, head, kv_head, 0} -- query rows [q_begin, q_end) of local
+ *       head `head` against keys [k_begin, k_end); causal visibility is
+ *       key <= row + delta.
+ *   SP_OP_BWD, dK/dV items: {k_begin, k_end, q_begin, q_end, delta, head,
+ *       kv_head, 1}.
+ * Writes at most `capacity` items to `items` (may be NULL) and the total
+ * count to *n_items.
+ */
+#define SP_SCHED_ITEM_INTS 8
+sp_status sp_attn_schedule(const sp_attn_desc* desc, int32_t op, int32_t* items, int32_t capacity,
+                           int32_t* n_items);
+
+/*
+ * Opt-in kernel timer (measurement support, per calling thread).  After
+ * sp_profile_events(id, start, stop) with hipEvent_t handles created by the
+ * caller, every launch of kernel `id` made by THIS thread records `start` when
+ * the kernel begins and `stop` when it ends (hipExtLaunchKernelGGL), on the
+ * stream of the call.  If a call launches that kernel more than once, the
+ * events describe the last launch.  Pass NULL events to disarm.  This is the
+ * only state the library keeps (thread-local, no allocation).
+ */
+enum {
+  SP_KERNEL_ATTN_FWD = 1,  /* forward / ring-step attention kernel */
+  SP_KERNEL_ATTN_DQ = 2,   /* backward dQ kernel                     */
+  SP_KERNEL_ATTN_DKDV = 3, /* backward dK/dV kernel                  */
+  SP_KERNEL_PACK = 4,      /* Ulysses pack                           */
+  SP_KERNEL_UNPACK = 5,    /* Ulysses unpack                         */
+  SP_KERNEL_LSE_MERGE = 6  /* standalone LSE merge                   */
+};
+sp_status sp_profile_events(int32_t kernel_id, void* start_event, void* stop_event);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SP_ATTN_H */

@@ -181,7 +181,7 @@ def attn_dkdv_keys(q, k, v, do, keys, **kw):
     need = np.zeros(T_q, dtype=bool)
     for b0 in range(0, T_q, 4096):
         r = np.arange(b0, min(T_q, b0 + 4096))
-        m = allowed_mask(r, seg_q, seg_k, pq, pk, causal)[:, keys]
+        m = allowed_mask(r, seg_q, seg_k[keys], pq, pk[keys], causal)
         need[r] = m.any(axis=1)
     rows = np.nonzero(need)[0]
     for h, kv in local_heads(kw["H_loc"], kw["head_offset"], kw["num_real_heads"],

@@ -1,0 +1,545 @@
+// Host side of the SP attention library: argument validation, the block-skip
+// scheduler, workspace layout and the C ABI declared in include/sp_attn.h.
+//
+// The scheduler replaces full masks (the paper notes the varlen path's
+// overhead, Section 6.3): from cu_seqlens and the segments' position bases it
+// lists one work item per (real head, segment, row tile) -- or per (real
+// head, segment, key tile) for dK/dV -- carrying the tile's visible key (row)
+// range and the causal offset delta (key j visible from row i iff
+// j <= i + delta).  Dummy head slots (Section 4.1) never enter the list.
+// Items are ordered longest first so the hardware dispatcher fills the 256
+// CUs the way longest-processing-time scheduling would.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+#include <vector>
+
+#include "../../include/sp_attn.h"
+#include "launch.h"
+
+namespace {
+
+using spk::kItemInts;
+
+constexpr int64_t kMaxTokens = int64_t(1) << 30;
+
+struct Seg {
+  int qa, qb, ka, kb, delta;
+};
+
+struct Problem {
+  int D = 0;
+  int n_real = 0;  // real local query heads: slots [0, n_real)
+  std::vector<Seg> segs;
+  int q_pad = 0, k_pad = 0;  // first padding row / key
+  std::vector<int> kv_of;    // per real local head
+  std::vector<int> kv_lo, kv_hi;  // per local KV head: real heads [lo, hi) reading it
+  bool direct = true;        // every KV head read by at most one real local head
+  int64_t Tqp = 0, Tkp = 0;  // padded lengths of transposed copies
+};
+
+inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
+
+sp_status validate(const sp_attn_desc* d, Problem& p) {
+  if (!d) return SP_ERR_INVALID_ARG;
+  if (d->reserved != 0) return SP_ERR_INVALID_ARG;
+  if (d->T_q < 0 || d->T_k < 0 || d->T_q >= kMaxTokens || d->T_k >= kMaxTokens)
+    return SP_ERR_INVALID_ARG;
+  if (d->head_dim != 64 && d->head_dim != 128) return SP_ERR_UNSUPPORTED;
+  if (d->H_loc < 1 || d->Hkv_loc < 1 || d->num_padded_heads < 1 || d->num_real_heads < 1 ||
+      d->gqa_group < 1 || d->head_offset < 0 || d->kv_head_offset < 0 || d->num_seqs < 0)
+    return SP_ERR_INVALID_ARG;
+  if (d->Hkv_loc > spk::kMaxKv || d->H_loc > 4096) return SP_ERR_UNSUPPORTED;
+  if (d->num_real_heads > d->num_padded_heads) return SP_ERR_INVALID_ARG;
+  if (d->num_padded_heads % d->H_loc != 0 || d->head_offset % d->H_loc != 0 ||
+      d->head_offset + d->H_loc > d->num_padded_heads)
+    return SP_ERR_INVALID_ARG;
+  const int sp = d->num_padded_heads / d->H_loc;
+  if (d->num_padded_heads - d->num_real_heads >= sp) return SP_ERR_INVALID_ARG;
+  if (d->num_real_heads % d->gqa_group != 0) return SP_ERR_INVALID_ARG;
+  if (!(d->softmax_scale > 0.f) || !std::isfinite(d->softmax_scale)) return SP_ERR_INVALID_ARG;
+  if (d->causal != 0 && d->causal != 1) return SP_ERR_INVALID_ARG;
+
+  p.D = d->head_dim;
+  p.n_real = std::max(0, std::min(d->H_loc, d->num_real_heads - d->head_offset));
+  p.kv_of.resize(p.n_real);
+  p.kv_lo.assign(d->Hkv_loc, 0);
+  p.kv_hi.assign(d->Hkv_loc, 0);
+  std::vector<int> cnt(d->Hkv_loc, 0);
+  for (int y = 0; y < p.n_real; ++y) {
+    int kv = (d->head_offset + y) / d->gqa_group - d->kv_head_offset;
+    if (kv < 0 || kv >= d->Hkv_loc) return SP_ERR_INVALID_ARG;
+    if (y > 0 && kv < p.kv_of[y - 1]) return SP_ERR_INVALID_ARG;  // monotone by construction
+    p.kv_of[y] = kv;
+    if (cnt[kv] == 0) p.kv_lo[kv] = y;
+    p.kv_hi[kv] = y + 1;
+    ++cnt[kv];
+  }
+  p.direct = true;
+  for (int c : cnt)
+    if (c > 1) p.direct = false;
+
+  // segments
+  const int n = d->num_seqs;
+  p.segs.clear();
+  p.q_pad = 0;
+  p.k_pad = 0;
+  if (n > 0) {
+    if (!d->cu_seqlens_q || !d->cu_seqlens_k) return SP_ERR_INVALID_ARG;
+    const int32_t* cq = d->cu_seqlens_q;
+    const int32_t* ck = d->cu_seqlens_k;
+    if (cq[0] != 0 || ck[0] != 0) return SP_ERR_INVALID_ARG;
+    for (int s = 0; s < n; ++s)
+      if (cq[s + 1] < cq[s] || ck[s + 1] < ck[s]) return SP_ERR_INVALID_ARG;
+    if (cq[n] > d->T_q || ck[n] > d->T_k) return SP_ERR_INVALID_ARG;
+    p.q_pad = cq[n];
+    p.k_pad = ck[n];
+    for (int s = 0; s < n; ++s) {
+      Seg g{cq[s], cq[s + 1], ck[s], ck[s + 1], 0};
+      int64_t pq = g.qa, pk = g.ka;  // default: positions restart at 0 per segment
+      if (d->position_ids_q && g.qb > g.qa) {
+        const int32_t* pos = d->position_ids_q;
+        for (int i = g.qa + 1; i < g.qb; ++i)
+          if ((int64_t)pos[i] != (int64_t)pos[i - 1] + 1) return SP_ERR_INVALID_ARG;
+        pq = (int64_t)g.qa - pos[g.qa];
+      }
+      if (d->position_ids_k && g.kb > g.ka) {
+        const int32_t* pos = d->position_ids_k;
+        for (int i = g.ka + 1; i < g.kb; ++i)
+          if ((int64_t)pos[i] != (int64_t)pos[i - 1] + 1) return SP_ERR_INVALID_ARG;
+        pk = (int64_t)g.ka - pos[g.ka];
+      }
+      // key j visible from row i iff pos_k[j] <= pos_q[i]
+      //   <=> j - pk <= i - pq  <=>  j <= i + (pk - pq)
+      int64_t delta = pk - pq;
+      if (delta > (int64_t(1) << 30) || delta < -(int64_t(1) << 30)) return SP_ERR_INVALID_ARG;
+      g.delta = (int)delta;
+      p.segs.push_back(g);
+    }
+  }
+  p.Tqp = round_up(std::max(d->T_q, 1), 8) + spk::kTransposePad;
+  p.Tkp = round_up(std::max(d->T_k, 1), 8) + spk::kTransposePad;
+  return SP_OK;
+}
+
+struct Item {
+  int v[kItemInts];
+  int64_t cost;
+};
+
+void sort_items(std::vector<Item>& items, std::vector<int32_t>& out) {
+  std::stable_sort(items.begin(), items.end(),
+                   [](const Item& a, const Item& b) { return a.cost > b.cost; });
+  out.resize(items.size() * kItemInts);
+  for (size_t i = 0; i < items.size(); ++i)
+    std::memcpy(&out[i * kItemInts], items[i].v, sizeof(int) * kItemInts);
+}
+
+// Row-tile items (forward, ring step, dQ).
+void schedule_rows(const sp_attn_desc* d, const Problem& p, int BM, int BN, bool include_empty,
+                   std::vector<int32_t>& out) {
+  std::vector<Item> items;
+  for (int y = 0; y < p.n_real; ++y) {
+    for (const Seg& g : p.segs) {
+      for (int a = g.qa; a < g.qb; a += BM) {
+        const int b = std::min(a + BM, g.qb);
+        int k1 = g.kb;
+        if (d->causal) k1 = (int)std::min<int64_t>(g.kb, (int64_t)b + g.delta);
+        const int k0 = g.ka;
+        const bool empty = k1 <= k0;
+        if (empty && !include_empty) continue;
+        Item it{{a, b, k0, empty ? k0 : k1, g.delta, y, p.kv_of[y], 0}, 0};
+        it.cost = empty ? 0 : (int64_t)((k1 - (k0 & ~7)) + BN - 1) / BN;
+        items.push_back(it);
+      }
+    }
+    if (include_empty)
+      for (int a = p.q_pad; a < d->T_q; a += BM)
+        items.push_back(Item{{a, std::min(a + BM, d->T_q), 0, 0, 0, y, p.kv_of[y], 0}, 0});
+  }
+  sort_items(items, out);
+}
+
+// Key-tile items (dK / dV).  Every key of every real head gets exactly one item.
+void schedule_keys(const sp_attn_desc* d, const Problem& p, int BNK, int BQ,
+                   std::vector<int32_t>& out) {
+  std::vector<Item> items;
+  for (int y = 0; y < p.n_real; ++y) {
+    for (const Seg& g : p.segs) {
+      for (int a = g.ka; a < g.kb; a += BNK) {
+        const int b = std::min(a + BNK, g.kb);
+        int q0 = g.qa;
+        if (d->causal) q0 = (int)std::max<int64_t>(g.qa, (int64_t)a - g.delta);
+        const bool empty = q0 >= g.qb;
+        Item it{{a, b, empty ? g.qb : q0, g.qb, g.delta, y, p.kv_of[y], 1}, 0};
+        it.cost = empty ? 0 : (int64_t)((g.qb - (q0 & ~7)) + BQ - 1) / BQ;
+        items.push_back(it);
+      }
+    }
+    for (int a = p.k_pad; a < d->T_k; a += BNK)
+      items.push_back(Item{{a, std::min(a + BNK, d->T_k), 0, 0, 0, y, p.kv_of[y], 1}, 0});
+  }
+  sort_items(items, out);
+}
+
+// Workspace layout.
+struct Layout {
+  size_t items_dq = 0, items_kv = 0, vt = 0, delta = 0, qt = 0, dot = 0, kt = 0, part_k = 0,
+         part_v = 0, total = 0;
+};
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+Layout layout_for(const sp_attn_desc* d, const Problem& p, int op, size_t n_items_a,
+                  size_t n_items_b) {
+  Layout L;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    size_t o = off;
+    off = align256(off + bytes);
+    return o;
+  };
+  const size_t D = p.D;
+  if (op == SP_OP_FWD || op == SP_OP_RING_STEP) {
+    L.items_dq = take(n_items_a * kItemInts * 4);
+    L.vt = take((size_t)d->Hkv_loc * D * p.Tkp * 2);
+  } else {
+    L.items_dq = take(n_items_a * kItemInts * 4);
+    L.items_kv = take(n_items_b * kItemInts * 4);
+    L.delta = take((size_t)std::max(p.n_real, 1) * d->T_q * 4);
+    L.qt = take((size_t)std::max(p.n_real, 1) * D * p.Tqp * 2);
+    L.dot = take((size_t)std::max(p.n_real, 1) * D * p.Tqp * 2);
+    L.kt = take((size_t)d->Hkv_loc * D * p.Tkp * 2);
+    if (!p.direct) {
+      L.part_k = take((size_t)p.n_real * d->T_k * D * 4);
+      L.part_v = take((size_t)p.n_real * d->T_k * D * 4);
+    }
+  }
+  L.total = std::max<size_t>(off, 256);
+  return L;
+}
+
+// Worst-case item counts (with empty items) for sizing.
+void item_counts(const sp_attn_desc* d, const Problem& p, int op, size_t& a, size_t& b) {
+  std::vector<int32_t> tmp;
+  if (op == SP_OP_BWD) {
+    schedule_rows(d, p, spk::kDqBM, spk::kDqBN, true, tmp);
+    a = tmp.size() / kItemInts;
+    schedule_keys(d, p, spk::kDkdvBN, spk::kDkdvBQ, tmp);
+    b = tmp.size() / kItemInts;
+  } else {
+    schedule_rows(d, p, spk::kFwdBM, spk::kFwdBN, true, tmp);
+    a = tmp.size() / kItemInts;
+    b = 0;
+  }
+}
+
+inline bool aligned16(const void* ptr) { return ((uintptr_t)ptr & 15u) == 0; }
+
+#define SP_HIP(call)                          \
+  do {                                        \
+    if ((call) != hipSuccess) return SP_ERR_HIP; \
+  } while (0)
+
+sp_status upload(void* dst, const std::vector<int32_t>& v, hipStream_t st) {
+  if (v.empty()) return SP_OK;
+  SP_HIP(hipMemcpyAsync(dst, v.data(), v.size() * sizeof(int32_t), hipMemcpyHostToDevice, st));
+  return SP_OK;
+}
+
+sp_status check_ws(const Layout& L, void* ws, size_t ws_bytes) {
+  if (!ws || ws_bytes < L.total || ((uintptr_t)ws & 255u) != 0) return SP_ERR_WORKSPACE;
+  return SP_OK;
+}
+
+char* at(void* ws, size_t off) { return (char*)ws + off; }
+
+// Zero dummy query slots and give them LSE -inf.
+sp_status fill_dummies_fwd(const sp_attn_desc* d, const Problem& p, void* o, float* lse,
+                           hipStream_t st) {
+  if (p.n_real >= d->H_loc) return SP_OK;
+  if (o) SP_HIP(spk::launch_zero_heads_bf16(o, d->T_q, d->H_loc, p.D, p.n_real, d->H_loc, st));
+  if (lse)
+    SP_HIP(spk::launch_fill_f32(lse + (size_t)p.n_real * d->T_q,
+                                (int64_t)(d->H_loc - p.n_real) * d->T_q, -INFINITY, st));
+  return SP_OK;
+}
+
+}  // namespace
+
+namespace spk {
+KernelTimer& timer_for(int kernel_id) {
+  static thread_local KernelTimer slots[kKCount];
+  return slots[(kernel_id > 0 && kernel_id < kKCount) ? kernel_id : 0];
+}
+}  // namespace spk
+
+extern "C" {
+
+sp_status sp_profile_events(int32_t kernel_id, void* start_event, void* stop_event) {
+  if (kernel_id < 1 || kernel_id >= spk::kKCount) return SP_ERR_INVALID_ARG;
+  spk::KernelTimer& t = spk::timer_for(kernel_id);
+  t.start = (hipEvent_t)start_event;
+  t.stop = (hipEvent_t)stop_event;
+  return SP_OK;
+}
+
+const char* sp_status_string(sp_status s) {
+  switch (s) {
+    case SP_OK: return "ok";
+    case SP_ERR_INVALID_ARG: return "invalid argument";
+    case SP_ERR_UNSUPPORTED: return "unsupported configuration";
+    case SP_ERR_WORKSPACE: return "workspace missing, misaligned or too small";
+    case SP_ERR_HIP: return "HIP launch or copy failed";
+  }
+  return "unknown status";
+}
+
+int32_t sp_version(void) { return 100; }
+
+sp_status sp_ulysses_pack(const void* src, int32_t T_loc, int32_t H_src, int32_t head_dim,
+                          int32_t sp, int32_t H_dst_loc, const int32_t* head_map, void* dst,
+                          void* stream) {
+  if (T_loc < 0 || H_src < 1 || head_dim < 8 || head_dim % 8 != 0 || sp < 1 || H_dst_loc < 1 ||
+      !head_map)
+    return SP_ERR_INVALID_ARG;
+  if ((int64_t)sp * H_dst_loc > spk::kMaxMap) return SP_ERR_UNSUPPORTED;
+  spk::PackArgs a;
+  a.sp = sp; a.T = T_loc; a.Hs = H_src; a.Hd = H_dst_loc; a.nch = head_dim / 8;
+  for (int i = 0; i < sp * H_dst_loc; ++i) {
+    if (head_map[i] < -1 || head_map[i] >= H_src) return SP_ERR_INVALID_ARG;
+    a.map[i] = head_map[i];
+  }
+  if (T_loc == 0) return SP_OK;
+  if (!src || !dst || !aligned16(src) || !aligned16(dst)) return SP_ERR_INVALID_ARG;
+  SP_HIP(spk::launch_pack(src, dst, a, (hipStream_t)stream));
+  return SP_OK;
+}
+
+sp_status sp_ulysses_unpack(const void* src, int32_t T_loc, int32_t H_src_loc, int32_t head_dim,
+                            int32_t sp, const int32_t* head_map, int32_t H_dst, void* dst,
+                            void* stream) {
+  if (T_loc < 0 || H_src_loc < 1 || head_dim < 8 || head_dim % 8 != 0 || sp < 1 || H_dst < 1 ||
+      !head_map)
+    return SP_ERR_INVALID_ARG;
+  if ((int64_t)sp * H_src_loc > spk::kMaxMap || H_dst > spk::kMaxMap) return SP_ERR_UNSUPPORTED;
+  spk::PackArgs a;
+  a.sp = sp; a.T = T_loc; a.Hs = H_src_loc; a.Hd = H_dst; a.nch = head_dim / 8;
+  std::vector<int> seen(H_dst, 0);
+  for (int i = 0; i < sp * H_src_loc; ++i) {
+    int g = head_map[i];
+    if (g < -1 || g >= H_dst) return SP_ERR_INVALID_ARG;
+    if (g >= 0) {
+      if (seen[g]++) return SP_ERR_INVALID_ARG;
+      a.map[g] = i;  // inverse map: dest head -> j*H_src_loc + h
+    }
+  }
+  for (int g = 0; g < H_dst; ++g)
+    if (seen[g] != 1) return SP_ERR_INVALID_ARG;
+  if (T_loc == 0) return SP_OK;
+  if (!src || !dst || !aligned16(src) || !aligned16(dst)) return SP_ERR_INVALID_ARG;
+  SP_HIP(spk::launch_unpack(src, dst, a, (hipStream_t)stream));
+  return SP_OK;
+}
+
+sp_status sp_attn_workspace_size(const sp_attn_desc* desc, int32_t op, size_t* bytes) {
+  if (!bytes) return SP_ERR_INVALID_ARG;
+  if (op != SP_OP_FWD && op != SP_OP_BWD && op != SP_OP_RING_STEP) return SP_ERR_INVALID_ARG;
+  Problem p;
+  sp_status s = validate(desc, p);
+  if (s != SP_OK) return s;
+  size_t a = 0, b = 0;
+  item_counts(desc, p, op, a, b);
+  *bytes = layout_for(desc, p, op, a, b).total;
+  return SP_OK;
+}
+
+sp_status sp_attn_schedule(const sp_attn_desc* desc, int32_t op, int32_t* items, int32_t capacity,
+                           int32_t* n_items) {
+  if (!n_items || capacity < 0) return SP_ERR_INVALID_ARG;
+  Problem p;
+  sp_status s = validate(desc, p);
+  if (s != SP_OK) return s;
+  std::vector<int32_t> v;
+  if (op == SP_OP_FWD || op == SP_OP_RING_STEP)
+    schedule_rows(desc, p, spk::kFwdBM, spk::kFwdBN, true, v);
+  else if (op == SP_OP_BWD)
+    schedule_keys(desc, p, spk::kDkdvBN, spk::kDkdvBQ, v);
+  else
+    return SP_ERR_INVALID_ARG;
+  const int32_t n = (int32_t)(v.size() / kItemInts);
+  *n_items = n;
+  if (items) std::memcpy(items, v.data(), sizeof(int32_t) * kItemInts * std::min(n, capacity));
+  return SP_OK;
+}
+
+static sp_status fwd_common(const sp_attn_desc* d, const void* q, const void* k, const void* v,
+                            void* o, float* lse, float* o_acc, float* lse_acc, int init,
+                            void* o_out, void* ws, size_t ws_bytes, void* stream, bool ring) {
+  Problem p;
+  sp_status s = validate(d, p);
+  if (s != SP_OK) return s;
+  if (!q || !k || !v) return SP_ERR_INVALID_ARG;
+  if (ring ? (!o_acc || !lse_acc) : (!o || !lse)) return SP_ERR_INVALID_ARG;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || (o && !aligned16(o)) ||
+      (o_acc && !aligned16(o_acc)) || (o_out && !aligned16(o_out)))
+    return SP_ERR_INVALID_ARG;
+  if (init != 0 && init != 1) return SP_ERR_INVALID_ARG;
+  const bool include_empty = !ring || init || o_out;
+  std::vector<int32_t> items;
+  schedule_rows(d, p, spk::kFwdBM, spk::kFwdBN, include_empty, items);
+  size_t na = 0, nb = 0;
+  item_counts(d, p, SP_OP_FWD, na, nb);
+  Layout L = layout_for(d, p, ring ? SP_OP_RING_STEP : SP_OP_FWD, na, nb);
+  if ((s = check_ws(L, ws, ws_bytes)) != SP_OK) return s;
+  hipStream_t st = (hipStream_t)stream;
+  const int n_items = (int)(items.size() / kItemInts);
+  if (n_items > 0) {
+    if ((s = upload(at(ws, L.items_dq), items, st)) != SP_OK) return s;
+    SP_HIP(spk::launch_transpose(v, at(ws, L.vt), d->T_k, (int)p.Tkp, d->Hkv_loc, 0, d->Hkv_loc,
+                                 p.D, st));
+    spk::FwdArgs a{};
+    a.q = (const uint16_t*)q;
+    a.k = (const uint16_t*)k;
+    a.vt = (const uint16_t*)at(ws, L.vt);
+    a.o = (uint16_t*)o;
+    a.lse = lse;
+    a.o_acc = o_acc;
+    a.lse_acc = lse_acc;
+    a.o_out = (uint16_t*)o_out;
+    a.items = (const int32_t*)at(ws, L.items_dq);
+    a.T_q = d->T_q; a.T_k = d->T_k; a.Tkp = (int)p.Tkp; a.H = d->H_loc; a.Hkv = d->Hkv_loc;
+    a.scale_log2 = d->softmax_scale * 1.4426950408889634f;
+    a.causal = d->causal;
+    a.init = init;
+    SP_HIP(spk::launch_attn_fwd(a, n_items, p.D, ring, st));
+  }
+  if (!ring) return fill_dummies_fwd(d, p, o, lse, st);
+  if (p.n_real < d->H_loc) {
+    if (init) {
+      SP_HIP(spk::launch_zero_heads_f32(o_acc, d->T_q, d->H_loc, p.D, p.n_real, d->H_loc, st));
+      SP_HIP(spk::launch_fill_f32(lse_acc + (size_t)p.n_real * d->T_q,
+                                  (int64_t)(d->H_loc - p.n_real) * d->T_q, -INFINITY, st));
+    }
+    if (o_out)
+      SP_HIP(spk::launch_zero_heads_bf16(o_out, d->T_q, d->H_loc, p.D, p.n_real, d->H_loc, st));
+  }
+  return SP_OK;
+}
+
+sp_status sp_attn_fwd(const sp_attn_desc* desc, const void* q, const void* k, const void* v,
+                      void* o, float* lse, void* workspace, size_t workspace_bytes,
+                      void* stream) {
+  return fwd_common(desc, q, k, v, o, lse, nullptr, nullptr, 1, nullptr, workspace,
+                    workspace_bytes, stream, false);
+}
+
+sp_status sp_ring_step(const sp_attn_desc* desc, const void* q, const void* k_chunk,
+                       const void* v_chunk, float* o_acc, float* lse_acc, int32_t init,
+                       void* o_out, void* workspace, size_t workspace_bytes, void* stream) {
+  return fwd_common(desc, q, k_chunk, v_chunk, nullptr, nullptr, o_acc, lse_acc, init, o_out,
+                    workspace, workspace_bytes, stream, true);
+}
+
+sp_status sp_attn_bwd(const sp_attn_desc* d, const void* q, const void* k, const void* v,
+                      const void* o, const float* lse, const void* dout, void* dq,
+                      float* dq_acc, void* dk, void* dv, void* ws, size_t ws_bytes,
+                      void* stream) {
+  Problem p;
+  sp_status s = validate(d, p);
+  if (s != SP_OK) return s;
+  if (!q || !k || !v || !o || !lse || !dout || !dk || !dv) return SP_ERR_INVALID_ARG;
+  if ((dq == nullptr) == (dq_acc == nullptr)) return SP_ERR_INVALID_ARG;
+  for (const void* ptr : {q, k, v, o, dout, (const void*)dk, (const void*)dv})
+    if (!aligned16(ptr)) return SP_ERR_INVALID_ARG;
+  if ((dq && !aligned16(dq)) || (dq_acc && !aligned16(dq_acc))) return SP_ERR_INVALID_ARG;
+  std::vector<int32_t> it_dq, it_kv;
+  schedule_rows(d, p, spk::kDqBM, spk::kDqBN, true, it_dq);
+  schedule_keys(d, p, spk::kDkdvBN, spk::kDkdvBQ, it_kv);
+  const size_t na = it_dq.size() / kItemInts, nb = it_kv.size() / kItemInts;
+  Layout L = layout_for(d, p, SP_OP_BWD, na, nb);
+  if ((s = check_ws(L, ws, ws_bytes)) != SP_OK) return s;
+  hipStream_t st = (hipStream_t)stream;
+  const int D = p.D;
+  if (p.n_real > 0) {
+    if ((s = upload(at(ws, L.items_dq), it_dq, st)) != SP_OK) return s;
+    if ((s = upload(at(ws, L.items_kv), it_kv, st)) != SP_OK) return s;
+    float* delta = (float*)at(ws, L.delta);
+    SP_HIP(spk::launch_rowdot(o, dout, delta, d->T_q, d->H_loc, p.n_real, D, st));
+    SP_HIP(spk::launch_transpose(q, at(ws, L.qt), d->T_q, (int)p.Tqp, d->H_loc, 0, p.n_real, D, st));
+    SP_HIP(spk::launch_transpose(dout, at(ws, L.dot), d->T_q, (int)p.Tqp, d->H_loc, 0, p.n_real, D,
+                                 st));
+    SP_HIP(spk::launch_transpose(k, at(ws, L.kt), d->T_k, (int)p.Tkp, d->Hkv_loc, 0, d->Hkv_loc, D,
+                                 st));
+    const float sl2 = d->softmax_scale * 1.4426950408889634f;
+    spk::DqArgs a{};
+    a.q = (const uint16_t*)q; a.k = (const uint16_t*)k; a.v = (const uint16_t*)v;
+    a.kt = (const uint16_t*)at(ws, L.kt); a.dout = (const uint16_t*)dout;
+    a.lse = lse; a.delta = delta; a.dq = (uint16_t*)dq; a.dq_acc = dq_acc;
+    a.items = (const int32_t*)at(ws, L.items_dq);
+    a.T_q = d->T_q; a.T_k = d->T_k; a.Tkp = (int)p.Tkp; a.H = d->H_loc; a.Hkv = d->Hkv_loc;
+    a.scale_log2 = sl2; a.scale = d->softmax_scale; a.causal = d->causal;
+    SP_HIP(spk::launch_attn_dq(a, (int)na, D, st));
+
+    spk::DkdvArgs b{};
+    b.q = (const uint16_t*)q; b.qt = (const uint16_t*)at(ws, L.qt);
+    b.dout = (const uint16_t*)dout; b.dot = (const uint16_t*)at(ws, L.dot);
+    b.lse = lse; b.delta = delta; b.k = (const uint16_t*)k; b.v = (const uint16_t*)v;
+    b.dk = (uint16_t*)dk; b.dv = (uint16_t*)dv;
+    b.part_k = p.direct ? nullptr : (float*)at(ws, L.part_k);
+    b.part_v = p.direct ? nullptr : (float*)at(ws, L.part_v);
+    b.items = (const int32_t*)at(ws, L.items_kv);
+    b.T_q = d->T_q; b.T_k = d->T_k; b.Tqp = (int)p.Tqp; b.H = d->H_loc; b.Hkv = d->Hkv_loc;
+    b.scale_log2 = sl2; b.scale = d->softmax_scale; b.causal = d->causal; b.direct = p.direct;
+    SP_HIP(spk::launch_attn_dkdv(b, (int)nb, D, st));
+    if (!p.direct) {
+      spk::ReduceArgs r{};
+      r.T = d->T_k; r.Hkv = d->Hkv_loc; r.D = D;
+      for (int kv = 0; kv < d->Hkv_loc; ++kv) {
+        r.head_lo[kv] = p.kv_lo[kv];
+        r.head_hi[kv] = p.kv_hi[kv];
+      }
+      SP_HIP(spk::launch_reduce_kv(b.part_k, dk, r, st));
+      SP_HIP(spk::launch_reduce_kv(b.part_v, dv, r, st));
+    }
+  }
+  // KV heads read by no real query head get zero gradients.
+  if (p.direct || p.n_real == 0) {
+    for (int kv = 0; kv < d->Hkv_loc; ++kv)
+      if (p.n_real == 0 || p.kv_hi[kv] == p.kv_lo[kv]) {
+        SP_HIP(spk::launch_zero_heads_bf16(dk, d->T_k, d->Hkv_loc, D, kv, kv + 1, st));
+        SP_HIP(spk::launch_zero_heads_bf16(dv, d->T_k, d->Hkv_loc, D, kv, kv + 1, st));
+      }
+  }
+  if (dq && p.n_real < d->H_loc)
+    SP_HIP(spk::launch_zero_heads_bf16(dq, d->T_q, d->H_loc, D, p.n_real, d->H_loc, st));
+  return SP_OK;
+}
+
+sp_status sp_lse_merge(float* o_acc, float* lse_acc, const void* o_part, int32_t o_part_is_bf16,
+                       const float* lse_part, int32_t T, int32_t H, int32_t head_dim,
+                       void* o_out_bf16, void* stream) {
+  if (T < 0 || H < 1 || head_dim < 8 || head_dim > 512 || (head_dim & (head_dim - 1)) != 0)
+    return SP_ERR_INVALID_ARG;
+  if (o_part_is_bf16 != 0 && o_part_is_bf16 != 1) return SP_ERR_INVALID_ARG;
+  if (T == 0) return SP_OK;
+  if (!o_acc || !lse_acc || !o_part || !lse_part) return SP_ERR_INVALID_ARG;
+  if (!aligned16(o_acc) || !aligned16(o_part) || (o_out_bf16 && !aligned16(o_out_bf16)))
+    return SP_ERR_INVALID_ARG;
+  SP_HIP(spk::launch_merge(o_acc, lse_acc, o_part, o_part_is_bf16 != 0, lse_part, T, H, head_dim,
+                           o_out_bf16, (hipStream_t)stream));
+  return SP_OK;
+}
+
+sp_status sp_f32_to_bf16(const float* src, void* dst, int64_t n, void* stream) {
+  if (n < 0) return SP_ERR_INVALID_ARG;
+  if (n == 0) return SP_OK;
+  if (!src || !dst || !aligned16(src) || !aligned16(dst)) return SP_ERR_INVALID_ARG;
+  SP_HIP(spk::launch_f32_to_bf16(src, dst, n, (hipStream_t)stream));
+  return SP_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,68 @@
+// Device-side helpers shared by the gfx950 kernels of the SP attention library.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+#define SP_DEV __device__ __forceinline__
+
+static constexpr float kLog2e = 1.4426950408889634f;
+static constexpr float kLn2 = 0.6931471805599453f;
+
+SP_DEV float neg_inf() { return -__builtin_inff(); }
+
+// 32x32x16 bf16 MFMA (fp32 accumulate).  Operand layouts (verified on gfx950):
+//   A (32 x 16): lane l holds row l%32, k = (l/32)*8 + [0..7]
+//   B (16 x 32): lane l holds col l%32, k = (l/32)*8 + [0..7]
+//   C (32 x 32): lane l holds col l%32, register r is row (r/4)*8 + (l/32)*4 + r%4
+SP_DEV f32x16 mfma32(const u32x4& a, const u32x4& b, const f32x16& c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
+                                                  __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+}
+
+// Round 8 floats to bf16 (RNE, v_cvt_pk_bf16_f32) and pack into 16 bytes.
+SP_DEV u32x4 pack_bf16x8(float a0, float a1, float a2, float a3, float a4, float a5, float a6,
+                         float a7) {
+  f32x8 v = {a0, a1, a2, a3, a4, a5, a6, a7};
+  return __builtin_bit_cast(u32x4, __builtin_convertvector(v, bf16x8));
+}
+SP_DEV u32x2 pack_bf16x4(float a0, float a1, float a2, float a3) {
+  f32x4 v = {a0, a1, a2, a3};
+  return __builtin_bit_cast(u32x2, __builtin_convertvector(v, bf16x4));
+}
+SP_DEV float bf16_to_f32(uint16_t b) { return __uint_as_float(((uint32_t)b) << 16); }
+
+// Row permutation used for MFMA A operands whose C result feeds a later MFMA as
+// a B operand: A row m is loaded from physical row perm32(m) so that, in the C
+// layout, lane half h of register block r/8 holds the 8 consecutive physical
+// rows (r/8)*16 + h*8 + [0..7] -- exactly a B operand's k-slice.
+SP_DEV int perm32(int m) { return ((m >> 4) << 4) | (((m >> 2) & 1) << 3) | (((m >> 3) & 1) << 2) | (m & 3); }
+
+// Physical index (row or key) held by C register r of lane half h after an
+// A operand loaded with perm32 rows.
+SP_DEV int c_row_of(int r, int h) { return ((r >> 3) << 4) + (h << 3) + (r & 7); }
+
+// XOR swizzle of 16-byte chunks inside an LDS tile row, so that 8 lanes that
+// read the same logical chunk of 8 different rows hit distinct banks.
+// `nch` = 16-byte chunks per row (8 or 16).
+template <int NCH>
+SP_DEV int swz(int row, int chunk) {
+  if constexpr (NCH >= 16) {
+    return row * NCH + (chunk ^ (row & 15));
+  } else {
+    // two 128-byte rows share one 256-byte bank window
+    return row * NCH + (chunk ^ ((row >> 1) & 7));
+  }
+}
+
+SP_DEV float wave_max_xor32(float x) { return fmaxf(x, __shfl_xor(x, 32)); }
+SP_DEV float wave_sum_xor32(float x) { return x + __shfl_xor(x, 32); }

@@ -1,0 +1,247 @@
+// Attention forward for one SP rank's real heads on gfx950.
+//
+// One workgroup = 4 wavefronts = 128 query rows of one head (a work item from
+// the host block-skip scheduler); wavefront w owns rows q_begin + 32w ..
+// +32.  The key loop walks 64-key tiles of the segment, staged in LDS
+// (K row-major, V transposed) with double buffering and register
+// prefetch of the next tile.
+//
+// Per 64-key tile and wavefront:
+//   S^T = K Q^T      (32x32x16 bf16 MFMA; Q^T kept in registers as B operand)
+//   online softmax   (fp32; the 32x32 C layout gives each lane one query row,
+//                     16 keys per tile half; the row max needs one exchange
+//                     with lane l^32)
+//   O^T += V^T P^T   (P^T from the C registers directly: K rows are loaded in
+//                     perm32 order so each lane half's C registers are 8
+//                     consecutive keys, i.e. a B operand k-slice)
+// The running max is only raised when it grows by more than 2^8 (exact:
+// the final normalisation uses the same max).  Masking is evaluated only on
+// tiles that straddle a segment edge or the causal diagonal.
+//
+// The ring variant (MERGE) folds the chunk's normalised (O_c, LSE_c) into
+// float32 accumulators with the log-sum-exp rule in the epilogue.
+#include "dev_common.h"
+#include "launch.h"
+
+namespace spk {
+
+namespace {
+
+constexpr int BM = kFwdBM;  // 128 rows per workgroup
+constexpr int BN = kFwdBN;  // 64 keys per tile
+constexpr int NT = 256;
+
+template <int D, bool MERGE>
+__global__ __launch_bounds__(NT, 2) void attn_fwd_kernel(FwdArgs a) {
+  constexpr int KS = D / 16;   // MFMA k-steps over D
+  constexpr int DB = D / 32;   // 32-dim blocks of O^T
+  constexpr int KCH = D / 8;   // 16-byte chunks per K row
+  constexpr int VCH = BN / 8;  // 16-byte chunks per V^T row
+  constexpr int KLD = BN * KCH / NT;
+  constexpr int VLD = D * VCH / NT;
+  static_assert(KLD * NT == BN * KCH && VLD * NT == D * VCH, "tile/threads mismatch");
+
+  __shared__ u32x4 sK[2][BN * KCH];
+  __shared__ u32x4 sV[2][D * VCH];
+
+  const int32_t* it = a.items + (int64_t)blockIdx.x * kItemInts;
+  const int q0 = it[0], q1 = it[1], k0 = it[2], k1 = it[3], delta = it[4], head = it[5],
+            kvh = it[6];
+  const int tid = threadIdx.x;
+  const int w = tid >> 6, lane = tid & 63, hh = lane >> 5, l32 = lane & 31;
+  const int row = q0 + w * 32 + l32;
+  const bool row_ok = row < q1;
+
+  // Q^T as B operand: lane holds query row `row`, dims ks*16 + hh*8 + [0..7].
+  u32x4 qf[KS];
+  {
+    const uint16_t* qp = a.q + ((int64_t)(row_ok ? row : q0) * a.H + head) * D + hh * 8;
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      qf[s] = *(const u32x4*)(qp + s * 16);
+      if (!row_ok) qf[s] = u32x4{0u, 0u, 0u, 0u};
+    }
+  }
+
+  f32x16 oacc[DB];
+#pragma unroll
+  for (int d = 0; d < DB; ++d)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) oacc[d][r] = 0.f;
+  float m_run = neg_inf(), l_part = 0.f;
+  const float c2 = a.scale_log2;
+
+  const int kt_first = k0 & ~7;
+  const int n_tiles = (k1 > k0) ? (k1 - kt_first + BN - 1) / BN : 0;
+
+  u32x4 stK[KLD], stV[VLD];
+  auto load_tile = [&](int kt) {
+#pragma unroll
+    for (int i = 0; i < KLD; ++i) {
+      int c = tid + i * NT;
+      int r = c / KCH, cc = c % KCH;
+      int key = kt + r;
+      stK[i] = u32x4{0u, 0u, 0u, 0u};
+      if (key < k1) stK[i] = *(const u32x4*)(a.k + ((int64_t)key * a.Hkv + kvh) * D + cc * 8);
+    }
+#pragma unroll
+    for (int i = 0; i < VLD; ++i) {
+      int c = tid + i * NT;
+      int d = c / VCH, cc = c % VCH;
+      stV[i] = *(const u32x4*)(a.vt + ((int64_t)kvh * D + d) * a.Tkp + kt + cc * 8);
+    }
+  };
+  auto store_tile = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < KLD; ++i) {
+      int c = tid + i * NT;
+      sK[buf][swz<KCH>(c / KCH, c % KCH)] = stK[i];
+    }
+#pragma unroll
+    for (int i = 0; i < VLD; ++i) {
+      int c = tid + i * NT;
+      sV[buf][swz<VCH>(c / VCH, c % VCH)] = stV[i];
+    }
+  };
+
+  if (n_tiles > 0) {
+    load_tile(kt_first);
+    store_tile(0);
+  }
+  __syncthreads();
+
+  const int prow = perm32(l32);
+  int buf = 0;
+  for (int n = 0; n < n_tiles; ++n) {
+    const int kt = kt_first + n * BN;
+    if (n + 1 < n_tiles) load_tile(kt + BN);
+
+    // ---- S^T = K Q^T for the two 32-key halves of the tile
+    f32x16 s[2];
+#pragma unroll
+    for (int g = 0; g < 2; ++g) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) s[g][r] = 0.f;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        u32x4 af = sK[buf][swz<KCH>(g * 32 + prow, ks * 2 + hh)];
+        s[g] = mfma32(af, qf[ks], s[g]);
+      }
+    }
+
+    // ---- mask (only on edge / diagonal tiles)
+    const bool need_mask = (kt < k0) || (kt + BN > k1) || (a.causal && kt + BN - 1 > q0 + delta);
+    if (need_mask) {
+#pragma unroll
+      for (int g = 0; g < 2; ++g)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          int key = kt + g * 32 + c_row_of(r, hh);
+          bool ok = key >= k0 && key < k1 && (!a.causal || key <= row + delta);
+          if (!ok) s[g][r] = neg_inf();
+        }
+    }
+
+    // ---- online softmax (lazy rescale)
+    float mx = neg_inf();
+#pragma unroll
+    for (int g = 0; g < 2; ++g)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[g][r]);
+    mx = wave_max_xor32(mx);
+    const float m_new = fmaxf(m_run, mx);
+    const bool need = (m_new - m_run) * c2 > 8.f;  // NaN (both -inf) -> false
+    if (__ballot(need)) {
+      float alpha = need ? exp2f((m_run - m_new) * c2) : 1.f;
+      if (need) m_run = m_new;
+      l_part *= alpha;
+#pragma unroll
+      for (int d = 0; d < DB; ++d)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) oacc[d][r] *= alpha;
+    }
+    const float msc = (m_run == neg_inf()) ? 0.f : m_run * c2;
+    u32x4 pb[4];
+#pragma unroll
+    for (int g = 0; g < 2; ++g) {
+      float p[16];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        p[r] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[g][r], c2, -msc));
+        l_part += p[r];
+      }
+      pb[2 * g] = pack_bf16x8(p[0], p[1], p[2], p[3], p[4], p[5], p[6], p[7]);
+      pb[2 * g + 1] = pack_bf16x8(p[8], p[9], p[10], p[11], p[12], p[13], p[14], p[15]);
+    }
+
+    // ---- O^T += V^T P^T
+#pragma unroll
+    for (int d = 0; d < DB; ++d)
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) {
+        u32x4 af = sV[buf][swz<VCH>(d * 32 + l32, ks * 2 + hh)];
+        oacc[d] = mfma32(af, pb[ks], oacc[d]);
+      }
+
+    if (n + 1 < n_tiles) store_tile(buf ^ 1);
+    __syncthreads();
+    buf ^= 1;
+  }
+
+  // ---- epilogue
+  const float l_tot = wave_sum_xor32(l_part);
+  const bool has = l_tot > 0.f;
+  const float inv = has ? 1.f / l_tot : 0.f;
+  const float lse_v = has ? (m_run * c2 + __log2f(l_tot)) * kLn2 : neg_inf();
+  if (!row_ok) return;
+  const int64_t obase = ((int64_t)row * a.H + head) * D + hh * 4;
+  if constexpr (!MERGE) {
+#pragma unroll
+    for (int d = 0; d < DB; ++d)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        u32x2 v = pack_bf16x4(oacc[d][j * 4] * inv, oacc[d][j * 4 + 1] * inv,
+                              oacc[d][j * 4 + 2] * inv, oacc[d][j * 4 + 3] * inv);
+        *(u32x2*)(a.o + obase + d * 32 + j * 8) = v;
+      }
+    if (hh == 0) a.lse[(int64_t)head * a.T_q + row] = lse_v;
+  } else {
+    const int64_t li = (int64_t)head * a.T_q + row;
+    const float la = a.init ? neg_inf() : a.lse_acc[li];
+    float wa = 0.f, wb = 0.f, L = neg_inf();
+    const float m = fmaxf(la, lse_v);
+    if (m != neg_inf()) {
+      float ea = __expf(la - m), eb = __expf(lse_v - m);
+      float ssum = ea + eb;
+      L = m + __logf(ssum);
+      wa = ea / ssum;
+      wb = eb / ssum * inv;  // folds the chunk's 1/l normalisation
+    }
+#pragma unroll
+    for (int d = 0; d < DB; ++d)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        float4* po = (float4*)(a.o_acc + obase + d * 32 + j * 8);
+        float4 old = a.init ? make_float4(0.f, 0.f, 0.f, 0.f) : *po;
+        float4 nv = make_float4(wa * old.x + wb * oacc[d][j * 4], wa * old.y + wb * oacc[d][j * 4 + 1],
+                                wa * old.z + wb * oacc[d][j * 4 + 2], wa * old.w + wb * oacc[d][j * 4 + 3]);
+        *po = nv;
+        if (a.o_out) *(u32x2*)(a.o_out + obase + d * 32 + j * 8) = pack_bf16x4(nv.x, nv.y, nv.z, nv.w);
+      }
+    if (hh == 0) a.lse_acc[li] = L;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_attn_fwd(const FwdArgs& a, int n_items, int D, bool merge, hipStream_t st) {
+  if (n_items <= 0) return hipSuccess;
+  dim3 grid(n_items), block(NT);
+  if (D == 128)
+    return merge ? sp_launch(kKFwd, attn_fwd_kernel<128, true>, grid, block, st, a)
+                 : sp_launch(kKFwd, attn_fwd_kernel<128, false>, grid, block, st, a);
+  return merge ? sp_launch(kKFwd, attn_fwd_kernel<64, true>, grid, block, st, a)
+               : sp_launch(kKFwd, attn_fwd_kernel<64, false>, grid, block, st, a);
+}
+
+}  // namespace spk

@@ -1,0 +1,354 @@
+// HBM-bound kernels of the SP attention library (gfx950):
+//   * Ulysses pack / unpack with dummy-head zero fill (Listing 1 pad/unpad
+//     around the all-to-all layout of Section 4),
+//   * the log-sum-exp merge of two partial attention results (ring combine,
+//     Section 2.1),
+//   * fills, bf16 casts, 8x8 register transposes feeding the attention
+//     kernels' transposed operands, the backward's row dot D_i = dO_i . O_i,
+//     and the GQA reduction of per-query-head dK/dV partials.
+// All accesses are 16-byte vectors; consecutive lanes touch consecutive
+// 16-byte chunks of a row.
+#include "dev_common.h"
+#include "launch.h"
+
+namespace spk {
+
+static constexpr int kBlock = 256;
+static constexpr int kMaxBlocks = 256 * 32;  // grid-stride beyond this
+
+static inline int grid_for(int64_t n_threads) {
+  int64_t b = (n_threads + kBlock - 1) / kBlock;
+  if (b < 1) b = 1;
+  return (int)(b > kMaxBlocks ? kMaxBlocks : b);
+}
+
+// ---------------------------------------------------------------- pack
+// dst[j, t, h, c] = src[t, map[j*Hd + h], c] or 0; c counts 16-byte chunks.
+__global__ __launch_bounds__(kBlock) void pack_kernel(const u32x4* __restrict__ src,
+                                                      u32x4* __restrict__ dst, PackArgs a) {
+  const int64_t n = (int64_t)a.sp * a.T * a.Hd * a.nch;
+  for (int64_t e = (int64_t)blockIdx.x * kBlock + threadIdx.x; e < n;
+       e += (int64_t)gridDim.x * kBlock) {
+    int c = (int)(e % a.nch);
+    int64_t r = e / a.nch;
+    int h = (int)(r % a.Hd);
+    r /= a.Hd;
+    int t = (int)(r % a.T);
+    int j = (int)(r / a.T);
+    int g = a.map[j * a.Hd + h];
+    u32x4 v = {0u, 0u, 0u, 0u};
+    if (g >= 0) v = src[((int64_t)t * a.Hs + g) * a.nch + c];
+    dst[e] = v;
+  }
+}
+
+// dst[t, g, c] = src[j, t, h, c] with inv[g] = j*Hs + h (every g named once).
+__global__ __launch_bounds__(kBlock) void unpack_kernel(const u32x4* __restrict__ src,
+                                                        u32x4* __restrict__ dst, PackArgs a) {
+  const int64_t n = (int64_t)a.T * a.Hd * a.nch;
+  for (int64_t e = (int64_t)blockIdx.x * kBlock + threadIdx.x; e < n;
+       e += (int64_t)gridDim.x * kBlock) {
+    int c = (int)(e % a.nch);
+    int64_t r = e / a.nch;
+    int g = (int)(r % a.Hd);
+    int t = (int)(r / a.Hd);
+    int s = a.map[g];
+    int j = s / a.Hs, h = s % a.Hs;
+    dst[e] = src[(((int64_t)j * a.T + t) * a.Hs + h) * a.nch + c];
+  }
+}
+
+hipError_t launch_pack(const void* src, void* dst, const PackArgs& a, hipStream_t st) {
+  int64_t n = (int64_t)a.sp * a.T * a.Hd * a.nch;
+  if (n == 0) return hipSuccess;
+  return sp_launch(kKPack, pack_kernel, dim3(grid_for(n)), dim3(kBlock), st, (const u32x4*)src,
+                   (u32x4*)dst, a);
+}
+
+hipError_t launch_unpack(const void* src, void* dst, const PackArgs& a, hipStream_t st) {
+  int64_t n = (int64_t)a.T * a.Hd * a.nch;
+  if (n == 0) return hipSuccess;
+  return sp_launch(kKUnpack, unpack_kernel, dim3(grid_for(n)), dim3(kBlock), st,
+                   (const u32x4*)src, (u32x4*)dst, a);
+}
+
+// ---------------------------------------------------------------- merge
+// Each group of D/8 consecutive lanes (a power of two dividing 64) owns one
+// (t, h) row, so the in-place LSE update happens after every lane of the row
+// has read it (same wavefront, program order).
+SP_DEV void merge_weights(float la, float lb, float& wa, float& wb, float& L) {
+  float m = fmaxf(la, lb);
+  if (m == neg_inf()) {
+    wa = 0.f; wb = 0.f; L = neg_inf();
+    return;
+  }
+  float ea = expf(la - m), eb = expf(lb - m);  // exp(-inf) = 0
+  float s = ea + eb;
+  L = m + logf(s);
+  float inv = 1.f / s;
+  wa = ea * inv;
+  wb = eb * inv;
+}
+
+template <bool PART_BF16>
+__global__ __launch_bounds__(kBlock) void merge_kernel(float* __restrict__ o_acc,
+                                                       float* __restrict__ lse_acc,
+                                                       const void* __restrict__ o_part,
+                                                       const float* __restrict__ lse_part,
+                                                       uint16_t* __restrict__ o_out, int T, int H,
+                                                       int D) {
+  const int n8 = D >> 3;
+  const int64_t n = (int64_t)T * H * n8;
+  for (int64_t e = (int64_t)blockIdx.x * kBlock + threadIdx.x; e < n;
+       e += (int64_t)gridDim.x * kBlock) {
+    int c = (int)(e % n8);
+    int64_t row = e / n8;  // t*H + h
+    int h = (int)(row % H);
+    int t = (int)(row / H);
+    int64_t li = (int64_t)h * T + t;
+    float la = lse_acc[li], lb = lse_part[li];
+    float wa, wb, L;
+    merge_weights(la, lb, wa, wb, L);
+    float4* oa = (float4*)(o_acc + row * D + c * 8);
+    float4 a0 = oa[0], a1 = oa[1];
+    float b[8];
+    if constexpr (PART_BF16) {
+      u32x4 pv = ((const u32x4*)o_part)[row * n8 + c];
+      for (int i = 0; i < 4; ++i) {
+        b[2 * i] = __uint_as_float(pv[i] << 16);
+        b[2 * i + 1] = __uint_as_float(pv[i] & 0xffff0000u);
+      }
+    } else {
+      const float4* pb = (const float4*)((const float*)o_part + row * D + c * 8);
+      float4 p0 = pb[0], p1 = pb[1];
+      b[0] = p0.x; b[1] = p0.y; b[2] = p0.z; b[3] = p0.w;
+      b[4] = p1.x; b[5] = p1.y; b[6] = p1.z; b[7] = p1.w;
+    }
+    float r[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
+    for (int i = 0; i < 8; ++i) r[i] = wa * r[i] + wb * b[i];
+    oa[0] = make_float4(r[0], r[1], r[2], r[3]);
+    oa[1] = make_float4(r[4], r[5], r[6], r[7]);
+    if (o_out) ((u32x4*)o_out)[row * n8 + c] = pack_bf16x8(r[0], r[1], r[2], r[3], r[4], r[5], r[6], r[7]);
+    if (c == 0) lse_acc[li] = L;
+  }
+}
+
+hipError_t launch_merge(float* o_acc, float* lse_acc, const void* o_part, bool part_bf16,
+                        const float* lse_part, int T, int H, int D, void* o_out, hipStream_t st) {
+  int64_t n = (int64_t)T * H * (D / 8);
+  if (n == 0) return hipSuccess;
+  // keep whole rows inside one wavefront: the grid-stride step must be a
+  // multiple of the row's lane count, which kBlock * grid already is.
+  if (part_bf16)
+    return sp_launch(kKMerge, merge_kernel<true>, dim3(grid_for(n)), dim3(kBlock), st, o_acc,
+                     lse_acc, o_part, lse_part, (uint16_t*)o_out, T, H, D);
+  return sp_launch(kKMerge, merge_kernel<false>, dim3(grid_for(n)), dim3(kBlock), st, o_acc,
+                   lse_acc, o_part, lse_part, (uint16_t*)o_out, T, H, D);
+}
+
+// ---------------------------------------------------------------- fills
+// Fill heads [h0, h1) of every row of a [T, H, D] bf16 tensor with zero.
+__global__ __launch_bounds__(kBlock) void zero_heads_bf16_kernel(u32x4* __restrict__ x, int T,
+                                                                 int H, int nch, int h0, int h1) {
+  const int per_row = (h1 - h0) * nch;
+  const int64_t n = (int64_t)T * per_row;
+  for (int64_t e = (int64_t)blockIdx.x * kBlock + threadIdx.x; e < n;
+       e += (int64_t)gridDim.x * kBlock) {
+    int t = (int)(e / per_row);
+    int w = (int)(e % per_row);
+    x[((int64_t)t * H + h0) * nch + w] = u32x4{0u, 0u, 0u, 0u};
+  }
+}
+
+hipError_t launch_zero_heads_bf16(void* x, int T, int H, int D, int h0, int h1, hipStream_t st) {
+  if (h1 <= h0 || T == 0) return hipSuccess;
+  int64_t n = (int64_t)T * (h1 - h0) * (D / 8);
+  hipLaunchKernelGGL(zero_heads_bf16_kernel, dim3(grid_for(n)), dim3(kBlock), 0, st, (u32x4*)x, T,
+                     H, D / 8, h0, h1);
+  return hipGetLastError();
+}
+
+__global__ __launch_bounds__(kBlock) void fill_f32_kernel(float* __restrict__ x, int64_t n,
+                                                          float v) {
+  for (int64_t e = (int64_t)blockIdx.x * kBlock + threadIdx.x; e < n;
+       e += (int64_t)gridDim.x * kBlock)
+    x[e] = v;
+}
+
+hipError_t launch_fill_f32(float* x, int64_t n, float v, hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(fill_f32_kernel, dim3(grid_for(n)), dim3(kBlock), 0, st, x, n, v);
+  return hipGetLastError();
+}
+
+// Fill heads [h0, h1) of a float32 [T, H, D] tensor with zero (o_acc dummies).
+__global__ __launch_bounds__(kBlock) void zero_heads_f32_kernel(float4* __restrict__ x, int T, int H,
+                                                                int n4, int h0, int h1) {
+  const int per_row = (h1 - h0) * n4;
+  const int64_t n = (int64_t)T * per_row;
+  for (int64_t e = (int64_t)blockIdx.x * kBlock + threadIdx.x; e < n;
+       e += (int64_t)gridDim.x * kBlock) {
+    int t = (int)(e / per_row);
+    int w = (int)(e % per_row);
+    x[((int64_t)t * H + h0) * n4 + w] = make_float4(0.f, 0.f, 0.f, 0.f);
+  }
+}
+
+hipError_t launch_zero_heads_f32(float* x, int T, int H, int D, int h0, int h1, hipStream_t st) {
+  if (h1 <= h0 || T == 0) return hipSuccess;
+  int64_t n = (int64_t)T * (h1 - h0) * (D / 4);
+  hipLaunchKernelGGL(zero_heads_f32_kernel, dim3(grid_for(n)), dim3(kBlock), 0, st, (float4*)x, T,
+                     H, D / 4, h0, h1);
+  return hipGetLastError();
+}
+
+__global__ __launch_bounds__(kBlock) void f32_to_bf16_kernel(const float* __restrict__ s,
+                                                             uint16_t* __restrict__ d, int64_t n) {
+  const int64_t n8 = n >> 3;
+  for (int64_t e = (int64_t)blockIdx.x * kBlock + threadIdx.x; e < n8;
+       e += (int64_t)gridDim.x * kBlock) {
+    const float4* p = (const float4*)(s + e * 8);
+    float4 a = p[0], b = p[1];
+    ((u32x4*)d)[e] = pack_bf16x8(a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w);
+  }
+  // tail (n % 8) handled by the first threads
+  int64_t tail0 = n8 * 8;
+  int64_t t = tail0 + (int64_t)blockIdx.x * kBlock + threadIdx.x;
+  if (t < n) {
+    f32x2 v = {s[t], 0.f};
+    bf16x2 r = __builtin_convertvector(v, bf16x2);
+    d[t] = (uint16_t)(__builtin_bit_cast(uint32_t, r) & 0xffffu);
+  }
+}
+
+hipError_t launch_f32_to_bf16(const float* s, void* d, int64_t n, hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(f32_to_bf16_kernel, dim3(grid_for((n + 7) / 8)), dim3(kBlock), 0, st, s,
+                     (uint16_t*)d, n);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- transpose
+// dst[y][d][t] = src[t][h0 + y][d] for t < T, 0 for T <= t < Tp.
+// Each lane moves an 8-token x 8-dim block through registers.
+template <int D>
+__global__ __launch_bounds__(kBlock) void transpose_kernel(const uint16_t* __restrict__ src,
+                                                           uint16_t* __restrict__ dst, int T,
+                                                           int Tp, int H, int h0) {
+  constexpr int NC = D / 8;             // 8-dim chunks per token row
+  constexpr int TPB = (kBlock / NC) * 8;  // tokens per block
+  const int y = blockIdx.y;
+  const int h = h0 + y;
+  const int lane = threadIdx.x;
+  const int dc = lane % NC;
+  const int t0 = blockIdx.x * TPB + (lane / NC) * 8;
+  if (t0 >= Tp) return;
+  uint16_t a[8][8];
+  for (int r = 0; r < 8; ++r) {
+    int t = t0 + r;
+    u32x4 v = {0u, 0u, 0u, 0u};
+    if (t < T) v = *(const u32x4*)(src + ((int64_t)t * H + h) * D + dc * 8);
+    for (int i = 0; i < 4; ++i) {
+      a[r][2 * i] = (uint16_t)(v[i] & 0xffffu);
+      a[r][2 * i + 1] = (uint16_t)(v[i] >> 16);
+    }
+  }
+  uint16_t* out = dst + (int64_t)y * D * Tp;
+  for (int d = 0; d < 8; ++d) {
+    u32x4 w;
+    for (int i = 0; i < 4; ++i) w[i] = (uint32_t)a[2 * i][d] | ((uint32_t)a[2 * i + 1][d] << 16);
+    *(u32x4*)(out + (int64_t)(dc * 8 + d) * Tp + t0) = w;
+  }
+}
+
+hipError_t launch_transpose(const void* src, void* dst, int T, int Tp, int H, int h0, int nh, int D,
+                            hipStream_t st) {
+  if (nh <= 0 || Tp <= 0) return hipSuccess;
+  const int tpb = (kBlock / (D / 8)) * 8;
+  dim3 grid((Tp + tpb - 1) / tpb, nh);
+  if (D == 128)
+    hipLaunchKernelGGL(transpose_kernel<128>, grid, dim3(kBlock), 0, st, (const uint16_t*)src,
+                       (uint16_t*)dst, T, Tp, H, h0);
+  else
+    hipLaunchKernelGGL(transpose_kernel<64>, grid, dim3(kBlock), 0, st, (const uint16_t*)src,
+                       (uint16_t*)dst, T, Tp, H, h0);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- row dot
+// delta[y][t] = sum_d dO[t][y][d] * O[t][y][d]  (float32), y < nh, t < T.
+template <int D>
+__global__ __launch_bounds__(kBlock) void rowdot_kernel(const uint16_t* __restrict__ o,
+                                                        const uint16_t* __restrict__ dout,
+                                                        float* __restrict__ delta, int T, int H,
+                                                        int nh) {
+  constexpr int NC = D / 8;  // lanes per row
+  const int64_t rows = (int64_t)T * nh;
+  const int64_t gid = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+  const int64_t row = gid / NC;
+  const int c = (int)(gid % NC);
+  float s = 0.f;
+  int t = 0, y = 0;
+  if (row < rows) {
+    y = (int)(row % nh);
+    t = (int)(row / nh);
+    int64_t off = ((int64_t)t * H + y) * D + c * 8;
+    u32x4 a = *(const u32x4*)(o + off);
+    u32x4 b = *(const u32x4*)(dout + off);
+    for (int i = 0; i < 4; ++i) {
+      s += __uint_as_float(a[i] << 16) * __uint_as_float(b[i] << 16);
+      s += __uint_as_float(a[i] & 0xffff0000u) * __uint_as_float(b[i] & 0xffff0000u);
+    }
+  }
+  for (int m = NC / 2; m >= 1; m >>= 1) s += __shfl_xor(s, m);
+  if (row < rows && c == 0) delta[(int64_t)y * T + t] = s;
+}
+
+hipError_t launch_rowdot(const void* o, const void* dout, float* delta, int T, int H, int nh, int D,
+                         hipStream_t st) {
+  int64_t n = (int64_t)T * nh * (D / 8);
+  if (n == 0) return hipSuccess;
+  int grid = (int)((n + kBlock - 1) / kBlock);
+  if (D == 128)
+    hipLaunchKernelGGL(rowdot_kernel<128>, dim3(grid), dim3(kBlock), 0, st, (const uint16_t*)o,
+                       (const uint16_t*)dout, delta, T, H, nh);
+  else
+    hipLaunchKernelGGL(rowdot_kernel<64>, dim3(grid), dim3(kBlock), 0, st, (const uint16_t*)o,
+                       (const uint16_t*)dout, delta, T, H, nh);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------- GQA dK/dV reduce
+// out[t][kv][d] = bf16( sum_{y in heads of kv} part[y][t][d] ), ascending y.
+__global__ __launch_bounds__(kBlock) void reduce_kv_kernel(const float* __restrict__ part,
+                                                           uint16_t* __restrict__ out,
+                                                           ReduceArgs a) {
+  const int n8 = a.D >> 3;
+  const int64_t n = (int64_t)a.T * a.Hkv * n8;
+  for (int64_t e = (int64_t)blockIdx.x * kBlock + threadIdx.x; e < n;
+       e += (int64_t)gridDim.x * kBlock) {
+    int c = (int)(e % n8);
+    int64_t r = e / n8;
+    int kv = (int)(r % a.Hkv);
+    int t = (int)(r / a.Hkv);
+    float s[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    int y0 = a.head_lo[kv], y1 = a.head_hi[kv];
+    for (int y = y0; y < y1; ++y) {
+      const float4* p = (const float4*)(part + ((int64_t)y * a.T + t) * a.D + c * 8);
+      float4 u = p[0], w = p[1];
+      s[0] += u.x; s[1] += u.y; s[2] += u.z; s[3] += u.w;
+      s[4] += w.x; s[5] += w.y; s[6] += w.z; s[7] += w.w;
+    }
+    ((u32x4*)out)[e] = pack_bf16x8(s[0], s[1], s[2], s[3], s[4], s[5], s[6], s[7]);
+  }
+}
+
+hipError_t launch_reduce_kv(const float* part, void* out, const ReduceArgs& a, hipStream_t st) {
+  int64_t n = (int64_t)a.T * a.Hkv * (a.D / 8);
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(reduce_kv_kernel, dim3(grid_for(n)), dim3(kBlock), 0, st, part,
+                     (uint16_t*)out, a);
+  return hipGetLastError();
+}
+
+}  // namespace spk

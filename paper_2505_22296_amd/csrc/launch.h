@@ -1,0 +1,131 @@
+// Internal interface between the host-side ABI code and the gfx950 kernels.
+#pragma once
+#include <hip/hip_ext.h>
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace spk {
+
+// Kernel identifiers of the opt-in per-thread launch timer (values match the
+// SP_KERNEL_* constants of the public header).
+enum KernelId { kKFwd = 1, kKDq = 2, kKDkdv = 3, kKPack = 4, kKUnpack = 5, kKMerge = 6, kKCount = 7 };
+
+struct KernelTimer {
+  hipEvent_t start = nullptr, stop = nullptr;
+};
+// Thread-local timer slot of a kernel id (defined with the C ABI).
+KernelTimer& timer_for(int kernel_id);
+
+// Launch `kernel`; when the calling thread armed events for `id`, record them
+// at the kernel's start and end (hipExtLaunchKernelGGL).
+template <typename F, typename... Args>
+inline hipError_t sp_launch(int id, F kernel, dim3 grid, dim3 block, hipStream_t st,
+                            Args... args) {
+  KernelTimer& t = timer_for(id);
+  if (t.start || t.stop)
+    hipExtLaunchKernelGGL(kernel, grid, block, 0, st, t.start, t.stop, 0, args...);
+  else
+    hipLaunchKernelGGL(kernel, grid, block, 0, st, args...);
+  return hipGetLastError();
+}
+
+// Maximum head-map entries a pack/unpack carries by value in its arguments.
+static constexpr int kMaxMap = 512;
+// Maximum local KV heads for the GQA dK/dV reduction.
+static constexpr int kMaxKv = 64;
+
+struct PackArgs {
+  int sp, T, Hs, Hd, nch;  // nch = 16-byte chunks per head row (D / 8)
+  int map[kMaxMap];        // pack: slot -> source head; unpack: dest head -> j*Hs + h
+};
+
+struct ReduceArgs {
+  int T, Hkv, D;
+  int head_lo[kMaxKv], head_hi[kMaxKv];  // query heads [lo, hi) feeding each KV head
+};
+
+// Work item of the attention kernels: 8 int32.
+//   fwd / dq:  {q_begin, q_end, k_begin, k_end, delta, head, kv_head, 0}
+//   dk/dv:     {k_begin, k_end, q_begin, q_end, delta, head, kv_head, 1}
+// Causal visibility of key j from row i is j <= i + delta.
+static constexpr int kItemInts = 8;
+
+struct FwdArgs {
+  const uint16_t* q;   // [T_q, H, D]
+  const uint16_t* k;   // [T_k, Hkv, D]
+  const uint16_t* vt;  // [Hkv, D, Tkp] (V transposed, zero past T_k)
+  uint16_t* o;         // [T_q, H, D] (plain forward)
+  float* lse;          // [H, T_q]
+  float* o_acc;        // ring: [T_q, H, D] float32 in/out
+  float* lse_acc;      // ring: [H, T_q] in/out
+  uint16_t* o_out;     // ring: optional bf16 copy of the merged O
+  const int32_t* items;
+  int T_q, T_k, Tkp, H, Hkv;
+  float scale_log2;    // softmax_scale * log2(e)
+  int causal, init;
+};
+
+struct DqArgs {
+  const uint16_t* q;     // [T_q, H, D]
+  const uint16_t* k;     // [T_k, Hkv, D]
+  const uint16_t* v;     // [T_k, Hkv, D]
+  const uint16_t* kt;    // [Hkv, D, Tkp]
+  const uint16_t* dout;  // [T_q, H, D]
+  const float* lse;      // [H, T_q]
+  const float* delta;    // [n_real, T_q]
+  uint16_t* dq;          // bf16 [T_q, H, D] or null
+  float* dq_acc;         // float32 [T_q, H, D] (+=) or null
+  const int32_t* items;
+  int T_q, T_k, Tkp, H, Hkv;
+  float scale_log2, scale;
+  int causal;
+};
+
+struct DkdvArgs {
+  const uint16_t* q;     // [T_q, H, D]
+  const uint16_t* qt;    // [n_real, D, Tqp]
+  const uint16_t* dout;  // [T_q, H, D]
+  const uint16_t* dot;   // [n_real, D, Tqp]
+  const float* lse;      // [H, T_q]
+  const float* delta;    // [n_real, T_q]
+  const uint16_t* k;     // [T_k, Hkv, D]
+  const uint16_t* v;     // [T_k, Hkv, D]
+  uint16_t* dk;          // bf16 [T_k, Hkv, D] (direct mode)
+  uint16_t* dv;
+  float* part_k;         // float32 [n_real, T_k, D] (GQA partial mode)
+  float* part_v;
+  const int32_t* items;
+  int T_q, T_k, Tqp, H, Hkv;
+  float scale_log2, scale;
+  int causal, direct;
+};
+
+hipError_t launch_pack(const void* src, void* dst, const PackArgs& a, hipStream_t st);
+hipError_t launch_unpack(const void* src, void* dst, const PackArgs& a, hipStream_t st);
+hipError_t launch_merge(float* o_acc, float* lse_acc, const void* o_part, bool part_bf16,
+                        const float* lse_part, int T, int H, int D, void* o_out, hipStream_t st);
+hipError_t launch_zero_heads_bf16(void* x, int T, int H, int D, int h0, int h1, hipStream_t st);
+hipError_t launch_zero_heads_f32(float* x, int T, int H, int D, int h0, int h1, hipStream_t st);
+hipError_t launch_fill_f32(float* x, int64_t n, float v, hipStream_t st);
+hipError_t launch_f32_to_bf16(const float* s, void* d, int64_t n, hipStream_t st);
+hipError_t launch_transpose(const void* src, void* dst, int T, int Tp, int H, int h0, int nh, int D,
+                            hipStream_t st);
+hipError_t launch_rowdot(const void* o, const void* dout, float* delta, int T, int H, int nh, int D,
+                         hipStream_t st);
+hipError_t launch_reduce_kv(const float* part, void* out, const ReduceArgs& a, hipStream_t st);
+
+hipError_t launch_attn_fwd(const FwdArgs& a, int n_items, int D, bool merge, hipStream_t st);
+hipError_t launch_attn_dq(const DqArgs& a, int n_items, int D, hipStream_t st);
+hipError_t launch_attn_dkdv(const DkdvArgs& a, int n_items, int D, hipStream_t st);
+
+// Tile sizes the host scheduler must use (rows per fwd/dq item, keys per
+// dk/dv item) and the padding of transposed copies.
+static constexpr int kFwdBM = 128;
+static constexpr int kFwdBN = 64;
+static constexpr int kDqBM = 128;
+static constexpr int kDqBN = 32;
+static constexpr int kDkdvBN = 128;
+static constexpr int kDkdvBQ = 32;
+static constexpr int kTransposePad = 64;
+
+}  // namespace spk

@@ -1,0 +1,192 @@
+"""CPU-only checks of the C-ABI library: it loads, exports every symbol the
+header declares, rejects invalid arguments before touching the GPU, and its
+block-skip schedule covers exactly the pairs the oracle's mask allows."""
+import ctypes
+
+import numpy as np
+import pytest
+
+import paper_2505_22296_amd as sp
+from oracle import attention as A
+from tests.helpers import header_functions, lib_desc, make_shard
+from workloads import workload, WORKLOADS
+
+
+def test_library_exports_header_symbols():
+    lib = sp.load()
+    declared = header_functions()
+    assert len(declared) >= 11, declared
+    for name in declared:
+        assert hasattr(lib, name), name
+    assert set(declared) == set(sp.EXPORTED)
+    assert lib.sp_version() >= 100
+    assert sp.status_string(sp.SP_ERR_WORKSPACE).startswith("workspace")
+
+
+def _good(**over):
+    kw = dict(T_q=256, T_k=256, head_dim=128, H_loc=4, head_offset=4, num_real_heads=7,
+              num_padded_heads=8, gqa_group=7, Hkv_loc=1, kv_head_offset=0,
+              cu_seqlens_q=[0, 100, 256], cu_seqlens_k=[0, 100, 256])
+    kw.update(over)
+    return sp.Desc(**kw)
+
+
+def _ws_status(d, op=sp.SP_OP_FWD):
+    n = ctypes.c_size_t(0)
+    return sp.load().sp_attn_workspace_size(d.ref, op, ctypes.byref(n)), n.value
+
+
+@pytest.mark.parametrize("over,expect", [
+    (dict(), sp.SP_OK),
+    (dict(head_dim=96), sp.SP_ERR_UNSUPPORTED),
+    (dict(num_padded_heads=9), sp.SP_ERR_INVALID_ARG),             # not a multiple of H_loc
+    (dict(num_real_heads=6, gqa_group=6), sp.SP_ERR_INVALID_ARG),  # 2 dummies with sp = 2
+    (dict(gqa_group=2), sp.SP_ERR_INVALID_ARG),                    # 7 % 2 != 0
+    (dict(head_offset=2), sp.SP_ERR_INVALID_ARG),                  # not slot aligned
+    (dict(kv_head_offset=1), sp.SP_ERR_INVALID_ARG),               # KV head outside local range
+    (dict(cu_seqlens_q=[0, 300, 256], cu_seqlens_k=[0, 300, 256]), sp.SP_ERR_INVALID_ARG),
+    (dict(cu_seqlens_q=[1, 100, 256]), sp.SP_ERR_INVALID_ARG),
+    (dict(cu_seqlens_q=[0, 100, 257]), sp.SP_ERR_INVALID_ARG),      # past T_q
+    (dict(softmax_scale=-1.0), sp.SP_ERR_INVALID_ARG),
+    (dict(position_ids_q=np.r_[np.arange(100), np.arange(156) * 2]), sp.SP_ERR_INVALID_ARG),
+    (dict(position_ids_q=np.r_[np.arange(100) + 7, np.arange(156)]), sp.SP_OK),
+    (dict(T_q=-1), sp.SP_ERR_INVALID_ARG),
+])
+def test_descriptor_validation(over, expect):
+    st, n = _ws_status(_good(**over))
+    assert st == expect
+    if expect == sp.SP_OK:
+        assert n >= 256 and n % 256 == 0
+
+
+def test_entry_points_reject_before_launch():
+    """Every error below is detected on the host; nothing reaches the GPU."""
+    lib = sp.load()
+    d = _good()
+    # null tensors
+    assert lib.sp_attn_fwd(d.ref, None, None, None, None, None, None, 0, None) == sp.SP_ERR_INVALID_ARG
+    # workspace too small / missing (pointers are fake but never dereferenced)
+    fake = 1 << 20
+    assert lib.sp_attn_fwd(d.ref, fake, fake, fake, fake, fake, None, 0, None) == sp.SP_ERR_WORKSPACE
+    assert lib.sp_attn_fwd(d.ref, fake, fake, fake, fake, fake, fake, 16, None) == sp.SP_ERR_WORKSPACE
+    # misaligned tensor
+    assert lib.sp_attn_fwd(d.ref, fake + 2, fake, fake, fake, fake, fake, 1 << 40, None) == sp.SP_ERR_INVALID_ARG
+    # bwd needs exactly one of dq / dq_acc
+    assert lib.sp_attn_bwd(d.ref, fake, fake, fake, fake, fake, fake, fake, fake, fake, fake,
+                           fake, 1 << 40, None) == sp.SP_ERR_INVALID_ARG
+    assert lib.sp_attn_bwd(d.ref, fake, fake, fake, fake, fake, fake, None, None, fake, fake,
+                           fake, 1 << 40, None) == sp.SP_ERR_INVALID_ARG
+    # ring init flag
+    assert lib.sp_ring_step(d.ref, fake, fake, fake, fake, fake, 2, None, fake, 1 << 40, None) == sp.SP_ERR_INVALID_ARG
+    # merge: head_dim must be a power of two in [8, 512]
+    assert lib.sp_lse_merge(fake, fake, fake, 1, fake, 4, 2, 96, None, None) == sp.SP_ERR_INVALID_ARG
+    assert lib.sp_f32_to_bf16(fake, fake, -1, None) == sp.SP_ERR_INVALID_ARG
+
+
+def test_pack_unpack_validation():
+    lib = sp.load()
+    i32p = ctypes.POINTER(ctypes.c_int32)
+
+    def m(*v):
+        a = np.array(v, dtype=np.int32)
+        return a, a.ctypes.data_as(i32p)
+
+    fake = 1 << 20
+    a, p = m(0, 1, 2, -1)
+    assert lib.sp_ulysses_pack(fake, 0, 3, 64, 2, 2, p, fake, None) == sp.SP_OK  # T=0: no-op
+    a, p = m(0, 1, 3, -1)  # source head 3 out of range for H_src=3
+    assert lib.sp_ulysses_pack(fake, 8, 3, 64, 2, 2, p, fake, None) == sp.SP_ERR_INVALID_ARG
+    a, p = m(0, 1, 2, -1)
+    assert lib.sp_ulysses_pack(fake, 8, 3, 60, 2, 2, p, fake, None) == sp.SP_ERR_INVALID_ARG
+    # unpack: destination head named twice / never
+    a, p = m(0, 1, 1, -1)
+    assert lib.sp_ulysses_unpack(fake, 8, 2, 64, 2, p, 3, fake, None) == sp.SP_ERR_INVALID_ARG
+    a, p = m(0, 1, -1, -1)
+    assert lib.sp_ulysses_unpack(fake, 8, 2, 64, 2, p, 3, fake, None) == sp.SP_ERR_INVALID_ARG
+    a, p = m(0, 1, 2, -1)
+    assert lib.sp_ulysses_unpack(fake, 0, 2, 64, 2, p, 3, fake, None) == sp.SP_OK
+
+
+# ------------------------------------------------------------- scheduler
+def _coverage_from_schedule(sh, items, kind):
+    """Boolean [T_q, T_k] per real head: pairs the work list may make visible
+    (tile range x key range with the causal offset)."""
+    cov = {}
+    for it in items:
+        if kind == "rows":
+            q0, q1, k0, k1, delta, head = it[:6]
+        else:
+            k0, k1, q0, q1, delta, head = it[:6]
+        m = cov.setdefault(head, np.zeros((sh.T_q, sh.T_k), dtype=np.int32))
+        if q1 <= q0 or k1 <= k0:
+            continue
+        i = np.arange(q0, q1)[:, None]
+        j = np.arange(k0, k1)[None, :]
+        vis = np.ones((q1 - q0, k1 - k0), bool)
+        if sh.causal:
+            vis &= j <= i + delta
+        m[q0:q1, k0:k1] += vis
+    return cov
+
+
+CASES = [
+    make_shard("varlen_gqa_dummy", 439, 439, 128, 4, 8, 10, 12, 5, 1, 1, [5, 130, 0, 200, 64]),
+    make_shard("ring_offsets", 200, 300, 128, 2, 0, 2, 2, 1, 2, 0, [200], [300],
+               pos_q=1000 + np.arange(200), pos_k=900 + np.arange(300)),
+    make_shard("noncausal_varlen", 300, 280, 64, 3, 0, 3, 3, 3, 1, 0, [100, 200], [180, 100],
+               causal=False),
+    make_shard("future_keys", 64, 64, 64, 1, 0, 1, 1, 1, 1, 0, [64], [64],
+               pos_q=np.arange(64), pos_k=500 + np.arange(64)),
+]
+
+
+@pytest.mark.parametrize("sh", CASES + [workload(WORKLOADS[0])], ids=lambda s: s.name)
+def test_schedule_covers_exactly_the_mask(sh):
+    """Every allowed (row, key) pair of every real head is covered exactly
+    once by the forward schedule and once by the dK/dV schedule, and no
+    disallowed pair is; dummy heads never appear (bit-exact integer check)."""
+    d = lib_desc(sh)
+    seg_q, seg_k = A.segment_ids(sh.cu_q, sh.T_q), A.segment_ids(sh.cu_k, sh.T_k)
+    mask = A.allowed_mask(np.arange(sh.T_q), seg_q, seg_k, sh.pos_q, sh.pos_k, sh.causal)
+    real = [h for h in range(sh.H_loc) if sh.head_offset + h < sh.num_real_heads]
+    for op, kind in ((sp.SP_OP_FWD, "rows"), (sp.SP_OP_BWD, "keys")):
+        items = sp.sp_attn_schedule(d, op)
+        heads = set(int(h) for h in items[:, 5])
+        assert heads == set(real)
+        for it in items:
+            assert it[6] == sh.kv_of(int(it[5]))
+        cov = _coverage_from_schedule(sh, items, kind)
+        for h in real:
+            assert np.array_equal(cov[h], mask.astype(np.int32)), (op, h)
+        # longest first: tile counts never increase along the list
+        a, b, step = (2, 3, 64) if kind == "rows" else (2, 3, 32)
+        cost = np.array([-(-(int(it[b]) - (int(it[a]) & ~7)) // step) if it[b] > it[a] else 0
+                         for it in items])
+        assert np.all(np.diff(cost) <= 0), (op, cost[:20])
+
+
+def test_schedule_rows_cover_every_row_once():
+    """Forward items tile every query row of every real head exactly once
+    (padding rows included, so their O = 0 / LSE = -inf get written)."""
+    for sh in CASES:
+        items = sp.sp_attn_schedule(lib_desc(sh), sp.SP_OP_FWD)
+        for h in range(sh.n_real_loc):
+            rows = np.zeros(sh.T_q, np.int32)
+            for it in items[items[:, 5] == h]:
+                rows[it[0]:it[1]] += 1
+            assert np.all(rows == 1), sh.name
+        items = sp.sp_attn_schedule(lib_desc(sh), sp.SP_OP_BWD)
+        for h in range(sh.n_real_loc):
+            keys = np.zeros(sh.T_k, np.int32)
+            for it in items[items[:, 5] == h]:
+                keys[it[0]:it[1]] += 1
+            assert np.all(keys == 1), sh.name
+
+
+def test_workspace_sizes_for_workloads():
+    for name in WORKLOADS:
+        sh = workload(name)
+        d = lib_desc(sh)
+        for op in (sp.SP_OP_FWD, sp.SP_OP_BWD, sp.SP_OP_RING_STEP):
+            n = sp.sp_attn_workspace_size(d, op)
+            assert 256 <= n < (8 << 30), (name, op, n)

@@ -1,0 +1,244 @@
+"""GPU parity: the HIP path (through the C ABI) against the fp64 oracle on the
+same seeded bf16 inputs.  Sizes span several tiles and ragged tails.
+
+Bars: pack/unpack bit-exact; attention O, dQ, dK, dV max-abs <= 2e-2 and
+rel-L2 <= 5e-3 over real heads; LSE max-abs <= 1e-3; dummy slots bit-zero;
+the float32 merge within 1e-5 max-abs / 1e-6 rel-L2."""
+import numpy as np
+import pytest
+
+import oracle
+from tests.helpers import (assert_close, bits_from_dev, from_dev, lib_desc, make_shard,
+                           oracle_kw, to_dev, LSE_MAX_ABS)
+from workloads import (padded_heads, randn_bf16_bits, shard_inputs, ulysses_kv_head_map,
+                       ulysses_q_head_map, workload, WORKLOADS)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def sp():
+    import torch
+    assert torch.cuda.is_available()
+    import paper_2505_22296_amd as m
+    m.load()
+    return m
+
+
+def _dec(bits):
+    return oracle.bf16_bits_to_f64(bits)
+
+
+# ------------------------------------------------------------ pack/unpack
+@pytest.mark.parametrize("T,hs,sp_size,D", [(512, 7, 2, 64), (4096, 28, 8, 128), (1000, 40, 16, 128),
+                                            (3, 5, 4, 64)])
+def test_pack_unpack_bit_exact(sp, T, hs, sp_size, D):
+    print(f"pack T={T} hs={hs} sp={sp_size} D={D}", flush=True)
+    bits = randn_bf16_bits((T, hs, D), seed=T + hs)
+    hm = ulysses_q_head_map(hs, sp_size)
+    hloc = padded_heads(hs, sp_size) // sp_size
+    x = to_dev(bits)
+    packed = sp.sp_ulysses_pack(x, sp_size, hloc, hm)
+    ref = oracle.ulysses_pack(bits, sp_size, hloc, hm)
+    got = bits_from_dev(packed)
+    assert np.array_equal(got, ref)
+    back = sp.sp_ulysses_unpack(packed, hm, hs)
+    assert np.array_equal(bits_from_dev(back), bits)
+    assert np.array_equal(bits_from_dev(back), oracle.ulysses_unpack(ref, hm, hs))
+
+
+def test_pack_gqa_kv_map_bit_exact(sp):
+    bits = randn_bf16_bits((256, 4, 128), seed=5)
+    hm = ulysses_kv_head_map(28, 4, 8)
+    w = len(hm) // 8
+    got = bits_from_dev(sp.sp_ulysses_pack(to_dev(bits), 8, w, hm))
+    assert np.array_equal(got, oracle.ulysses_pack(bits, 8, w, hm))
+
+
+# ------------------------------------------------------------------ merge
+@pytest.mark.parametrize("part_bf16", [False, True])
+def test_lse_merge(sp, part_bf16):
+    import torch
+    rng = np.random.default_rng(3)
+    T, H, D = 777, 3, 128
+    oa = rng.standard_normal((T, H, D)).astype(np.float32)
+    la = rng.standard_normal((H, T)).astype(np.float32) * 3
+    ob_bits = randn_bf16_bits((T, H, D), seed=9)
+    ob = _dec(ob_bits).astype(np.float32) if part_bf16 else rng.standard_normal((T, H, D)).astype(np.float32)
+    lb = rng.standard_normal((H, T)).astype(np.float32) * 3
+    la[0, :50] = -np.inf
+    lb[0, 25:75] = -np.inf
+    lb[1, :10] = -np.inf
+    la[1, :10] = -np.inf
+    d_oa = torch.from_numpy(oa).cuda()
+    d_la = torch.from_numpy(la).cuda()
+    d_ob = to_dev(ob_bits) if part_bf16 else torch.from_numpy(ob).cuda()
+    d_lb = torch.from_numpy(lb).cuda()
+    out = torch.empty((T, H, D), dtype=torch.bfloat16, device="cuda")
+    sp.sp_lse_merge(d_oa, d_la, d_ob, d_lb, o_out=out)
+    ro, rl = oracle.lse_merge(oa.astype(np.float64), la.astype(np.float64), ob.astype(np.float64),
+                              lb.astype(np.float64))
+    go, gl = d_oa.cpu().numpy().astype(np.float64), d_la.cpu().numpy().astype(np.float64)
+    assert np.array_equal(np.isneginf(gl), np.isneginf(rl))
+    fin = np.isfinite(rl)
+    assert np.abs(gl[fin] - rl[fin]).max() < 1e-5
+    assert_close(go, ro, "merged O", max_abs=1e-5, rel_l2=1e-6)
+    assert np.all(go[:10, 1] == 0)  # both -inf rows -> 0
+    assert_close(from_dev(out), ro, "bf16 finalize", max_abs=2e-2, rel_l2=5e-3)
+
+
+# -------------------------------------------------------- attention parity
+CASES = [
+    # name, T_q, T_k, D, H_loc, head_off, real, padded, gqa, Hkv, kv_off, seg_q, seg_k, extra
+    ("gqa4_T333_d128", 333, 333, 128, 4, 0, 4, 4, 4, 1, 0, [333], None, {}),
+    ("varlen_gqa5_dummy2_d128", 439, 439, 128, 4, 8, 10, 12, 5, 1, 1, [5, 130, 0, 200, 64], None, {}),
+    ("mha_dummy_d64", 300, 300, 64, 4, 4, 7, 8, 1, 4, 4, [300], None, {}),
+    ("ring_offsets_d128", 200, 300, 128, 2, 0, 2, 2, 1, 2, 0, [200], [300],
+     dict(pos_q=1000 + np.arange(200), pos_k=900 + np.arange(300))),
+    ("noncausal_varlen_d64", 300, 280, 64, 3, 0, 3, 3, 3, 1, 0, [100, 200], [180, 100],
+     dict(causal=False)),
+    ("gqa2_partial_d128", 257, 257, 128, 4, 0, 4, 4, 2, 2, 0, [129, 128], None, {}),
+]
+
+
+def _case(c, seed):
+    name, Tq, Tk, D, H, ho, nr, npd, g, Hkv, ko, sq, sk, extra = c
+    return make_shard(name, Tq, Tk, D, H, ho, nr, npd, g, Hkv, ko, sq, sk, seed_base=seed, **extra)
+
+
+def _run_fwd_bwd(sp, sh, q, k, v, do):
+    import torch
+    d = lib_desc(sh)
+    dq_, dk_, dv_ = (to_dev(x) for x in (q, k, v))
+    o, lse = sp.sp_attn_fwd(d, dq_, dk_, dv_)
+    gq, gk, gv = sp.sp_attn_bwd(d, dq_, dk_, dv_, o, lse, to_dev(do))
+    torch.cuda.synchronize()
+    return o, lse, gq, gk, gv
+
+
+@pytest.mark.parametrize("c", CASES, ids=lambda c: c[0])
+def test_attention_fwd_bwd_parity(sp, c):
+    sh = _case(c, seed=1000 + len(c[0]))
+    print(f"case {sh.name}", flush=True)
+    q, k, v, do = shard_inputs(sh)
+    o, lse, gq, gk, gv = _run_fwd_bwd(sp, sh, q, k, v, do)
+    Q, K, V, dO = (_dec(x) for x in (q, k, v, do))
+    kw = oracle_kw(sh)
+    RO, RL = oracle.attn_forward(Q, K, V, **kw)
+    RdQ, RdK, RdV = oracle.attn_backward(Q, K, V, dO, **kw)
+    nr = sh.n_real_loc
+    GO, GL = from_dev(o), lse.cpu().numpy().astype(np.float64)
+    assert_close(GO[:, :nr], RO[:, :nr], "O")
+    fin = np.isfinite(RL[:nr])
+    assert np.array_equal(np.isfinite(GL[:nr]), fin)
+    assert np.abs(GL[:nr][fin] - RL[:nr][fin]).max() <= LSE_MAX_ABS
+    assert_close(from_dev(gq)[:, :nr], RdQ[:, :nr], "dQ")
+    assert_close(from_dev(gk), RdK, "dK")
+    assert_close(from_dev(gv), RdV, "dV")
+    # dummy slots: bit-zero outputs, LSE -inf
+    if nr < sh.H_loc:
+        assert np.all(bits_from_dev(o)[:, nr:] == 0)
+        assert np.all(bits_from_dev(gq)[:, nr:] == 0)
+        assert np.all(np.isneginf(GL[nr:]))
+    # rows with no keys: exact zero
+    none = ~np.isfinite(RL[0]) if nr else np.zeros(sh.T_q, bool)
+    if nr and none.any():
+        assert np.all(bits_from_dev(o)[none][:, :nr] == 0)
+
+
+def test_c0_workload_and_dummy_kv(sp):
+    """The tiny Ulysses shard: MHA 7 heads padded to 8 for SP 2, rank 1 (head
+    7 and KV head 7 are dummies), D = 64, L = 1024."""
+    sh = workload(WORKLOADS[0])
+    q, k, v, do = shard_inputs(sh)
+    o, lse, gq, gk, gv = _run_fwd_bwd(sp, sh, q, k, v, do)
+    Q, K, V, dO = (_dec(x) for x in (q, k, v, do))
+    kw = oracle_kw(sh)
+    RO, RL = oracle.attn_forward(Q, K, V, **kw)
+    RdQ, RdK, RdV = oracle.attn_backward(Q, K, V, dO, **kw)
+    assert_close(from_dev(o)[:, :3], RO[:, :3], "O")
+    assert_close(from_dev(gq)[:, :3], RdQ[:, :3], "dQ")
+    assert_close(from_dev(gk)[:, :3], RdK[:, :3], "dK")
+    assert_close(from_dev(gv)[:, :3], RdV[:, :3], "dV")
+    for t in (o, gq, gk, gv):
+        assert np.all(bits_from_dev(t)[:, 3] == 0)
+    assert np.all(np.isneginf(lse.cpu().numpy()[3]))
+
+
+def test_peaky_inputs_exercise_rescale(sp):
+    """Q scaled by 3 makes the running max jump often (online rescale path)."""
+    sh = _case(CASES[0], seed=77)
+    q, k, v, do = shard_inputs(sh, peaky=3.0)
+    o, lse, gq, gk, gv = _run_fwd_bwd(sp, sh, q, k, v, do)
+    Q, K, V, dO = (_dec(x) for x in (q, k, v, do))
+    kw = oracle_kw(sh)
+    RO, RL = oracle.attn_forward(Q, K, V, **kw)
+    RdQ, RdK, RdV = oracle.attn_backward(Q, K, V, dO, **kw)
+    # Q x 3 scales dK up to |10|, where one bf16 ulp is 0.0625: the absolute
+    # bar becomes two bf16 ulps of the largest reference value (never below
+    # 2e-2); rel-L2 keeps the 5e-3 bar.
+    for g, r, what in ((from_dev(o), RO, "O"), (from_dev(gq), RdQ, "dQ"),
+                       (from_dev(gk), RdK, "dK"), (from_dev(gv), RdV, "dV")):
+        bar = max(2e-2, 2.0 ** -7 * float(np.abs(r).max()))
+        assert_close(g, r, what, max_abs=bar)
+    assert np.abs(lse.cpu().numpy() - RL).max() <= LSE_MAX_ABS
+
+
+def test_deterministic(sp):
+    sh = _case(CASES[1], seed=5)
+    q, k, v, do = shard_inputs(sh)
+    a = _run_fwd_bwd(sp, sh, q, k, v, do)
+    b = _run_fwd_bwd(sp, sh, q, k, v, do)
+    for x, y in zip(a, b):
+        if x.dtype.is_floating_point and x.dtype != __import__("torch").float32:
+            assert np.array_equal(bits_from_dev(x), bits_from_dev(y))
+        else:
+            assert np.array_equal(x.cpu().numpy(), y.cpu().numpy())
+
+
+# -------------------------------------------------------------------- ring
+def test_ring_rank_fwd_bwd(sp):
+    """Rank r = 2 of a contiguous ring: Q chunk against KV chunks 0..2 with
+    the fused LSE merge; backward per chunk with the final O/LSE and an fp32
+    dQ accumulator.  Oracle: ring fold and per-chunk backward."""
+    import torch
+    C, r, H, Hkv, D = 160, 2, 4, 2, 128
+    base = make_shard("ring", C, C, D, H, 0, H, H, 2, Hkv, 0, [C], [C])
+    q = randn_bf16_bits((C, H, D), 11)
+    do = randn_bf16_bits((C, H, D), 12)
+    ks = [randn_bf16_bits((C, Hkv, D), 20 + c) for c in range(r + 1)]
+    vs = [randn_bf16_bits((C, Hkv, D), 40 + c) for c in range(r + 1)]
+    pos_q = r * C + np.arange(C)
+    dq = to_dev(q)
+    o_acc = torch.empty((C, H, D), dtype=torch.float32, device="cuda")
+    lse_acc = torch.empty((H, C), dtype=torch.float32, device="cuda")
+    o_bf = torch.empty((C, H, D), dtype=torch.bfloat16, device="cuda")
+    for c in range(r + 1):
+        d = lib_desc(base, pos_q=pos_q, pos_k=c * C + np.arange(C))
+        sp.sp_ring_step(d, dq, to_dev(ks[c]), to_dev(vs[c]), o_acc, lse_acc, init=(c == 0),
+                        o_out=o_bf if c == r else None)
+    common = dict(H_loc=H, head_offset=0, num_real_heads=H, gqa_group=2, kv_head_offset=0,
+                  scale=base.scale)
+    chunks = [(_dec(ks[c]), _dec(vs[c])) for c in range(r + 1)]
+    kvpos = [c * C + np.arange(C) for c in range(r + 1)]
+    RO, RL = oracle.ring_forward(_dec(q), chunks, q_pos=pos_q, kv_pos=kvpos, **common)
+    assert_close(o_acc.cpu().numpy().astype(np.float64), RO, "ring O acc")
+    assert_close(from_dev(o_bf), RO, "ring O bf16")
+    assert np.abs(lse_acc.cpu().numpy() - RL).max() <= LSE_MAX_ABS
+    # backward
+    dq_acc = torch.zeros((C, H, D), dtype=torch.float32, device="cuda")
+    dks, dvs = [], []
+    for c in range(r + 1):
+        d = lib_desc(base, pos_q=pos_q, pos_k=c * C + np.arange(C))
+        _, gk, gv = sp.sp_attn_bwd(d, dq, to_dev(ks[c]), to_dev(vs[c]), o_bf, lse_acc, to_dev(do),
+                                   dq_acc=dq_acc)
+        dks.append(from_dev(gk))
+        dvs.append(from_dev(gv))
+    RdQ, RdKs, RdVs = oracle.ring_backward(_dec(q), chunks, _dec(do), RO, RL, q_pos=pos_q,
+                                           kv_pos=kvpos, **common)
+    assert_close(dq_acc.cpu().numpy().astype(np.float64), RdQ, "ring dQ")
+    gq_bf = sp.sp_f32_to_bf16(dq_acc)
+    assert_close(from_dev(gq_bf), RdQ, "ring dQ bf16")
+    for c in range(r + 1):
+        assert_close(dks[c], RdKs[c], f"ring dK chunk {c}")
+        assert_close(dvs[c], RdVs[c], f"ring dV chunk {c}")

@@ -140,9 +140,20 @@ class Shard:
         return (self.head_offset + h) // self.gqa_group - self.kv_head_offset
 
     def without_dummies(self) -> "Shard":
-        """Same real heads with the dummy slots removed (for overhead timing)."""
-        return dataclasses.replace(self, name=self.name + "_nodummy",
-                                   H_loc=self.n_real_loc)
+        """The same real heads reading the same KV heads, described as a shard
+        with no dummy slots (for timing the cost of the dummy slots)."""
+        nr = self.n_real_loc
+        kvs = [self.kv_of(h) for h in range(nr)]
+        if self.gqa_group == 1:
+            g, off = 1, -kvs[0]
+        elif len(set(kvs)) == 1:
+            g, off = nr, -kvs[0]
+        else:
+            raise ValueError("real heads span several KV heads under GQA")
+        return dataclasses.replace(self, name=self.name + "_nodummy", H_loc=nr, head_offset=0,
+                                   num_real_heads=nr, num_padded_heads=nr, gqa_group=g,
+                                   kv_head_offset=off if off >= 0 else 0, sp=1,
+                                   seed_base=self.seed_base)
 
 
 def _ramp_positions(cu: np.ndarray, T: int, base: int = 0) -> np.ndarray:
