@@ -53,21 +53,25 @@ class KernelTimers:
         self.sp, self.torch = sp, torch
         self.pool, self.used, self.on = [], [], False
 
-    def arm(self, kid, flops):
-        if not self.on:
-            return
-        if len(self.used) >= len(self.pool):
+    def reserve(self, n):
+        """Create (and record once) n event pairs ahead of the timed region."""
+        while len(self.pool) < n:
             a = self.torch.cuda.Event(enable_timing=True)
             b = self.torch.cuda.Event(enable_timing=True)
             a.record()
             b.record()
             self.pool.append((a, b))
+
+    def arm(self, kid, flops):
+        if not self.on:
+            return
+        self.reserve(len(self.used) + 1)
         pair = self.pool[len(self.used)]
         self.used.append((kid, flops, pair))
         self.sp.sp_profile_events(kid, *pair)
 
     def disarm(self):
-        for kid in (1, 2, 3, 4, 5, 6):
+        for kid in KNAMES:
             self.sp.sp_profile_events(kid, None, None)
 
     def summary(self):
@@ -81,8 +85,8 @@ class KernelTimers:
         return out
 
 
-KNAMES = {1: "attn_fwd_kernel", 2: "attn_dq_kernel", 3: "attn_dkdv_kernel", 4: "pack_kernel",
-          5: "unpack_kernel", 6: "merge_kernel"}
+KNAMES = {1: "attn_fwd_kernel", 2: "attn_dq_kernel", 3: "attn_dk_kernel", 4: "pack_kernel",
+          5: "unpack_kernel", 6: "merge_kernel", 7: "attn_dv_kernel"}
 
 
 def lib_desc(sp, sh, pos_k=None):
@@ -170,7 +174,8 @@ class Step:
         H = nr * D
         self.flops_fwd = [4.0 * H * p for p in self.pairs]
         self.flops_dq = [6.0 * H * p for p in self.pairs]
-        self.flops_dkdv = [8.0 * H * p for p in self.pairs]
+        self.flops_dk = [6.0 * H * p for p in self.pairs]   # S, dP, dK
+        self.flops_dv = [4.0 * H * p for p in self.pairs]   # S, dV
         self.flops_metric = 14.0 * H * sum(self.pairs)
         self.flops_strict = 12.0 * H * sum(self.pairs)
         sh_ = sh
@@ -192,7 +197,8 @@ class Step:
             self.dq_acc.zero_()
             for c in range(n):
                 t.arm(sp.SP_KERNEL_ATTN_DQ, self.flops_dq[c])
-                t.arm(sp.SP_KERNEL_ATTN_DKDV, self.flops_dkdv[c])
+                t.arm(sp.SP_KERNEL_ATTN_DK, self.flops_dk[c])
+                t.arm(sp.SP_KERNEL_ATTN_DV, self.flops_dv[c])
                 sp.sp_attn_bwd(self.descs[c], self.q, self.k[c], self.v[c], self.o, self.lse_acc,
                                self.do, dq_acc=self.dq_acc, dk=self.dk[c], dv=self.dv[c],
                                workspace=self.ws_b)
@@ -212,7 +218,8 @@ class Step:
                                  dst=self.o_pre)
             sp.sp_ulysses_pack(self.do_pre, sh.sp, sh.H_loc, self.qmap, dst=self.send_do)
         t.arm(sp.SP_KERNEL_ATTN_DQ, self.flops_dq[0])
-        t.arm(sp.SP_KERNEL_ATTN_DKDV, self.flops_dkdv[0])
+        t.arm(sp.SP_KERNEL_ATTN_DK, self.flops_dk[0])
+        t.arm(sp.SP_KERNEL_ATTN_DV, self.flops_dv[0])
         sp.sp_attn_bwd(self.desc, self.q, self.k, self.v, self.o, self.lse, self.do, dq=self.dq,
                        dk=self.dk, dv=self.dv, workspace=self.ws_b)
         if self.ulysses:
@@ -259,34 +266,86 @@ def cpu_baseline(sh, budget_s=15.0):
             "seconds": round(dt, 2)}
 
 
-def measure(sp, torch, name, steps, warmup, per_kernel=True):
+def measure(sp, torch, name, steps, warmup, per_kernel=True, warmup_s=1.5):
     sh = workload(name)
     timers = KernelTimers(sp, torch)
     st = Step(sp, torch, sh, timers)
-    for _ in range(warmup):
-        st.run()
-    torch.cuda.synchronize()
+    # The event pool for the timed steps is created and exercised during the
+    # warmup: the first launches that record fresh timing events run slowly.
     timers.on = per_kernel
-    t0 = time.perf_counter()
-    for _ in range(steps):
+    timers.reserve(8 * (steps + warmup))
+    # W warmup steps, continued until ~1.5 s of GPU work so clocks settle
+    t_w = time.perf_counter()
+    n_w = 0
+    while n_w < warmup or time.perf_counter() - t_w < warmup_s:
+        if n_w == max(1, warmup // 2):
+            timers.used = []  # re-use the pool from the start
         st.run()
+        n_w += 1
+        if n_w % 4 == 0:
+            torch.cuda.synchronize()
+    torch.cuda.synchronize()
+    timers.used = []
+    marks = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    for m in marks:
+        m.record()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        marks[i].record()
+        st.run()
+    marks[steps].record()
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
     timers.on = False
     timers.disarm()
     ms = dt * 1e3 / steps
-    return sh, st, ms, timers.summary()
+    per_step = sorted(marks[i].elapsed_time(marks[i + 1]) for i in range(steps))
+    return sh, st, ms, timers.summary(), per_step
+
+
+def measured_traffic(kernel, workload_name):
+    """HBM bytes per launch of `kernel` from the committed rocprofv3 counter
+    summary (profiles/traffic_<kernel>_<workload>.json), or None when the
+    kernel's source changed since the counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_{workload_name}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    src = os.path.join(ROOT, rec["source"])
+    with open(src, "rb") as f:
+        if hashlib.sha256(f.read()).hexdigest() != rec["source_sha256"]:
+            return None
+    return rec["hbm_bytes_per_launch"]
+
+
+def copy_calibration(torch, nbytes=1 << 30):
+    """One plain device-to-device copy of known size, for scaling the
+    FETCH_SIZE / WRITE_SIZE counters of a profiling run."""
+    a = torch.empty(nbytes, dtype=torch.uint8, device="cuda").random_(0, 255)
+    b = torch.empty_like(a)
+    torch.cuda.synchronize()
+    b.copy_(a)
+    torch.cuda.synchronize()
+    log(f"copy calibration: {nbytes} bytes read, {nbytes} bytes written")
+    del a, b
 
 
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=30)
+    ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD, choices=WORKLOADS)
     ap.add_argument("--all", action="store_true", help="one JSON line per workload")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--dummy-overhead", action="store_true")
+    ap.add_argument("--warmup-seconds", type=float, default=1.5,
+                    help="keep warming up until this much time has passed")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="run one 1 GiB device copy first (counter scaling)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path "
@@ -295,9 +354,12 @@ def main():
     import torch
     import paper_2505_22296_amd as sp
     sp.load()
+    if args.copy_calibration:
+        copy_calibration(torch)
     names = WORKLOADS if args.all else [args.workload]
     for name in names:
-        sh, st, ms, ks = measure(sp, torch, name, args.steps, args.warmup)
+        sh, st, ms, ks, per_step = measure(sp, torch, name, args.steps, args.warmup,
+                                           warmup_s=args.warmup_seconds)
         value = st.flops_metric / (ms * 1e-3) / 1e12
         # dominant kernel: most time per step
         dom = max(ks.items(), key=lambda kv: kv[1]["ms"]) if ks else None
@@ -314,7 +376,8 @@ def main():
             ach = s["flops"] / s["n"] / avg_s / 1e12
             roof = {"bound": "mfma", "kernel": KNAMES[kid], "achieved": round(ach, 1),
                     "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                    "frac": round(ach / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                    "frac": round(ach / PEAK_BF16_TFLOPS, 4),
+                    "traffic": measured_traffic(KNAMES[kid], name),
                     "avg_launch_ms": round(s["ms"] / s["n"], 4),
                     "flops_per_launch": s["flops"] / s["n"]}
         out = {
@@ -329,6 +392,11 @@ def main():
                        "flops_per_step": st.flops_metric},
             "pct_of_bf16_peak": round(100.0 * value / PEAK_BF16_TFLOPS, 2),
             "strict_12D_tflops": round(st.flops_strict / (ms * 1e-3) / 1e12, 2),
+            # per-step GPU times (events between steps): the spread shows the
+            # occasional slow dispatches seen on the box; `value` uses the mean
+            "ms_per_step_median": round(per_step[len(per_step) // 2], 4),
+            "ms_per_step_min": round(per_step[0], 4),
+            "tflops_at_median_step": round(st.flops_metric / (per_step[len(per_step) // 2] * 1e-3) / 1e12, 2),
             "kernels": kern,
             "roofline": roof,
         }

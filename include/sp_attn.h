@@ -32,8 +32,9 @@
  *               anything is enqueued; on error nothing is launched and no
  *               output is touched.  SP_ERR_HIP reports a failed launch or copy.
  *               No C++ exception crosses this interface.
- *   Threading   The library holds no state; calls are reentrant.  Calls that
- *               share a workspace must be ordered on one stream.
+ *   Threading   The library holds no state (apart from the opt-in per-thread
+ *               kernel timer of sp_profile_events); calls are reentrant.  Calls
+ *               that share a workspace must be ordered on one stream.
  *
  * Numerics: bf16 operands, float32 accumulation, float32 softmax statistics,
  * outputs rounded to bf16 with round-to-nearest-even.
@@ -247,12 +248,13 @@ sp_status sp_attn_schedule(const sp_attn_desc* desc, int32_t op, int32_t* items,
  * only state the library keeps (thread-local, no allocation).
  */
 enum {
-  SP_KERNEL_ATTN_FWD = 1,  /* forward / ring-step attention kernel */
-  SP_KERNEL_ATTN_DQ = 2,   /* backward dQ kernel                     */
-  SP_KERNEL_ATTN_DKDV = 3, /* backward dK/dV kernel                  */
-  SP_KERNEL_PACK = 4,      /* Ulysses pack                           */
-  SP_KERNEL_UNPACK = 5,    /* Ulysses unpack                         */
-  SP_KERNEL_LSE_MERGE = 6  /* standalone LSE merge                   */
+  SP_KERNEL_ATTN_FWD = 1, /* forward / ring-step attention kernel        */
+  SP_KERNEL_ATTN_DQ = 2,  /* backward dQ kernel (S, dP, dQ)              */
+  SP_KERNEL_ATTN_DK = 3,  /* backward dK kernel (S, dP, dK)              */
+  SP_KERNEL_PACK = 4,     /* Ulysses pack                                */
+  SP_KERNEL_UNPACK = 5,   /* Ulysses unpack                              */
+  SP_KERNEL_LSE_MERGE = 6,/* standalone LSE merge                        */
+  SP_KERNEL_ATTN_DV = 7   /* backward dV kernel (S, dV)                  */
 };
 sp_status sp_profile_events(int32_t kernel_id, void* start_event, void* stop_event);
 

@@ -187,8 +187,8 @@ void schedule_keys(const sp_attn_desc* d, const Problem& p, int BNK, int BQ,
 
 // Workspace layout.
 struct Layout {
-  size_t items_dq = 0, items_kv = 0, vt = 0, delta = 0, qt = 0, dot = 0, kt = 0, part_k = 0,
-         part_v = 0, total = 0;
+  size_t items_dq = 0, items_kv = 0, vt = 0, delta = 0, lse2 = 0, qt = 0, dot = 0, kt = 0,
+         part_k = 0, part_v = 0, total = 0;
 };
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
@@ -210,6 +210,7 @@ Layout layout_for(const sp_attn_desc* d, const Problem& p, int op, size_t n_item
     L.items_dq = take(n_items_a * kItemInts * 4);
     L.items_kv = take(n_items_b * kItemInts * 4);
     L.delta = take((size_t)std::max(p.n_real, 1) * d->T_q * 4);
+    L.lse2 = take((size_t)std::max(p.n_real, 1) * d->T_q * 4);
     L.qt = take((size_t)std::max(p.n_real, 1) * D * p.Tqp * 2);
     L.dot = take((size_t)std::max(p.n_real, 1) * D * p.Tqp * 2);
     L.kt = take((size_t)d->Hkv_loc * D * p.Tkp * 2);
@@ -468,7 +469,8 @@ sp_status sp_attn_bwd(const sp_attn_desc* d, const void* q, const void* k, const
     if ((s = upload(at(ws, L.items_dq), it_dq, st)) != SP_OK) return s;
     if ((s = upload(at(ws, L.items_kv), it_kv, st)) != SP_OK) return s;
     float* delta = (float*)at(ws, L.delta);
-    SP_HIP(spk::launch_rowdot(o, dout, delta, d->T_q, d->H_loc, p.n_real, D, st));
+    float* lse2 = (float*)at(ws, L.lse2);
+    SP_HIP(spk::launch_rowdot(o, dout, lse, delta, lse2, d->T_q, d->H_loc, p.n_real, D, st));
     SP_HIP(spk::launch_transpose(q, at(ws, L.qt), d->T_q, (int)p.Tqp, d->H_loc, 0, p.n_real, D, st));
     SP_HIP(spk::launch_transpose(dout, at(ws, L.dot), d->T_q, (int)p.Tqp, d->H_loc, 0, p.n_real, D,
                                  st));
@@ -487,7 +489,7 @@ sp_status sp_attn_bwd(const sp_attn_desc* d, const void* q, const void* k, const
     spk::DkdvArgs b{};
     b.q = (const uint16_t*)q; b.qt = (const uint16_t*)at(ws, L.qt);
     b.dout = (const uint16_t*)dout; b.dot = (const uint16_t*)at(ws, L.dot);
-    b.lse = lse; b.delta = delta; b.k = (const uint16_t*)k; b.v = (const uint16_t*)v;
+    b.lse2 = lse2; b.delta = delta; b.k = (const uint16_t*)k; b.v = (const uint16_t*)v;
     b.dk = (uint16_t*)dk; b.dv = (uint16_t*)dv;
     b.part_k = p.direct ? nullptr : (float*)at(ws, L.part_k);
     b.part_v = p.direct ? nullptr : (float*)at(ws, L.part_v);

@@ -66,3 +66,22 @@ SP_DEV int swz(int row, int chunk) {
 
 SP_DEV float wave_max_xor32(float x) { return fmaxf(x, __shfl_xor(x, 32)); }
 SP_DEV float wave_sum_xor32(float x) { return x + __shfl_xor(x, 32); }
+
+// Direct global -> LDS copy of 16 bytes per lane (gfx950 global_load_lds_dwordx4).
+// `lds_block` must be wave-uniform: lane i's 16 bytes land at lds_block + 16 i.
+// Completion is tracked by vmcnt only; callers wait with wait_vmcnt<N>() and a
+// barrier before other wavefronts read the data.
+SP_DEV void dma16(const void* gsrc, void* lds_block) {
+  __builtin_amdgcn_global_load_lds(gsrc, (__attribute__((address_space(3))) void*)lds_block, 16,
+                                   0, 0);
+}
+SP_DEV void dma4(const void* gsrc, void* lds_block) {
+  __builtin_amdgcn_global_load_lds(gsrc, (__attribute__((address_space(3))) void*)lds_block, 4,
+                                   0, 0);
+}
+// s_waitcnt vmcnt(N) leaving expcnt / lgkmcnt unconstrained (gfx9 encoding).
+template <int N>
+SP_DEV void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}

@@ -12,8 +12,8 @@
 //     dQ^T += K^T dS^T               (dS^T C registers used directly as B)
 // dk/dv kernel (key-stationary): workgroup = 128 keys of one KV head and
 //   one query head, wavefront w owns 32 keys (K, V rows as B operands in
-//   registers); per 32-row query chunk (Q, dO row-major and Q^T, dO^T
-//   staged in LDS):
+//   registers); per 32-row query chunk, visited last to first (Q, dO
+//   row-major and Q^T, dO^T staged in LDS):
 //     S = Q K^T, dP = dO V^T          (Q, dO rows loaded in perm32 order)
 //     dS = P (dP - D)
 //     dV^T += dO^T P, dK^T += Q^T dS (P, dS C registers used directly as B)
@@ -85,14 +85,10 @@ __global__ __launch_bounds__(NT, 2) void attn_dq_kernel(DqArgs a) {
     for (int i = 0; i < RLD; ++i) {
       int c = tid + i * NT;
       int r = c / KCH, cc = c % KCH;
-      int key = kt + r;
-      stK[i] = u32x4{0u, 0u, 0u, 0u};
-      stV[i] = u32x4{0u, 0u, 0u, 0u};
-      if (key < k1) {
-        int64_t off = ((int64_t)key * a.Hkv + kvh) * D + cc * 8;
-        stK[i] = *(const u32x4*)(a.k + off);
-        stV[i] = *(const u32x4*)(a.v + off);
-      }
+      int key = min(kt + r, k1 - 1);  // keys past k1 are masked
+      int64_t off = ((int64_t)key * a.Hkv + kvh) * D + cc * 8;
+      stK[i] = *(const u32x4*)(a.k + off);
+      stV[i] = *(const u32x4*)(a.v + off);
     }
 #pragma unroll
     for (int i = 0; i < TLD; ++i) {
@@ -185,123 +181,150 @@ __global__ __launch_bounds__(NT, 2) void attn_dq_kernel(DqArgs a) {
 }
 
 // ---------------------------------------------------------------- dK / dV
-template <int D>
-__global__ __launch_bounds__(NT, 1) void attn_dkdv_kernel(DkdvArgs a) {
+// The query-side chunk of every iteration (Q, dO row-major; Q^T, dO^T; the
+// rows' LSE*log2(e) and D) is copied global -> LDS by DMA into a 3-stage ring,
+// two chunks ahead of the compute; no staging registers.  Row-major tiles use
+// a padded row stride (KCH + 1 chunks: conflict-free for the 8 rows a
+// ds_read_b128 phase serves, and every k-step is an immediate offset);
+// transposed tiles use the 4-chunk XOR swizzle.
+SP_DEV void wait_vmcnt_dyn(int n) {
+  switch (n) {
+    case 0: wait_vmcnt<0>(); break;
+    case 1: wait_vmcnt<1>(); break;
+    case 2: wait_vmcnt<2>(); break;
+    case 3: wait_vmcnt<3>(); break;
+    case 4: wait_vmcnt<4>(); break;
+    case 5: wait_vmcnt<5>(); break;
+    case 6: wait_vmcnt<6>(); break;
+    case 7: wait_vmcnt<7>(); break;
+    case 8: wait_vmcnt<8>(); break;
+    case 9: wait_vmcnt<9>(); break;
+    case 10: wait_vmcnt<10>(); break;
+    case 11: wait_vmcnt<11>(); break;
+    default: wait_vmcnt<0>(); break;
+  }
+}
+
+// MODE 0: dK and dV together (one wave per SIMD: ~350 registers);
+// MODE 1: dV only (S, P, dV += dO^T P); MODE 2: dK only (S, dP, dS,
+// dK += Q^T dS).  The split kernels recompute S but fit two waves per SIMD.
+template <int D, int MODE>
+__global__ __launch_bounds__(NT, MODE == 0 ? 1 : 2)
+void attn_dkdv_kernel(DkdvArgs a) {
+  constexpr bool DO_V = MODE != 2, DO_K = MODE != 1;
   constexpr int BQ = kDkdvBQ;  // 32 query rows per chunk
   constexpr int KS = D / 16;
   constexpr int DB = D / 32;
-  constexpr int KCH = D / 8;
-  constexpr int RLD = BQ * KCH / NT;
-  constexpr int TLD = D * 4 / NT;
-  static_assert(RLD * NT == BQ * KCH && TLD * NT == D * 4, "tile/threads mismatch");
+  constexpr int KCH = D / 8;              // 16-byte chunks per row
+  constexpr int RS = KCH + 1;             // padded row stride of row-major tiles
+  constexpr int QSLOT = BQ * RS;          // slots of a padded [BQ][D] tile
+  constexpr int QB = (QSLOT + 63) / 64;   // 1 KB DMA blocks per padded tile
+  constexpr int TBLK = D / 16;            // 1 KB blocks per [D][BQ] tile (16 dims each)
+  // tiles in stage order: Q (always), dO (dK), Q^T (dK), dO^T (dV)
+  constexpr int NQ = QB, NO = DO_K ? QB : 0, NQT = DO_K ? TBLK : 0, NOT = DO_V ? TBLK : 0;
+  constexpr int NB = NQ + NO + NQT + NOT;  // DMA blocks per stage
+  constexpr int NST = 3;
+  constexpr int OFF_O = NQ * 64, OFF_QT = OFF_O + NO * 64, OFF_OT = OFF_QT + NQT * 64,
+                OFF_LD = OFF_OT + NOT * 64, STAGE = OFF_LD + 16;  // in 16-byte chunks
 
-  __shared__ u32x4 sQ[2][BQ * KCH];
-  __shared__ u32x4 sO[2][BQ * KCH];   // dO rows
-  __shared__ u32x4 sQt[2][D * 4];
-  __shared__ u32x4 sOt[2][D * 4];     // dO^T
-  __shared__ float sL[2][BQ];         // LSE * log2(e) (+inf for rows without keys)
-  __shared__ float sD[2][BQ];         // D_i
+  __shared__ u32x4 smem[NST * STAGE];
 
   const int32_t* it = a.items + (int64_t)blockIdx.x * kItemInts;
   const int k0 = it[0], k1 = it[1], qb = it[2], qe = it[3], delta = it[4], head = it[5],
             kvh = it[6];
   const int tid = threadIdx.x;
-  const int w = tid >> 6, lane = tid & 63, hh = lane >> 5, l32 = lane & 31;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
+  const int lane = tid & 63, hh = lane >> 5, l32 = lane & 31;
   const int key = k0 + w * 32 + l32;  // this lane's key (column of S)
   const bool key_ok = key < k1;
+  // DMA instructions this wave issues per stage (blocks w, w+4, ..; wave 3
+  // also copies the LSE / D rows)
+  const int n_dma = (NB - w + 3) / 4 + (w == 3 ? 1 : 0);
 
-  // K, V rows as B operands (col = key, k = dims).
-  u32x4 kf[KS], vf[KS];
+  const int qc_first = qb & ~7;
+  const int n_chunks = (qe > qb) ? (qe - qc_first + BQ - 1) / BQ : 0;
+  const int Tq1 = a.T_q - 1;
+  const uint16_t* qh = a.q + (int64_t)head * D;
+  const uint16_t* oh = a.dout + (int64_t)head * D;
+  const uint16_t* qth = a.qt + (int64_t)head * D * a.Tqp;
+  const uint16_t* oth = a.dot + (int64_t)head * D * a.Tqp;
+  const float* lh = a.lse2 + (int64_t)head * a.T_q;
+  const float* dh = a.delta + (int64_t)head * a.T_q;
+
+  // Chunks are visited from the segment end backwards: every item of a segment
+  // ends at the same row, so blocks running together stream the same rows at
+  // the same time and share them in L2.
+  const int qc_last = qc_first + (n_chunks - 1) * BQ;
+  auto issue = [&](int n) {
+    const int qc = qc_last - n * BQ;
+    u32x4* stg = smem + (n % NST) * STAGE;
+    const int64_t hstride = (int64_t)a.H * D;
+#pragma unroll
+    for (int b = w; b < NB; b += 4) {
+      if (b < NQ + NO) {
+        const bool isq = b < NQ;
+        const int bb = isq ? b : b - NQ;
+        const int slot = bb * 64 + lane;        // padded tile slot this lane fills
+        const int r = slot / RS;
+        const int c = min(slot % RS, KCH - 1);  // pad slots repeat the last chunk
+        const int64_t off = (int64_t)min(qc + r, Tq1) * hstride + c * 8;
+        if (slot < QSLOT) dma16((isq ? qh : oh) + off, stg + (isq ? 0 : OFF_O) + bb * 64);
+      } else {
+        const bool isq = b < NQ + NO + NQT;
+        const int bb = isq ? b - NQ - NO : b - NQ - NO - NQT;
+        const int dim = bb * 16 + lane / 4;
+        const int lc = (lane % 4) ^ ((dim >> 2) & 3);
+        const int64_t off = (int64_t)dim * a.Tqp + qc + lc * 8;
+        dma16((isq ? qth : oth) + off, stg + (isq ? OFF_QT : OFF_OT) + bb * 64);
+      }
+    }
+    if (w == 3) {
+      const int rr = min(qc + (lane & (BQ - 1)), Tq1);
+      dma4((lane < BQ ? lh : dh) + rr, stg + OFF_LD);
+    }
+  };
+
+  // K (and for dK: V) rows as B operands (col = key, k = dims).
+  u32x4 kf[KS], vf[DO_K ? KS : 1];
   {
     const int64_t off = ((int64_t)(key_ok ? key : k0) * a.Hkv + kvh) * D + hh * 8;
 #pragma unroll
     for (int s = 0; s < KS; ++s) {
       kf[s] = *(const u32x4*)(a.k + off + s * 16);
-      vf[s] = *(const u32x4*)(a.v + off + s * 16);
-      if (!key_ok) {
-        kf[s] = u32x4{0u, 0u, 0u, 0u};
-        vf[s] = u32x4{0u, 0u, 0u, 0u};
-      }
+      if constexpr (DO_K) vf[s] = *(const u32x4*)(a.v + off + s * 16);
     }
   }
-  f32x16 dk[DB], dv[DB];
+  f32x16 dk[DO_K ? DB : 1], dv[DO_V ? DB : 1];
 #pragma unroll
   for (int d = 0; d < DB; ++d)
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      dk[d][r] = 0.f;
-      dv[d][r] = 0.f;
+      if constexpr (DO_K) dk[d][r] = 0.f;
+      if constexpr (DO_V) dv[d][r] = 0.f;
     }
   const float c2 = a.scale_log2;
+  // lane-constant LDS chunk indices of the fragments (k-steps / dim blocks
+  // add compile-time offsets)
+  const int fq_base = perm32(l32) * RS + hh;
+  const int t0_base = swz4(l32, hh), t1_base = swz4(l32, 2 + hh);
 
-  const int qc_first = qb & ~7;
-  const int n_chunks = (qe > qb) ? (qe - qc_first + BQ - 1) / BQ : 0;
-
-  u32x4 stQ[RLD], stO[RLD], stQt[TLD], stOt[TLD];
-  float stL = 0.f;
-  auto load_chunk = [&](int qc) {
-#pragma unroll
-    for (int i = 0; i < RLD; ++i) {
-      int c = tid + i * NT;
-      int r = c / KCH, cc = c % KCH;
-      int rr = qc + r;
-      stQ[i] = u32x4{0u, 0u, 0u, 0u};
-      stO[i] = u32x4{0u, 0u, 0u, 0u};
-      if (rr < a.T_q) {
-        int64_t off = ((int64_t)rr * a.H + head) * D + cc * 8;
-        stQ[i] = *(const u32x4*)(a.q + off);
-        stO[i] = *(const u32x4*)(a.dout + off);
-      }
-    }
-#pragma unroll
-    for (int i = 0; i < TLD; ++i) {
-      int c = tid + i * NT;
-      int d = c / 4, cc = c % 4;
-      int64_t off = ((int64_t)head * D + d) * a.Tqp + qc + cc * 8;
-      stQt[i] = *(const u32x4*)(a.qt + off);
-      stOt[i] = *(const u32x4*)(a.dot + off);
-    }
-    if (tid < 2 * BQ) {
-      int rr = qc + (tid & (BQ - 1));
-      if (tid < BQ) {
-        float l = rr < a.T_q ? a.lse[(int64_t)head * a.T_q + rr] : neg_inf();
-        stL = (l == neg_inf()) ? __builtin_inff() : l * kLog2e;
-      } else {
-        stL = rr < a.T_q ? a.delta[(int64_t)head * a.T_q + rr] : 0.f;
-      }
-    }
-  };
-  auto store_chunk = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < RLD; ++i) {
-      int c = tid + i * NT;
-      int idx = swz<KCH>(c / KCH, c % KCH);
-      sQ[buf][idx] = stQ[i];
-      sO[buf][idx] = stO[i];
-    }
-#pragma unroll
-    for (int i = 0; i < TLD; ++i) {
-      int c = tid + i * NT;
-      int idx = swz4(c / 4, c % 4);
-      sQt[buf][idx] = stQt[i];
-      sOt[buf][idx] = stOt[i];
-    }
-    if (tid < BQ) sL[buf][tid] = stL;
-    else if (tid < 2 * BQ) sD[buf][tid - BQ] = stL;
-  };
-
-  if (n_chunks > 0) {
-    load_chunk(qc_first);
-    store_chunk(0);
-  }
+  if (n_chunks > 0) issue(0);
+  if (n_chunks > 1) issue(1);
+  wait_vmcnt_dyn(n_chunks > 1 ? n_dma : 0);
   __syncthreads();
 
-  const int prow = perm32(l32);
-  int buf = 0;
   for (int n = 0; n < n_chunks; ++n) {
-    const int qc = qc_first + n * BQ;
-    if (n + 1 < n_chunks) load_chunk(qc + BQ);
+    const int qc = qc_last - n * BQ;
+    const u32x4* stg = smem + (n % NST) * STAGE;
+    if (n + 2 < n_chunks) issue(n + 2);
 
+    // A fragments of S = Q K^T (and dP = dO V^T), then the MFMAs
+    u32x4 fq[KS], fo[DO_K ? KS : 1];
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      fq[ks] = stg[fq_base + ks * 2];
+      if constexpr (DO_K) fo[ks] = stg[OFF_O + fq_base + ks * 2];
+    }
     f32x16 s, dp;
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
@@ -310,44 +333,77 @@ __global__ __launch_bounds__(NT, 1) void attn_dkdv_kernel(DkdvArgs a) {
     }
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
-      int idx = swz<KCH>(prow, ks * 2 + hh);
-      s = mfma32(sQ[buf][idx], kf[ks], s);
-      dp = mfma32(sO[buf][idx], vf[ks], dp);
+      s = mfma32(fq[ks], kf[ks], s);
+      if constexpr (DO_K) dp = mfma32(fo[ks], vf[ks], dp);
+    }
+    // A fragments of dV^T = dO^T P and dK^T = Q^T dS (read while the softmax runs)
+    u32x4 fv[DO_V ? DB : 1][2], fk[DO_K ? DB : 1][2];
+#pragma unroll
+    for (int d = 0; d < DB; ++d) {
+      if constexpr (DO_V) {
+        fv[d][0] = stg[OFF_OT + t0_base + d * 128];
+        fv[d][1] = stg[OFF_OT + t1_base + d * 128];
+      }
+      if constexpr (DO_K) {
+        fk[d][0] = stg[OFF_QT + t0_base + d * 128];
+        fk[d][1] = stg[OFF_QT + t1_base + d * 128];
+      }
     }
     // chunk needs masking if it straddles the item's row range, the key
     // tile's end, or the causal diagonal of this wavefront's keys
     const int wk0 = k0 + w * 32;
     const bool need_mask = (qc < qb) || (qc + BQ > qe) || (wk0 + 32 > k1) ||
                            (a.causal && wk0 + 31 > qc + delta);
-    float p[16], ds[16];
+    // visible chunk rows for this lane's key: lo <= row-in-chunk < hi
+    int lo = qb - qc, hi = qe - qc;
+    if (a.causal) lo = max(lo, key - delta - qc);
+    if (!key_ok) hi = lo;
+    lo -= hh * 8;
+    hi -= hh * 8;
+    const f32x4* vL = (const f32x4*)(stg + OFF_LD);
+    const f32x4* vD = vL + BQ / 4;
+    u32x4 pb[2], db[2];
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int lr = c_row_of(r, hh);
-      float pv = __builtin_amdgcn_exp2f(__builtin_fmaf(s[r], c2, -sL[buf][lr]));
-      if (need_mask) {
-        int rr = qc + lr;
-        bool ok = rr >= qb && rr < qe && key_ok && (!a.causal || key <= rr + delta);
-        pv = ok ? pv : 0.f;
+    for (int half = 0; half < 2; ++half) {
+      const f32x4 La = vL[half * 4 + hh * 2], Lb = vL[half * 4 + hh * 2 + 1];
+      const float Lr[8] = {La[0], La[1], La[2], La[3], Lb[0], Lb[1], Lb[2], Lb[3]};
+      float Dr[8];
+      if constexpr (DO_K) {
+        const f32x4 Da = vD[half * 4 + hh * 2], Db = vD[half * 4 + hh * 2 + 1];
+        Dr[0] = Da[0]; Dr[1] = Da[1]; Dr[2] = Da[2]; Dr[3] = Da[3];
+        Dr[4] = Db[0]; Dr[5] = Db[1]; Dr[6] = Db[2]; Dr[7] = Db[3];
       }
-      p[r] = pv;
-      ds[r] = pv * (dp[r] - sD[buf][lr]);
+      float p[8], ds[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const int r = half * 8 + i;
+        float pv = __builtin_amdgcn_exp2f(__builtin_fmaf(s[r], c2, -Lr[i]));
+        if (need_mask) {
+          const int br = half * 16 + i;  // chunk row minus hh*8
+          pv = (br >= lo && br < hi) ? pv : 0.f;
+        }
+        p[i] = pv;
+        if constexpr (DO_K) ds[i] = pv * (dp[r] - Dr[i]);
+      }
+      if constexpr (DO_V) pb[half] = pack_bf16x8(p[0], p[1], p[2], p[3], p[4], p[5], p[6], p[7]);
+      if constexpr (DO_K)
+        db[half] = pack_bf16x8(ds[0], ds[1], ds[2], ds[3], ds[4], ds[5], ds[6], ds[7]);
     }
-    u32x4 pb0 = pack_bf16x8(p[0], p[1], p[2], p[3], p[4], p[5], p[6], p[7]);
-    u32x4 pb1 = pack_bf16x8(p[8], p[9], p[10], p[11], p[12], p[13], p[14], p[15]);
-    u32x4 db0 = pack_bf16x8(ds[0], ds[1], ds[2], ds[3], ds[4], ds[5], ds[6], ds[7]);
-    u32x4 db1 = pack_bf16x8(ds[8], ds[9], ds[10], ds[11], ds[12], ds[13], ds[14], ds[15]);
 #pragma unroll
     for (int d = 0; d < DB; ++d) {
-      const int r0 = swz4(d * 32 + l32, hh), r1 = swz4(d * 32 + l32, 2 + hh);
-      dv[d] = mfma32(sOt[buf][r0], pb0, dv[d]);
-      dv[d] = mfma32(sOt[buf][r1], pb1, dv[d]);
-      dk[d] = mfma32(sQt[buf][r0], db0, dk[d]);
-      dk[d] = mfma32(sQt[buf][r1], db1, dk[d]);
+      if constexpr (DO_V) {
+        dv[d] = mfma32(fv[d][0], pb[0], dv[d]);
+        dv[d] = mfma32(fv[d][1], pb[1], dv[d]);
+      }
+      if constexpr (DO_K) {
+        dk[d] = mfma32(fk[d][0], db[0], dk[d]);
+        dk[d] = mfma32(fk[d][1], db[1], dk[d]);
+      }
     }
 
-    if (n + 1 < n_chunks) store_chunk(buf ^ 1);
+    // chunk n+1 must have landed (chunk n+2 may still be in flight)
+    wait_vmcnt_dyn(n + 2 < n_chunks ? n_dma : 0);
     __syncthreads();
-    buf ^= 1;
   }
 
   if (!key_ok) return;
@@ -357,18 +413,22 @@ __global__ __launch_bounds__(NT, 1) void attn_dkdv_kernel(DkdvArgs a) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int dim = d * 32 + j * 8 + hh * 4;
-      float k0v = dk[d][j * 4] * sc, k1v = dk[d][j * 4 + 1] * sc;
-      float k2v = dk[d][j * 4 + 2] * sc, k3v = dk[d][j * 4 + 3] * sc;
       if (a.direct) {
         const int64_t off = ((int64_t)key * a.Hkv + kvh) * D + dim;
-        *(u32x2*)(a.dk + off) = pack_bf16x4(k0v, k1v, k2v, k3v);
-        *(u32x2*)(a.dv + off) = pack_bf16x4(dv[d][j * 4], dv[d][j * 4 + 1], dv[d][j * 4 + 2],
-                                            dv[d][j * 4 + 3]);
+        if constexpr (DO_K)
+          *(u32x2*)(a.dk + off) = pack_bf16x4(dk[d][j * 4] * sc, dk[d][j * 4 + 1] * sc,
+                                              dk[d][j * 4 + 2] * sc, dk[d][j * 4 + 3] * sc);
+        if constexpr (DO_V)
+          *(u32x2*)(a.dv + off) = pack_bf16x4(dv[d][j * 4], dv[d][j * 4 + 1], dv[d][j * 4 + 2],
+                                              dv[d][j * 4 + 3]);
       } else {
         const int64_t off = ((int64_t)head * a.T_k + key) * D + dim;
-        *(float4*)(a.part_k + off) = make_float4(k0v, k1v, k2v, k3v);
-        *(float4*)(a.part_v + off) =
-            make_float4(dv[d][j * 4], dv[d][j * 4 + 1], dv[d][j * 4 + 2], dv[d][j * 4 + 3]);
+        if constexpr (DO_K)
+          *(float4*)(a.part_k + off) = make_float4(dk[d][j * 4] * sc, dk[d][j * 4 + 1] * sc,
+                                                   dk[d][j * 4 + 2] * sc, dk[d][j * 4 + 3] * sc);
+        if constexpr (DO_V)
+          *(float4*)(a.part_v + off) =
+              make_float4(dv[d][j * 4], dv[d][j * 4 + 1], dv[d][j * 4 + 2], dv[d][j * 4 + 3]);
       }
     }
 }
@@ -383,8 +443,15 @@ hipError_t launch_attn_dq(const DqArgs& a, int n_items, int D, hipStream_t st) {
 
 hipError_t launch_attn_dkdv(const DkdvArgs& a, int n_items, int D, hipStream_t st) {
   if (n_items <= 0) return hipSuccess;
-  if (D == 128) return sp_launch(kKDkdv, attn_dkdv_kernel<128>, dim3(n_items), dim3(NT), st, a);
-  return sp_launch(kKDkdv, attn_dkdv_kernel<64>, dim3(n_items), dim3(NT), st, a);
+  // dV and dK as two kernels (each fits two waves per SIMD)
+  const dim3 g(n_items), b(NT);
+  hipError_t e;
+  if (D == 128) {
+    if ((e = sp_launch(kKDv, attn_dkdv_kernel<128, 1>, g, b, st, a)) != hipSuccess) return e;
+    return sp_launch(kKDk, attn_dkdv_kernel<128, 2>, g, b, st, a);
+  }
+  if ((e = sp_launch(kKDv, attn_dkdv_kernel<64, 1>, g, b, st, a)) != hipSuccess) return e;
+  return sp_launch(kKDk, attn_dkdv_kernel<64, 2>, g, b, st, a);
 }
 
 }  // namespace spk

@@ -80,9 +80,8 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_kernel(FwdArgs a) {
     for (int i = 0; i < KLD; ++i) {
       int c = tid + i * NT;
       int r = c / KCH, cc = c % KCH;
-      int key = kt + r;
-      stK[i] = u32x4{0u, 0u, 0u, 0u};
-      if (key < k1) stK[i] = *(const u32x4*)(a.k + ((int64_t)key * a.Hkv + kvh) * D + cc * 8);
+      int key = min(kt + r, k1 - 1);  // keys past k1 are masked
+      stK[i] = *(const u32x4*)(a.k + ((int64_t)key * a.Hkv + kvh) * D + cc * 8);
     }
 #pragma unroll
     for (int i = 0; i < VLD; ++i) {

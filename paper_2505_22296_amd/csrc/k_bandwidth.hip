@@ -276,11 +276,14 @@ hipError_t launch_transpose(const void* src, void* dst, int T, int Tp, int H, in
 }
 
 // ---------------------------------------------------------------- row dot
-// delta[y][t] = sum_d dO[t][y][d] * O[t][y][d]  (float32), y < nh, t < T.
+// delta[y][t] = sum_d dO[t][y][d] * O[t][y][d]  (float32), y < nh, t < T;
+// lse2[y][t] = LSE[y][t] * log2(e) (+inf where LSE = -inf: rows without keys).
 template <int D>
 __global__ __launch_bounds__(kBlock) void rowdot_kernel(const uint16_t* __restrict__ o,
                                                         const uint16_t* __restrict__ dout,
-                                                        float* __restrict__ delta, int T, int H,
+                                                        const float* __restrict__ lse,
+                                                        float* __restrict__ delta,
+                                                        float* __restrict__ lse2, int T, int H,
                                                         int nh) {
   constexpr int NC = D / 8;  // lanes per row
   const int64_t rows = (int64_t)T * nh;
@@ -293,28 +296,33 @@ __global__ __launch_bounds__(kBlock) void rowdot_kernel(const uint16_t* __restri
     y = (int)(row % nh);
     t = (int)(row / nh);
     int64_t off = ((int64_t)t * H + y) * D + c * 8;
-    u32x4 a = *(const u32x4*)(o + off);
-    u32x4 b = *(const u32x4*)(dout + off);
+    u32x4 va = *(const u32x4*)(o + off);
+    u32x4 vb = *(const u32x4*)(dout + off);
     for (int i = 0; i < 4; ++i) {
-      s += __uint_as_float(a[i] << 16) * __uint_as_float(b[i] << 16);
-      s += __uint_as_float(a[i] & 0xffff0000u) * __uint_as_float(b[i] & 0xffff0000u);
+      s += __uint_as_float(va[i] << 16) * __uint_as_float(vb[i] << 16);
+      s += __uint_as_float(va[i] & 0xffff0000u) * __uint_as_float(vb[i] & 0xffff0000u);
     }
   }
   for (int m = NC / 2; m >= 1; m >>= 1) s += __shfl_xor(s, m);
-  if (row < rows && c == 0) delta[(int64_t)y * T + t] = s;
+  if (row < rows && c == 0) {
+    const int64_t i = (int64_t)y * T + t;
+    delta[i] = s;
+    const float l = lse[i];
+    lse2[i] = (l == neg_inf()) ? __builtin_inff() : l * kLog2e;
+  }
 }
 
-hipError_t launch_rowdot(const void* o, const void* dout, float* delta, int T, int H, int nh, int D,
-                         hipStream_t st) {
+hipError_t launch_rowdot(const void* o, const void* dout, const float* lse, float* delta,
+                         float* lse2, int T, int H, int nh, int D, hipStream_t st) {
   int64_t n = (int64_t)T * nh * (D / 8);
   if (n == 0) return hipSuccess;
   int grid = (int)((n + kBlock - 1) / kBlock);
   if (D == 128)
     hipLaunchKernelGGL(rowdot_kernel<128>, dim3(grid), dim3(kBlock), 0, st, (const uint16_t*)o,
-                       (const uint16_t*)dout, delta, T, H, nh);
+                       (const uint16_t*)dout, lse, delta, lse2, T, H, nh);
   else
     hipLaunchKernelGGL(rowdot_kernel<64>, dim3(grid), dim3(kBlock), 0, st, (const uint16_t*)o,
-                       (const uint16_t*)dout, delta, T, H, nh);
+                       (const uint16_t*)dout, lse, delta, lse2, T, H, nh);
   return hipGetLastError();
 }
 

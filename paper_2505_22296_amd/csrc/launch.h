@@ -8,7 +8,7 @@ namespace spk {
 
 // Kernel identifiers of the opt-in per-thread launch timer (values match the
 // SP_KERNEL_* constants of the public header).
-enum KernelId { kKFwd = 1, kKDq = 2, kKDkdv = 3, kKPack = 4, kKUnpack = 5, kKMerge = 6, kKCount = 7 };
+enum KernelId { kKFwd = 1, kKDq = 2, kKDk = 3, kKPack = 4, kKUnpack = 5, kKMerge = 6, kKDv = 7, kKCount = 8 };
 
 struct KernelTimer {
   hipEvent_t start = nullptr, stop = nullptr;
@@ -86,7 +86,7 @@ struct DkdvArgs {
   const uint16_t* qt;    // [n_real, D, Tqp]
   const uint16_t* dout;  // [T_q, H, D]
   const uint16_t* dot;   // [n_real, D, Tqp]
-  const float* lse;      // [H, T_q]
+  const float* lse2;     // [n_real, T_q]: LSE * log2(e), +inf for rows without keys
   const float* delta;    // [n_real, T_q]
   const uint16_t* k;     // [T_k, Hkv, D]
   const uint16_t* v;     // [T_k, Hkv, D]
@@ -110,8 +110,8 @@ hipError_t launch_fill_f32(float* x, int64_t n, float v, hipStream_t st);
 hipError_t launch_f32_to_bf16(const float* s, void* d, int64_t n, hipStream_t st);
 hipError_t launch_transpose(const void* src, void* dst, int T, int Tp, int H, int h0, int nh, int D,
                             hipStream_t st);
-hipError_t launch_rowdot(const void* o, const void* dout, float* delta, int T, int H, int nh, int D,
-                         hipStream_t st);
+hipError_t launch_rowdot(const void* o, const void* dout, const float* lse, float* delta,
+                         float* lse2, int T, int H, int nh, int D, hipStream_t st);
 hipError_t launch_reduce_kv(const float* part, void* out, const ReduceArgs& a, hipStream_t st);
 
 hipError_t launch_attn_fwd(const FwdArgs& a, int n_items, int D, bool merge, hipStream_t st);

@@ -1,0 +1,164 @@
+"""GPU parity at the benchmark's full shard sizes, in the launch configuration
+bench.py times (same entry points, same tile schedule).
+
+The oracle evaluates sampled outputs one by one: O and LSE for sampled query
+rows, dQ for sampled rows, dK/dV for sampled keys near segment ends (only
+rows after them see those keys).  Over the whole arrays, properties that
+hold at any size are checked: per segment and KV head sum_j dK_j = 0 and
+sum_j dV_j = sum over the group's rows of dO_i (rows of P sum to one), and
+dummy slots are bit-zero."""
+import numpy as np
+import pytest
+
+import oracle
+from tests.helpers import (LSE_MAX_ABS, assert_close, bits_from_dev, from_dev, lib_desc, oracle_kw,
+                           to_dev)
+from workloads import ring_chunk_positions, shard_inputs, workload, WORKLOADS
+
+pytestmark = [pytest.mark.gpu, pytest.mark.timeout(300)]
+
+
+@pytest.fixture(scope="module")
+def sp():
+    import torch
+    assert torch.cuda.is_available()
+    import paper_2505_22296_amd as m
+    m.load()
+    return m
+
+
+def _sample_rows(sh, n_rand=24, seed=0):
+    rng = np.random.default_rng(seed)
+    rows = set()
+    for s in range(len(sh.cu_q) - 1):
+        a, b = int(sh.cu_q[s]), int(sh.cu_q[s + 1])
+        if b > a:
+            rows.update([a, min(a + 1, b - 1), (a + b) // 2, b - 1])
+    rows.update(rng.integers(0, sh.T_q, size=n_rand).tolist())
+    return np.array(sorted(rows))
+
+
+def _tail_keys(sh, per_seg=4):
+    keys = []
+    for s in range(len(sh.cu_k) - 1):
+        a, b = int(sh.cu_k[s]), int(sh.cu_k[s + 1])
+        if b - a >= 8:
+            keys += [b - 1, b - 3, b - 40 if b - 40 >= a else a, b - 130 if b - 130 >= a else a][:per_seg]
+    return np.array(sorted(set(keys)))
+
+
+def _grad_sums(sh, dk, dv, do, nr):
+    """Whole-array gradient identities per segment and KV head."""
+    for s in range(len(sh.cu_k) - 1):
+        a, b = int(sh.cu_k[s]), int(sh.cu_k[s + 1])
+        qa, qb = int(sh.cu_q[s]), int(sh.cu_q[s + 1])
+        if b <= a or qb <= qa:
+            continue
+        for kv in range(sh.Hkv_loc):
+            heads = [h for h in range(nr) if sh.kv_of(h) == kv]
+            if not heads:
+                continue
+            sk = dk[a:b, kv].sum(axis=0)
+            nk = np.sqrt((dk[a:b, kv] ** 2).sum())
+            assert np.abs(sk).max() <= 2e-2 * max(nk, 1e-6), ("sum dK", s, kv)
+            want = do[qa:qb][:, heads].sum(axis=(0, 1))
+            got = dv[a:b, kv].sum(axis=0)
+            assert np.abs(got - want).max() <= 1e-2 * max(1.0, np.abs(want).max()), ("sum dV", s, kv)
+
+
+@pytest.mark.parametrize("name", [w for w in WORKLOADS if not w.startswith("ring")])
+def test_fullsize_shard(sp, name):
+    import torch
+    sh = workload(name)
+    print(f"full-size {name}: T={sh.T_q} H_loc={sh.H_loc} real={sh.n_real_loc}", flush=True)
+    q, k, v, do = shard_inputs(sh)
+    d = lib_desc(sh)
+    Q, K, V, dO = (to_dev(x) for x in (q, k, v, do))
+    o, lse = sp.sp_attn_fwd(d, Q, K, V)
+    gq, gk, gv = sp.sp_attn_bwd(d, Q, K, V, o, lse, dO)
+    torch.cuda.synchronize()
+    nr = sh.n_real_loc
+    qf, kf, vf, dof = (oracle.bf16_bits_to_f64(x) for x in (q, k, v, do))
+    kw = oracle_kw(sh)
+    rows = _sample_rows(sh)
+    RO, RL = oracle.attn_forward(qf, kf, vf, rows=rows, **kw)
+    GO = from_dev(o[torch.from_numpy(rows).cuda()])
+    assert_close(GO[:, :nr], RO[:, :nr], "O rows")
+    GL = lse.cpu().numpy()[:, rows].astype(np.float64)
+    assert np.abs(GL[:nr] - RL[:nr]).max() <= LSE_MAX_ABS
+    rq = rows[::2]
+    RdQ, _, _ = oracle.attn_dq_rows(qf, kf, vf, dof, rq, **kw)
+    assert_close(from_dev(gq[torch.from_numpy(rq).cuda()])[:, :nr], RdQ[:, :nr], "dQ rows")
+    keys = _tail_keys(sh)
+    RdK, RdV = oracle.attn_dkdv_keys(qf, kf, vf, dof, keys, **kw)
+    kidx = torch.from_numpy(keys).cuda()
+    used = sorted({sh.kv_of(h) for h in range(nr)})
+    assert_close(from_dev(gk[kidx])[:, used], RdK[:, used], "dK keys")
+    assert_close(from_dev(gv[kidx])[:, used], RdV[:, used], "dV keys")
+    _grad_sums(sh, from_dev(gk), from_dev(gv), dof, nr)
+    if nr < sh.H_loc:
+        assert torch.all(o[:, nr:].view(torch.int16) == 0)
+        assert torch.all(gq[:, nr:].view(torch.int16) == 0)
+        assert bool(torch.all(torch.isneginf(lse[nr:])))
+
+
+def test_fullsize_ring_rank(sp):
+    """Ring rank 4 of 8 (Q chunk of 16384 against KV chunks 0..4, 28 query /
+    4 KV heads): fused ring steps, then per-chunk backward into an fp32 dQ
+    accumulator.  The oracle is monolithic attention over the concatenated
+    chunks (the ring fold equals it exactly)."""
+    import torch
+    sh = [workload(w) for w in WORKLOADS if w.startswith("ring")][0]
+    n, C, H, D = sh.ring_chunks, sh.chunk, sh.H_loc, sh.D
+    q, _, _, do = shard_inputs(sh, chunk=0)
+    ks, vs = [], []
+    for c in range(n):
+        _, k, v, _ = shard_inputs(sh, chunk=c)
+        ks.append(k)
+        vs.append(v)
+    Q, dO = to_dev(q), to_dev(do)
+    Ks, Vs = [to_dev(x) for x in ks], [to_dev(x) for x in vs]
+    o_acc = torch.empty((C, H, D), dtype=torch.float32, device="cuda")
+    lse = torch.empty((H, C), dtype=torch.float32, device="cuda")
+    o = torch.empty((C, H, D), dtype=torch.bfloat16, device="cuda")
+    descs = [lib_desc(sh, pos_k=ring_chunk_positions(sh, c)) for c in range(n)]
+    for c in range(n):
+        sp.sp_ring_step(descs[c], Q, Ks[c], Vs[c], o_acc, lse, init=(c == 0),
+                        o_out=o if c == n - 1 else None)
+    dq_acc = torch.zeros((C, H, D), dtype=torch.float32, device="cuda")
+    dks, dvs = [], []
+    for c in range(n):
+        _, gk, gv = sp.sp_attn_bwd(descs[c], Q, Ks[c], Vs[c], o, lse, dO, dq_acc=dq_acc)
+        dks.append(gk)
+        dvs.append(gv)
+    torch.cuda.synchronize()
+    # monolithic oracle over the concatenated keys
+    kcat = oracle.bf16_bits_to_f64(np.concatenate(ks))
+    vcat = oracle.bf16_bits_to_f64(np.concatenate(vs))
+    qf, dof = oracle.bf16_bits_to_f64(q), oracle.bf16_bits_to_f64(do)
+    kw = dict(cu_q=np.array([0, C]), cu_k=np.array([0, n * C]), pos_q=sh.pos_q,
+              pos_k=np.arange(n * C), H_loc=H, head_offset=0, num_real_heads=H,
+              gqa_group=sh.gqa_group, kv_head_offset=0, scale=sh.scale, causal=True)
+    rows = np.array(sorted({0, 1, C // 2, C - 1} | set(np.random.default_rng(1).integers(0, C, 12).tolist())))
+    RO, RL = oracle.attn_forward(qf, kcat, vcat, rows=rows, **kw)
+    ridx = torch.from_numpy(rows).cuda()
+    assert_close(from_dev(o[ridx]), RO, "ring O rows")
+    assert_close(o_acc[ridx].cpu().numpy().astype(np.float64), RO, "ring O acc rows")
+    assert np.abs(lse[:, ridx].cpu().numpy() - RL).max() <= LSE_MAX_ABS
+    RdQ, _, _ = oracle.attn_dq_rows(qf, kcat, vcat, dof, rows[::2], **kw)
+    assert_close(dq_acc[torch.from_numpy(rows[::2]).cuda()].cpu().numpy().astype(np.float64), RdQ,
+                 "ring dQ rows")
+    # keys near the end of the diagonal chunk: few rows see them
+    keys = np.array([n * C - 1, n * C - 5, n * C - 70])
+    RdK, RdV = oracle.attn_dkdv_keys(qf, kcat, vcat, dof, keys, **kw)
+    kl = torch.from_numpy(keys - (n - 1) * C).cuda()
+    assert_close(from_dev(dks[-1][kl]), RdK, "ring dK keys")
+    assert_close(from_dev(dvs[-1][kl]), RdV, "ring dV keys")
+    # whole-array identities over all chunks
+    dk_all = np.concatenate([from_dev(x) for x in dks])
+    dv_all = np.concatenate([from_dev(x) for x in dvs])
+    for kv in range(sh.Hkv_loc):
+        heads = [h for h in range(H) if sh.kv_of(h) == kv]
+        assert np.abs(dk_all[:, kv].sum(axis=0)).max() <= 2e-2 * np.sqrt((dk_all[:, kv] ** 2).sum())
+        want = dof[:, heads].sum(axis=(0, 1))
+        assert np.abs(dv_all[:, kv].sum(axis=0) - want).max() <= 1e-2 * max(1.0, np.abs(want).max())
