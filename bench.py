@@ -78,10 +78,11 @@ class KernelTimers:
         out = {}
         for kid, flops, (a, b) in self.used:
             ms = a.elapsed_time(b)
-            s = out.setdefault(kid, {"ms": 0.0, "n": 0, "flops": 0.0})
+            s = out.setdefault(kid, {"ms": 0.0, "n": 0, "flops": 0.0, "all": []})
             s["ms"] += ms
             s["n"] += 1
             s["flops"] += flops
+            s["all"].append(ms)
         return out
 
 
@@ -367,8 +368,12 @@ def main():
         kern = {}
         for kid, s in ks.items():
             avg = s["ms"] / s["n"]
-            kern[KNAMES[kid]] = {"avg_ms": round(avg, 4), "launches_per_step": s["n"] / args.steps,
+            med = sorted(s["all"])[len(s["all"]) // 2]
+            kern[KNAMES[kid]] = {"avg_ms": round(avg, 4), "median_ms": round(med, 4),
+                                 "launches_per_step": s["n"] / args.steps,
                                  "tflops": round(s["flops"] / s["n"] / (avg * 1e-3) / 1e12, 1)
+                                 if s["flops"] else None,
+                                 "tflops_at_median": round(s["flops"] / s["n"] / (med * 1e-3) / 1e12, 1)
                                  if s["flops"] else None}
         if dom:
             kid, s = dom

@@ -187,21 +187,59 @@ __global__ __launch_bounds__(NT, 2) void attn_dq_kernel(DqArgs a) {
 // a padded row stride (KCH + 1 chunks: conflict-free for the 8 rows a
 // ds_read_b128 phase serves, and every k-step is an immediate offset);
 // transposed tiles use the 4-chunk XOR swizzle.
-SP_DEV void wait_vmcnt_dyn(int n) {
-  switch (n) {
-    case 0: wait_vmcnt<0>(); break;
-    case 1: wait_vmcnt<1>(); break;
-    case 2: wait_vmcnt<2>(); break;
-    case 3: wait_vmcnt<3>(); break;
-    case 4: wait_vmcnt<4>(); break;
-    case 5: wait_vmcnt<5>(); break;
-    case 6: wait_vmcnt<6>(); break;
-    case 7: wait_vmcnt<7>(); break;
-    case 8: wait_vmcnt<8>(); break;
-    case 9: wait_vmcnt<9>(); break;
-    case 10: wait_vmcnt<10>(); break;
-    case 11: wait_vmcnt<11>(); break;
-    default: wait_vmcnt<0>(); break;
+
+// Static description of one dK/dV stage: which tiles it holds and where.
+template <int D, int MODE>
+struct DkdvStage {
+  static constexpr bool DO_V = MODE != 2, DO_K = MODE != 1;
+  static constexpr int BQ = kDkdvBQ;
+  static constexpr int KCH = D / 8;             // 16-byte chunks per row
+  static constexpr int RS = KCH + 1;            // padded row stride (chunks)
+  static constexpr int QSLOT = BQ * RS;         // slots of a padded [BQ][D] tile
+  static constexpr int QB = (QSLOT + 63) / 64;  // 1 KB DMA blocks per padded tile
+  static constexpr int TBLK = D / 16;           // 1 KB blocks per [D][BQ] tile
+  // tiles in stage order: Q (always), dO (dK), Q^T (dK), dO^T (dV)
+  static constexpr int NQ = QB, NO = DO_K ? QB : 0, NQT = DO_K ? TBLK : 0,
+                       NOT = DO_V ? TBLK : 0;
+  static constexpr int NB = NQ + NO + NQT + NOT;
+  static constexpr int NBW = (NB + 3) / 4;      // DMA slots per wave (last ones may be junk)
+  static constexpr int OFF_O = NQ * 64, OFF_QT = OFF_O + NO * 64, OFF_OT = OFF_QT + NQT * 64,
+                       OFF_LD = OFF_OT + NOT * 64, STAGE = OFF_LD + 16;  // 16-byte chunks
+  static constexpr int NST = 3;
+  static constexpr int JUNK = NST * STAGE;      // 1 KB sink for unused slots
+  static constexpr int SMEM = JUNK + 64;
+  // tile of block b: 0 Q, 1 dO, 2 Q^T, 3 dO^T, 4 none
+  static constexpr int kind(int b) {
+    return b < NQ ? 0 : b < NQ + NO ? 1 : b < NQ + NO + NQT ? 2 : b < NB ? 3 : 4;
+  }
+  static constexpr int first(int k) {
+    return k == 0 ? 0 : k == 1 ? NQ : k == 2 ? NQ + NO : NQ + NO + NQT;
+  }
+  static constexpr int lds_off(int b) {  // chunk offset of block b inside a stage
+    return kind(b) == 0 ? b * 64
+         : kind(b) == 1 ? OFF_O + (b - NQ) * 64
+         : kind(b) == 2 ? OFF_QT + (b - NQ - NO) * 64
+         : kind(b) == 3 ? OFF_OT + (b - NQ - NO - NQT) * 64 : 0;
+  }
+};
+
+// Uniform per-chunk source pointers of the four tiles.
+struct DkdvSrc {
+  const uint16_t *q, *o, *qt, *ot;
+};
+
+// DMA of one stage by wave W: every slot is compile-time; the per-lane part of
+// each source address is `off[j]` (elements), the chunk part is in `src`.
+template <int D, int MODE, int W>
+SP_DEV void dkdv_issue(const DkdvSrc& src, const int (&off)[DkdvStage<D, MODE>::NBW], u32x4* stg,
+                       u32x4* junk) {
+  using S = DkdvStage<D, MODE>;
+#pragma unroll
+  for (int j = 0; j < S::NBW; ++j) {
+    const int b = W + 4 * j;
+    const int k = S::kind(b);
+    const uint16_t* base = k == 0 ? src.q : k == 1 ? src.o : k == 2 ? src.qt : k == 3 ? src.ot : src.q;
+    dma16(base + off[j], k == 4 ? junk : stg + S::lds_off(b));
   }
 }
 
@@ -211,23 +249,13 @@ SP_DEV void wait_vmcnt_dyn(int n) {
 template <int D, int MODE>
 __global__ __launch_bounds__(NT, MODE == 0 ? 1 : 2)
 void attn_dkdv_kernel(DkdvArgs a) {
-  constexpr bool DO_V = MODE != 2, DO_K = MODE != 1;
-  constexpr int BQ = kDkdvBQ;  // 32 query rows per chunk
-  constexpr int KS = D / 16;
-  constexpr int DB = D / 32;
-  constexpr int KCH = D / 8;              // 16-byte chunks per row
-  constexpr int RS = KCH + 1;             // padded row stride of row-major tiles
-  constexpr int QSLOT = BQ * RS;          // slots of a padded [BQ][D] tile
-  constexpr int QB = (QSLOT + 63) / 64;   // 1 KB DMA blocks per padded tile
-  constexpr int TBLK = D / 16;            // 1 KB blocks per [D][BQ] tile (16 dims each)
-  // tiles in stage order: Q (always), dO (dK), Q^T (dK), dO^T (dV)
-  constexpr int NQ = QB, NO = DO_K ? QB : 0, NQT = DO_K ? TBLK : 0, NOT = DO_V ? TBLK : 0;
-  constexpr int NB = NQ + NO + NQT + NOT;  // DMA blocks per stage
-  constexpr int NST = 3;
-  constexpr int OFF_O = NQ * 64, OFF_QT = OFF_O + NO * 64, OFF_OT = OFF_QT + NQT * 64,
-                OFF_LD = OFF_OT + NOT * 64, STAGE = OFF_LD + 16;  // in 16-byte chunks
+  using S = DkdvStage<D, MODE>;
+  constexpr bool DO_V = S::DO_V, DO_K = S::DO_K;
+  constexpr int BQ = S::BQ, KS = D / 16, DB = D / 32, KCH = S::KCH, RS = S::RS;
+  constexpr int NST = S::NST, STAGE = S::STAGE, NBW = S::NBW;
+  constexpr int OFF_O = S::OFF_O, OFF_QT = S::OFF_QT, OFF_OT = S::OFF_OT, OFF_LD = S::OFF_LD;
 
-  __shared__ u32x4 smem[NST * STAGE];
+  __shared__ u32x4 smem[S::SMEM];
 
   const int32_t* it = a.items + (int64_t)blockIdx.x * kItemInts;
   const int k0 = it[0], k1 = it[1], qb = it[2], qe = it[3], delta = it[4], head = it[5],
@@ -237,13 +265,11 @@ void attn_dkdv_kernel(DkdvArgs a) {
   const int lane = tid & 63, hh = lane >> 5, l32 = lane & 31;
   const int key = k0 + w * 32 + l32;  // this lane's key (column of S)
   const bool key_ok = key < k1;
-  // DMA instructions this wave issues per stage (blocks w, w+4, ..; wave 3
-  // also copies the LSE / D rows)
-  const int n_dma = (NB - w + 3) / 4 + (w == 3 ? 1 : 0);
 
   const int qc_first = qb & ~7;
   const int n_chunks = (qe > qb) ? (qe - qc_first + BQ - 1) / BQ : 0;
   const int Tq1 = a.T_q - 1;
+  const int hstride = a.H * D;  // elements between consecutive rows
   const uint16_t* qh = a.q + (int64_t)head * D;
   const uint16_t* oh = a.dout + (int64_t)head * D;
   const uint16_t* qth = a.qt + (int64_t)head * D * a.Tqp;
@@ -251,47 +277,71 @@ void attn_dkdv_kernel(DkdvArgs a) {
   const float* lh = a.lse2 + (int64_t)head * a.T_q;
   const float* dh = a.delta + (int64_t)head * a.T_q;
 
+  // Per-lane, chunk-independent element offsets of this wave's DMA slots.
+  // Row-major slots: padded tile slot -> (row, chunk); the pad column repeats
+  // the last chunk and slots past the tile stay inside its 1 KB blocks.
+  int off[NBW], row_of[NBW];
+#pragma unroll
+  for (int j = 0; j < NBW; ++j) {
+    const int b = w + 4 * j;
+    const int k = S::kind(b);
+    off[j] = 0;
+    row_of[j] = 0;
+    if (k == 0 || k == 1) {
+      const int slot = (b - S::first(k)) * 64 + lane;
+      const int r = min(slot / RS, BQ - 1);
+      row_of[j] = r;
+      off[j] = r * hstride + min(slot % RS, KCH - 1) * 8;
+    } else if (k == 2 || k == 3) {
+      const int dim = (b - S::first(k)) * 16 + lane / 4;
+      off[j] = dim * a.Tqp + ((lane % 4) ^ ((dim >> 2) & 3)) * 8;
+    }
+  }
+
   // Chunks are visited from the segment end backwards: every item of a segment
   // ends at the same row, so blocks running together stream the same rows at
   // the same time and share them in L2.
   const int qc_last = qc_first + (n_chunks - 1) * BQ;
-  auto issue = [&](int n) {
+  auto issue = [&](int n, int st) {
     const int qc = qc_last - n * BQ;
-    u32x4* stg = smem + (n % NST) * STAGE;
-    const int64_t hstride = (int64_t)a.H * D;
+    u32x4* stg = smem + st * STAGE;
+    DkdvSrc src{qh + (int64_t)qc * hstride, oh + (int64_t)qc * hstride, qth + qc, oth + qc};
+    if (qc + BQ > a.T_q) {
+      // tail chunk: clamp rows past T_q to the last row (masked below)
+      int o2[NBW];
 #pragma unroll
-    for (int b = w; b < NB; b += 4) {
-      if (b < NQ + NO) {
-        const bool isq = b < NQ;
-        const int bb = isq ? b : b - NQ;
-        const int slot = bb * 64 + lane;        // padded tile slot this lane fills
-        const int r = slot / RS;
-        const int c = min(slot % RS, KCH - 1);  // pad slots repeat the last chunk
-        const int64_t off = (int64_t)min(qc + r, Tq1) * hstride + c * 8;
-        if (slot < QSLOT) dma16((isq ? qh : oh) + off, stg + (isq ? 0 : OFF_O) + bb * 64);
-      } else {
-        const bool isq = b < NQ + NO + NQT;
-        const int bb = isq ? b - NQ - NO : b - NQ - NO - NQT;
-        const int dim = bb * 16 + lane / 4;
-        const int lc = (lane % 4) ^ ((dim >> 2) & 3);
-        const int64_t off = (int64_t)dim * a.Tqp + qc + lc * 8;
-        dma16((isq ? qth : oth) + off, stg + (isq ? OFF_QT : OFF_OT) + bb * 64);
+      for (int j = 0; j < NBW; ++j) {
+        const int k = S::kind(w + 4 * j);
+        o2[j] = off[j];
+        if (k == 0 || k == 1) o2[j] += (min(qc + row_of[j], Tq1) - qc - row_of[j]) * hstride;
+      }
+      switch (w) {
+        case 0: dkdv_issue<D, MODE, 0>(src, o2, stg, smem + S::JUNK); break;
+        case 1: dkdv_issue<D, MODE, 1>(src, o2, stg, smem + S::JUNK); break;
+        case 2: dkdv_issue<D, MODE, 2>(src, o2, stg, smem + S::JUNK); break;
+        default: dkdv_issue<D, MODE, 3>(src, o2, stg, smem + S::JUNK); break;
+      }
+    } else {
+      switch (w) {
+        case 0: dkdv_issue<D, MODE, 0>(src, off, stg, smem + S::JUNK); break;
+        case 1: dkdv_issue<D, MODE, 1>(src, off, stg, smem + S::JUNK); break;
+        case 2: dkdv_issue<D, MODE, 2>(src, off, stg, smem + S::JUNK); break;
+        default: dkdv_issue<D, MODE, 3>(src, off, stg, smem + S::JUNK); break;
       }
     }
-    if (w == 3) {
-      const int rr = min(qc + (lane & (BQ - 1)), Tq1);
-      dma4((lane < BQ ? lh : dh) + rr, stg + OFF_LD);
-    }
+    // every wave copies the LSE / D rows (identical data): uniform DMA counts
+    const int rr = min(qc + (lane & (BQ - 1)), Tq1);
+    dma4((lane < BQ ? lh : dh) + rr, stg + OFF_LD);
   };
 
   // K (and for dK: V) rows as B operands (col = key, k = dims).
   u32x4 kf[KS], vf[DO_K ? KS : 1];
   {
-    const int64_t off = ((int64_t)(key_ok ? key : k0) * a.Hkv + kvh) * D + hh * 8;
+    const int64_t koff = ((int64_t)(key_ok ? key : k0) * a.Hkv + kvh) * D + hh * 8;
 #pragma unroll
     for (int s = 0; s < KS; ++s) {
-      kf[s] = *(const u32x4*)(a.k + off + s * 16);
-      if constexpr (DO_K) vf[s] = *(const u32x4*)(a.v + off + s * 16);
+      kf[s] = *(const u32x4*)(a.k + koff + s * 16);
+      if constexpr (DO_K) vf[s] = *(const u32x4*)(a.v + koff + s * 16);
     }
   }
   f32x16 dk[DO_K ? DB : 1], dv[DO_V ? DB : 1];
@@ -308,33 +358,44 @@ void attn_dkdv_kernel(DkdvArgs a) {
   const int fq_base = perm32(l32) * RS + hh;
   const int t0_base = swz4(l32, hh), t1_base = swz4(l32, 2 + hh);
 
-  if (n_chunks > 0) issue(0);
-  if (n_chunks > 1) issue(1);
-  wait_vmcnt_dyn(n_chunks > 1 ? n_dma : 0);
+  if (n_chunks > 0) issue(0, 0);
+  if (n_chunks > 1) issue(1, 1);
+  if (n_chunks > 1) wait_vmcnt<NBW + 1>(); else wait_vmcnt<0>();
   __syncthreads();
 
+  int st = 0, st_next2 = 2;
   for (int n = 0; n < n_chunks; ++n) {
     const int qc = qc_last - n * BQ;
-    const u32x4* stg = smem + (n % NST) * STAGE;
-    if (n + 2 < n_chunks) issue(n + 2);
+    const u32x4* stg = smem + st * STAGE;
+    if (n + 2 < n_chunks) issue(n + 2, st_next2);
 
-    // A fragments of S = Q K^T (and dP = dO V^T), then the MFMAs
-    u32x4 fq[KS], fo[DO_K ? KS : 1];
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      fq[ks] = stg[fq_base + ks * 2];
-      if constexpr (DO_K) fo[ks] = stg[OFF_O + fq_base + ks * 2];
-    }
     f32x16 s, dp;
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       s[r] = 0.f;
       dp[r] = 0.f;
     }
+    if constexpr (MODE == 2) {
+      // dK: registers are at the two-waves-per-SIMD limit; fragments are read
+      // next to their MFMAs and the compiler keeps a few in flight.
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      s = mfma32(fq[ks], kf[ks], s);
-      if constexpr (DO_K) dp = mfma32(fo[ks], vf[ks], dp);
+      for (int ks = 0; ks < KS; ++ks) {
+        s = mfma32(stg[fq_base + ks * 2], kf[ks], s);
+        dp = mfma32(stg[OFF_O + fq_base + ks * 2], vf[ks], dp);
+      }
+    } else {
+      // all A fragments of S = Q K^T (and dP = dO V^T) first, then the MFMAs
+      u32x4 fq[KS], fo[DO_K ? KS : 1];
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        fq[ks] = stg[fq_base + ks * 2];
+        if constexpr (DO_K) fo[ks] = stg[OFF_O + fq_base + ks * 2];
+      }
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        s = mfma32(fq[ks], kf[ks], s);
+        if constexpr (DO_K) dp = mfma32(fo[ks], vf[ks], dp);
+      }
     }
     // A fragments of dV^T = dO^T P and dK^T = Q^T dS (read while the softmax runs)
     u32x4 fv[DO_V ? DB : 1][2], fk[DO_K ? DB : 1][2];
@@ -402,8 +463,10 @@ void attn_dkdv_kernel(DkdvArgs a) {
     }
 
     // chunk n+1 must have landed (chunk n+2 may still be in flight)
-    wait_vmcnt_dyn(n + 2 < n_chunks ? n_dma : 0);
+    if (n + 2 < n_chunks) wait_vmcnt<NBW + 1>(); else wait_vmcnt<0>();
     __syncthreads();
+    st = (st == NST - 1) ? 0 : st + 1;
+    st_next2 = (st_next2 == NST - 1) ? 0 : st_next2 + 1;
   }
 
   if (!key_ok) return;
@@ -414,20 +477,20 @@ void attn_dkdv_kernel(DkdvArgs a) {
     for (int j = 0; j < 4; ++j) {
       const int dim = d * 32 + j * 8 + hh * 4;
       if (a.direct) {
-        const int64_t off = ((int64_t)key * a.Hkv + kvh) * D + dim;
+        const int64_t o = ((int64_t)key * a.Hkv + kvh) * D + dim;
         if constexpr (DO_K)
-          *(u32x2*)(a.dk + off) = pack_bf16x4(dk[d][j * 4] * sc, dk[d][j * 4 + 1] * sc,
-                                              dk[d][j * 4 + 2] * sc, dk[d][j * 4 + 3] * sc);
+          *(u32x2*)(a.dk + o) = pack_bf16x4(dk[d][j * 4] * sc, dk[d][j * 4 + 1] * sc,
+                                            dk[d][j * 4 + 2] * sc, dk[d][j * 4 + 3] * sc);
         if constexpr (DO_V)
-          *(u32x2*)(a.dv + off) = pack_bf16x4(dv[d][j * 4], dv[d][j * 4 + 1], dv[d][j * 4 + 2],
-                                              dv[d][j * 4 + 3]);
+          *(u32x2*)(a.dv + o) = pack_bf16x4(dv[d][j * 4], dv[d][j * 4 + 1], dv[d][j * 4 + 2],
+                                            dv[d][j * 4 + 3]);
       } else {
-        const int64_t off = ((int64_t)head * a.T_k + key) * D + dim;
+        const int64_t o = ((int64_t)head * a.T_k + key) * D + dim;
         if constexpr (DO_K)
-          *(float4*)(a.part_k + off) = make_float4(dk[d][j * 4] * sc, dk[d][j * 4 + 1] * sc,
-                                                   dk[d][j * 4 + 2] * sc, dk[d][j * 4 + 3] * sc);
+          *(float4*)(a.part_k + o) = make_float4(dk[d][j * 4] * sc, dk[d][j * 4 + 1] * sc,
+                                                 dk[d][j * 4 + 2] * sc, dk[d][j * 4 + 3] * sc);
         if constexpr (DO_V)
-          *(float4*)(a.part_v + off) =
+          *(float4*)(a.part_v + o) =
               make_float4(dv[d][j * 4], dv[d][j * 4 + 1], dv[d][j * 4 + 2], dv[d][j * 4 + 3]);
       }
     }
