@@ -33,36 +33,62 @@ constexpr int NT = 256;
 SP_DEV int swz4(int row, int chunk) { return row * 4 + (chunk ^ ((row >> 2) & 3)); }
 
 // ------------------------------------------------------------------- dQ
+// LDS stage: K and V tiles [32 keys][D] with a padded row stride, K^T tile
+// [D][32 keys] with the 4-chunk XOR swizzle; filled by DMA three tiles deep.
+template <int D>
+struct DqStage {
+  static constexpr int BN = kDqBN;
+  static constexpr int KCH = D / 8, RS = KCH + 1;
+  static constexpr int RSLOT = BN * RS;
+  static constexpr int RB = (RSLOT + 63) / 64;  // 1 KB blocks of a padded row tile
+  static constexpr int TB = D / 16;             // 1 KB blocks of the K^T tile
+  static constexpr int NB = 2 * RB + TB, NBW = (NB + 3) / 4;
+  static constexpr int OFF_V = RB * 64, OFF_T = 2 * RB * 64, STAGE = OFF_T + TB * 64;
+  static constexpr int NST = 3;
+  static constexpr int JUNK = NST * STAGE, SMEM = JUNK + 64;
+  static constexpr int kind(int b) { return b < RB ? 0 : b < 2 * RB ? 1 : b < NB ? 2 : 3; }
+  static constexpr int lds_off(int b) {
+    return b < RB ? b * 64 : b < 2 * RB ? OFF_V + (b - RB) * 64 : OFF_T + (b - 2 * RB) * 64;
+  }
+};
+
+template <int D, int W>
+SP_DEV void dq_issue(const uint16_t* ksrc, const uint16_t* vsrc, const uint16_t* tsrc,
+                     const int (&off)[DqStage<D>::NBW], u32x4* stg, u32x4* junk) {
+  using S = DqStage<D>;
+#pragma unroll
+  for (int j = 0; j < S::NBW; ++j) {
+    const int b = W + 4 * j;
+    const int k = S::kind(b);
+    dma16((k == 1 ? vsrc : k == 2 ? tsrc : ksrc) + off[j], k == 3 ? junk : stg + S::lds_off(b));
+  }
+}
+
 template <int D>
 __global__ __launch_bounds__(NT, 2) void attn_dq_kernel(DqArgs a) {
-  constexpr int BN = kDqBN;    // 32 keys per tile
-  constexpr int KS = D / 16;
-  constexpr int DB = D / 32;
-  constexpr int KCH = D / 8;
-  constexpr int RLD = BN * KCH / NT;  // chunks per thread for a [32][D] tile
-  constexpr int TLD = D * 4 / NT;     // chunks per thread for a [D][32] tile
-  static_assert(RLD * NT == BN * KCH && TLD * NT == D * 4, "tile/threads mismatch");
+  using S = DqStage<D>;
+  constexpr int BN = S::BN, KS = D / 16, DB = D / 32, KCH = S::KCH, RS = S::RS;
+  constexpr int NBW = S::NBW, NST = S::NST, STAGE = S::STAGE;
 
-  __shared__ u32x4 sK[2][BN * KCH];
-  __shared__ u32x4 sV[2][BN * KCH];
-  __shared__ u32x4 sKt[2][D * 4];
+  __shared__ u32x4 smem[S::SMEM];
 
   const int32_t* it = a.items + (int64_t)blockIdx.x * kItemInts;
   const int q0 = it[0], q1 = it[1], k0 = it[2], k1 = it[3], delta = it[4], head = it[5],
             kvh = it[6];
   const int tid = threadIdx.x;
-  const int w = tid >> 6, lane = tid & 63, hh = lane >> 5, l32 = lane & 31;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int lane = tid & 63, hh = lane >> 5, l32 = lane & 31;
   const int row = q0 + w * 32 + l32;
   const bool row_ok = row < q1;
   const int lrow = row_ok ? row : q0;
 
   u32x4 qf[KS], df[KS];
   {
-    const int64_t off = ((int64_t)lrow * a.H + head) * D + hh * 8;
+    const int64_t qoff = ((int64_t)lrow * a.H + head) * D + hh * 8;
 #pragma unroll
     for (int s = 0; s < KS; ++s) {
-      qf[s] = *(const u32x4*)(a.q + off + s * 16);
-      df[s] = *(const u32x4*)(a.dout + off + s * 16);
+      qf[s] = *(const u32x4*)(a.q + qoff + s * 16);
+      df[s] = *(const u32x4*)(a.dout + qoff + s * 16);
     }
   }
   const float lse = a.lse[(int64_t)head * a.T_q + lrow];
@@ -79,50 +105,62 @@ __global__ __launch_bounds__(NT, 2) void attn_dq_kernel(DqArgs a) {
   const int kt_first = k0 & ~7;
   const int n_tiles = (k1 > k0) ? (k1 - kt_first + BN - 1) / BN : 0;
 
-  u32x4 stK[RLD], stV[RLD], stT[TLD];
-  auto load_tile = [&](int kt) {
+  const int kstride = a.Hkv * D;
+  int off[NBW], key_of[NBW];
 #pragma unroll
-    for (int i = 0; i < RLD; ++i) {
-      int c = tid + i * NT;
-      int r = c / KCH, cc = c % KCH;
-      int key = min(kt + r, k1 - 1);  // keys past k1 are masked
-      int64_t off = ((int64_t)key * a.Hkv + kvh) * D + cc * 8;
-      stK[i] = *(const u32x4*)(a.k + off);
-      stV[i] = *(const u32x4*)(a.v + off);
+  for (int j = 0; j < NBW; ++j) {
+    const int b = w + 4 * j;
+    const int k = S::kind(b);
+    off[j] = 0;
+    key_of[j] = 0;
+    if (k == 0 || k == 1) {
+      const int slot = (k == 0 ? b : b - S::RB) * 64 + lane;
+      const int r = min(slot / RS, BN - 1);
+      key_of[j] = r;
+      off[j] = r * kstride + min(slot % RS, KCH - 1) * 8;
+    } else if (k == 2) {
+      const int dim = (b - 2 * S::RB) * 16 + lane / 4;
+      off[j] = dim * a.Tkp + ((lane % 4) ^ ((dim >> 2) & 3)) * 8;
     }
-#pragma unroll
-    for (int i = 0; i < TLD; ++i) {
-      int c = tid + i * NT;
-      int d = c / 4, cc = c % 4;
-      stT[i] = *(const u32x4*)(a.kt + ((int64_t)kvh * D + d) * a.Tkp + kt + cc * 8);
-    }
-  };
-  auto store_tile = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < RLD; ++i) {
-      int c = tid + i * NT;
-      int idx = swz<KCH>(c / KCH, c % KCH);
-      sK[buf][idx] = stK[i];
-      sV[buf][idx] = stV[i];
-    }
-#pragma unroll
-    for (int i = 0; i < TLD; ++i) {
-      int c = tid + i * NT;
-      sKt[buf][swz4(c / 4, c % 4)] = stT[i];
-    }
-  };
-
-  if (n_tiles > 0) {
-    load_tile(kt_first);
-    store_tile(0);
   }
-  __syncthreads();
+  const uint16_t* kbase = a.k + (int64_t)kvh * D;
+  const uint16_t* vbase = a.v + (int64_t)kvh * D;
+  const uint16_t* tbase = a.kt + (int64_t)kvh * D * a.Tkp;
+  auto issue = [&](int kt, int st) {
+    u32x4* stg = smem + st * STAGE;
+    const int64_t rowoff = (int64_t)kt * kstride;
+    int o2[NBW];
+    const bool tail = kt + BN > k1;  // keys past k1 (masked) are clamped to k1-1
+#pragma unroll
+    for (int j = 0; j < NBW; ++j) {
+      const int k = S::kind(w + 4 * j);
+      o2[j] = off[j];
+      if ((k == 0 || k == 1) && tail)
+        o2[j] += (min(kt + key_of[j], k1 - 1) - kt - key_of[j]) * kstride;
+    }
+    switch (w) {
+      case 0: dq_issue<D, 0>(kbase + rowoff, vbase + rowoff, tbase + kt, o2, stg, smem + S::JUNK); break;
+      case 1: dq_issue<D, 1>(kbase + rowoff, vbase + rowoff, tbase + kt, o2, stg, smem + S::JUNK); break;
+      case 2: dq_issue<D, 2>(kbase + rowoff, vbase + rowoff, tbase + kt, o2, stg, smem + S::JUNK); break;
+      default: dq_issue<D, 3>(kbase + rowoff, vbase + rowoff, tbase + kt, o2, stg, smem + S::JUNK); break;
+    }
+  };
 
-  const int prow = perm32(l32);
-  int buf = 0;
+  // Three LDS stages, two tiles in flight: at the top of iteration n the
+  // barrier publishes tile n and retires every read of tile n-1, whose stage
+  // then receives tile n+2.
+  if (n_tiles > 0) issue(kt_first, 0);
+  if (n_tiles > 1) issue(kt_first + BN, 1);
+  const int kf_base = perm32(l32) * RS + hh;
+  const int t0_base = S::OFF_T + swz4(l32, hh), t1_base = S::OFF_T + swz4(l32, 2 + hh);
+  int st = 0;
   for (int n = 0; n < n_tiles; ++n) {
     const int kt = kt_first + n * BN;
-    if (n + 1 < n_tiles) load_tile(kt + BN);
+    if (n + 1 < n_tiles) wait_vmcnt<NBW>(); else wait_vmcnt<0>();
+    __syncthreads();
+    if (n + 2 < n_tiles) issue(kt + 2 * BN, st == 0 ? NST - 1 : st - 1);
+    const u32x4* stg = smem + st * STAGE;
+    st = (st == NST - 1) ? 0 : st + 1;
 
     f32x16 s, dp;
 #pragma unroll
@@ -130,35 +168,37 @@ __global__ __launch_bounds__(NT, 2) void attn_dq_kernel(DqArgs a) {
       s[r] = 0.f;
       dp[r] = 0.f;
     }
+    __builtin_amdgcn_s_setprio(1);
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
-      int idx = swz<KCH>(prow, ks * 2 + hh);
-      s = mfma32(sK[buf][idx], qf[ks], s);
-      dp = mfma32(sV[buf][idx], df[ks], dp);
+      s = mfma32(stg[kf_base + ks * 2], qf[ks], s);
+      dp = mfma32(stg[S::OFF_V + kf_base + ks * 2], df[ks], dp);
     }
-    const bool need_mask = (kt < k0) || (kt + BN > k1) || (a.causal && kt + BN - 1 > q0 + delta);
+    __builtin_amdgcn_s_setprio(0);
     float ds[16];
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[r], c2, -l2));
-      if (need_mask) {
+      ds[r] = p * (dp[r] - drow);
+    }
+    const bool need_mask = (kt < k0) | (kt + BN > k1) | (a.causal & (kt + BN - 1 > q0 + delta));
+    if (need_mask) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
         int key = kt + c_row_of(r, hh);
         bool ok = key >= k0 && key < k1 && (!a.causal || key <= row + delta);
-        p = ok ? p : 0.f;
+        ds[r] = ok ? ds[r] : 0.f;
       }
-      ds[r] = p * (dp[r] - drow);
     }
     u32x4 b0 = pack_bf16x8(ds[0], ds[1], ds[2], ds[3], ds[4], ds[5], ds[6], ds[7]);
     u32x4 b1 = pack_bf16x8(ds[8], ds[9], ds[10], ds[11], ds[12], ds[13], ds[14], ds[15]);
+    __builtin_amdgcn_s_setprio(1);
 #pragma unroll
     for (int d = 0; d < DB; ++d) {
-      acc[d] = mfma32(sKt[buf][swz4(d * 32 + l32, hh)], b0, acc[d]);
-      acc[d] = mfma32(sKt[buf][swz4(d * 32 + l32, 2 + hh)], b1, acc[d]);
+      acc[d] = mfma32(stg[t0_base + d * 128], b0, acc[d]);
+      acc[d] = mfma32(stg[t1_base + d * 128], b1, acc[d]);
     }
-
-    if (n + 1 < n_tiles) store_tile(buf ^ 1);
-    __syncthreads();
-    buf ^= 1;
+    __builtin_amdgcn_s_setprio(0);
   }
 
   if (!row_ok) return;
@@ -179,14 +219,6 @@ __global__ __launch_bounds__(NT, 2) void attn_dq_kernel(DqArgs a) {
       }
     }
 }
-
-// ---------------------------------------------------------------- dK / dV
-// The query-side chunk of every iteration (Q, dO row-major; Q^T, dO^T; the
-// rows' LSE*log2(e) and D) is copied global -> LDS by DMA into a 3-stage ring,
-// two chunks ahead of the compute; no staging registers.  Row-major tiles use
-// a padded row stride (KCH + 1 chunks: conflict-free for the 8 rows a
-// ds_read_b128 phase serves, and every k-step is an immediate offset);
-// transposed tiles use the 4-chunk XOR swizzle.
 
 // Static description of one dK/dV stage: which tiles it holds and where.
 template <int D, int MODE>
@@ -375,6 +407,7 @@ void attn_dkdv_kernel(DkdvArgs a) {
       s[r] = 0.f;
       dp[r] = 0.f;
     }
+    __builtin_amdgcn_s_setprio(1);
     if constexpr (MODE == 2) {
       // dK: registers are at the two-waves-per-SIMD limit; fragments are read
       // next to their MFMAs and the compiler keeps a few in flight.
@@ -397,6 +430,7 @@ void attn_dkdv_kernel(DkdvArgs a) {
         if constexpr (DO_K) dp = mfma32(fo[ks], vf[ks], dp);
       }
     }
+    __builtin_amdgcn_s_setprio(0);
     // A fragments of dV^T = dO^T P and dK^T = Q^T dS (read while the softmax runs)
     u32x4 fv[DO_V ? DB : 1][2], fk[DO_K ? DB : 1][2];
 #pragma unroll
@@ -450,6 +484,7 @@ void attn_dkdv_kernel(DkdvArgs a) {
       if constexpr (DO_K)
         db[half] = pack_bf16x8(ds[0], ds[1], ds[2], ds[3], ds[4], ds[5], ds[6], ds[7]);
     }
+    __builtin_amdgcn_s_setprio(1);
 #pragma unroll
     for (int d = 0; d < DB; ++d) {
       if constexpr (DO_V) {
@@ -461,6 +496,7 @@ void attn_dkdv_kernel(DkdvArgs a) {
         dk[d] = mfma32(fk[d][1], db[1], dk[d]);
       }
     }
+    __builtin_amdgcn_s_setprio(0);
 
     // chunk n+1 must have landed (chunk n+2 may still be in flight)
     if (n + 2 < n_chunks) wait_vmcnt<NBW + 1>(); else wait_vmcnt<0>();

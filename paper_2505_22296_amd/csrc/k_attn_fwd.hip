@@ -31,24 +31,51 @@ constexpr int BM = kFwdBM;  // 128 rows per workgroup
 constexpr int BN = kFwdBN;  // 64 keys per tile
 constexpr int NT = 256;
 
+// LDS stage of the forward: K tile [BN][D] with a padded row stride (one base
+// address per lane, k-steps are immediate offsets) and V^T tile [D][BN] with
+// an XOR swizzle of its 8 chunks per row; both filled by DMA.
+template <int D>
+struct FwdStage {
+  static constexpr int KCH = D / 8, RS = KCH + 1;
+  static constexpr int KSLOT = BN * RS;
+  static constexpr int KB = (KSLOT + 63) / 64;  // 1 KB blocks of the K tile
+  static constexpr int VCH = BN / 8;            // chunks per V^T row
+  static constexpr int VB = D * VCH / 64;       // 1 KB blocks of the V^T tile
+  static constexpr int NB = KB + VB, NBW = (NB + 3) / 4;
+  static constexpr int OFF_V = KB * 64, STAGE = OFF_V + VB * 64;  // 16-byte chunks
+  static constexpr int NST = 2;
+  static constexpr int JUNK = NST * STAGE, SMEM = JUNK + 64;
+  static constexpr int kind(int b) { return b < KB ? 0 : b < NB ? 1 : 2; }
+  static constexpr int lds_off(int b) { return b < KB ? b * 64 : OFF_V + (b - KB) * 64; }
+};
+
+template <int D, int W>
+SP_DEV void fwd_issue(const uint16_t* ksrc, const uint16_t* vsrc,
+                      const int (&off)[FwdStage<D>::NBW], u32x4* stg, u32x4* junk) {
+  using S = FwdStage<D>;
+#pragma unroll
+  for (int j = 0; j < S::NBW; ++j) {
+    const int b = W + 4 * j;
+    const int k = S::kind(b);
+    dma16((k == 1 ? vsrc : ksrc) + off[j], k == 2 ? junk : stg + S::lds_off(b));
+  }
+}
+
 template <int D, bool MERGE>
 __global__ __launch_bounds__(NT, 2) void attn_fwd_kernel(FwdArgs a) {
+  using S = FwdStage<D>;
   constexpr int KS = D / 16;   // MFMA k-steps over D
   constexpr int DB = D / 32;   // 32-dim blocks of O^T
-  constexpr int KCH = D / 8;   // 16-byte chunks per K row
-  constexpr int VCH = BN / 8;  // 16-byte chunks per V^T row
-  constexpr int KLD = BN * KCH / NT;
-  constexpr int VLD = D * VCH / NT;
-  static_assert(KLD * NT == BN * KCH && VLD * NT == D * VCH, "tile/threads mismatch");
+  constexpr int KCH = S::KCH, RS = S::RS, VCH = S::VCH, NBW = S::NBW, STAGE = S::STAGE;
 
-  __shared__ u32x4 sK[2][BN * KCH];
-  __shared__ u32x4 sV[2][D * VCH];
+  __shared__ u32x4 smem[S::SMEM];
 
   const int32_t* it = a.items + (int64_t)blockIdx.x * kItemInts;
   const int q0 = it[0], q1 = it[1], k0 = it[2], k1 = it[3], delta = it[4], head = it[5],
             kvh = it[6];
   const int tid = threadIdx.x;
-  const int w = tid >> 6, lane = tid & 63, hh = lane >> 5, l32 = lane & 31;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int lane = tid & 63, hh = lane >> 5, l32 = lane & 31;
   const int row = q0 + w * 32 + l32;
   const bool row_ok = row < q1;
 
@@ -74,59 +101,76 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_kernel(FwdArgs a) {
   const int kt_first = k0 & ~7;
   const int n_tiles = (k1 > k0) ? (k1 - kt_first + BN - 1) / BN : 0;
 
-  u32x4 stK[KLD], stV[VLD];
-  auto load_tile = [&](int kt) {
+  // per-lane, tile-independent element offsets of this wave's DMA slots
+  const int kstride = a.Hkv * D;
+  int off[NBW], key_of[NBW];
 #pragma unroll
-    for (int i = 0; i < KLD; ++i) {
-      int c = tid + i * NT;
-      int r = c / KCH, cc = c % KCH;
-      int key = min(kt + r, k1 - 1);  // keys past k1 are masked
-      stK[i] = *(const u32x4*)(a.k + ((int64_t)key * a.Hkv + kvh) * D + cc * 8);
+  for (int j = 0; j < NBW; ++j) {
+    const int b = w + 4 * j;
+    const int k = S::kind(b);
+    off[j] = 0;
+    key_of[j] = 0;
+    if (k == 0) {
+      const int slot = b * 64 + lane;
+      const int r = min(slot / RS, BN - 1);
+      key_of[j] = r;
+      off[j] = r * kstride + min(slot % RS, KCH - 1) * 8;
+    } else if (k == 1) {
+      const int slot = (b - S::KB) * 64 + lane;
+      const int d = slot / VCH, pc = slot % VCH;
+      off[j] = d * a.Tkp + (pc ^ ((d >> 1) & 7)) * 8;
     }
+  }
+  const uint16_t* kbase = a.k + (int64_t)kvh * D;
+  const uint16_t* vbase = a.vt + (int64_t)kvh * D * a.Tkp;
+  auto issue = [&](int kt, int st) {
+    u32x4* stg = smem + st * STAGE;
+    const uint16_t* ks_ = kbase + (int64_t)kt * kstride;
+    const uint16_t* vs_ = vbase + kt;
+    int o2[NBW];
+    const bool tail = kt + BN > k1;  // keys past k1 (masked) are clamped to k1-1
 #pragma unroll
-    for (int i = 0; i < VLD; ++i) {
-      int c = tid + i * NT;
-      int d = c / VCH, cc = c % VCH;
-      stV[i] = *(const u32x4*)(a.vt + ((int64_t)kvh * D + d) * a.Tkp + kt + cc * 8);
+    for (int j = 0; j < NBW; ++j) {
+      o2[j] = off[j];
+      if (S::kind(w + 4 * j) == 0 && tail)
+        o2[j] += (min(kt + key_of[j], k1 - 1) - kt - key_of[j]) * kstride;
     }
-  };
-  auto store_tile = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < KLD; ++i) {
-      int c = tid + i * NT;
-      sK[buf][swz<KCH>(c / KCH, c % KCH)] = stK[i];
-    }
-#pragma unroll
-    for (int i = 0; i < VLD; ++i) {
-      int c = tid + i * NT;
-      sV[buf][swz<VCH>(c / VCH, c % VCH)] = stV[i];
+    switch (w) {
+      case 0: fwd_issue<D, 0>(ks_, vs_, o2, stg, smem + S::JUNK); break;
+      case 1: fwd_issue<D, 1>(ks_, vs_, o2, stg, smem + S::JUNK); break;
+      case 2: fwd_issue<D, 2>(ks_, vs_, o2, stg, smem + S::JUNK); break;
+      default: fwd_issue<D, 3>(ks_, vs_, o2, stg, smem + S::JUNK); break;
     }
   };
 
-  if (n_tiles > 0) {
-    load_tile(kt_first);
-    store_tile(0);
-  }
+  if (n_tiles > 0) issue(kt_first, 0);
+  wait_vmcnt<0>();
   __syncthreads();
 
-  const int prow = perm32(l32);
-  int buf = 0;
+  // lane-constant LDS chunk indices of the fragments
+  const int kf_base = perm32(l32) * RS + hh;
+  int vf_base[4];
+#pragma unroll
+  for (int ks = 0; ks < 4; ++ks) vf_base[ks] = S::OFF_V + l32 * VCH + ((ks * 2 + hh) ^ ((l32 >> 1) & 7));
+
+  int st = 0;
   for (int n = 0; n < n_tiles; ++n) {
     const int kt = kt_first + n * BN;
-    if (n + 1 < n_tiles) load_tile(kt + BN);
+    const u32x4* stg = smem + st * STAGE;
+    if (n + 1 < n_tiles) issue(kt + BN, st ^ 1);
 
     // ---- S^T = K Q^T for the two 32-key halves of the tile
     f32x16 s[2];
 #pragma unroll
-    for (int g = 0; g < 2; ++g) {
+    for (int g = 0; g < 2; ++g)
 #pragma unroll
       for (int r = 0; r < 16; ++r) s[g][r] = 0.f;
+    __builtin_amdgcn_s_setprio(1);
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        u32x4 af = sK[buf][swz<KCH>(g * 32 + prow, ks * 2 + hh)];
-        s[g] = mfma32(af, qf[ks], s[g]);
-      }
-    }
+    for (int g = 0; g < 2; ++g)
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) s[g] = mfma32(stg[kf_base + g * 32 * RS + ks * 2], qf[ks], s[g]);
+    __builtin_amdgcn_s_setprio(0);
 
     // ---- mask (only on edge / diagonal tiles)
     const bool need_mask = (kt < k0) || (kt + BN > k1) || (a.causal && kt + BN - 1 > q0 + delta);
@@ -142,12 +186,16 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_kernel(FwdArgs a) {
     }
 
     // ---- online softmax (lazy rescale)
-    float mx = neg_inf();
+    // tree reductions keep the dependency chains short
+    float mx8[8];
 #pragma unroll
-    for (int g = 0; g < 2; ++g)
+    for (int i = 0; i < 8; ++i)
+      mx8[i] = fmaxf(fmaxf(s[0][i], s[0][i + 8]), fmaxf(s[1][i], s[1][i + 8]));
 #pragma unroll
-      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[g][r]);
-    mx = wave_max_xor32(mx);
+    for (int w2 = 4; w2 >= 1; w2 >>= 1)
+#pragma unroll
+      for (int i = 0; i < w2; ++i) mx8[i] = fmaxf(mx8[i], mx8[i + w2]);
+    const float mx = wave_max_xor32(mx8[0]);
     const float m_new = fmaxf(m_run, mx);
     const bool need = (m_new - m_run) * c2 > 8.f;  // NaN (both -inf) -> false
     if (__ballot(need)) {
@@ -161,30 +209,31 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_kernel(FwdArgs a) {
     }
     const float msc = (m_run == neg_inf()) ? 0.f : m_run * c2;
     u32x4 pb[4];
+    float ps[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int g = 0; g < 2; ++g) {
       float p[16];
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         p[r] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[g][r], c2, -msc));
-        l_part += p[r];
+        ps[r & 3] += p[r];
       }
       pb[2 * g] = pack_bf16x8(p[0], p[1], p[2], p[3], p[4], p[5], p[6], p[7]);
       pb[2 * g + 1] = pack_bf16x8(p[8], p[9], p[10], p[11], p[12], p[13], p[14], p[15]);
     }
+    l_part += (ps[0] + ps[1]) + (ps[2] + ps[3]);
 
     // ---- O^T += V^T P^T
+    __builtin_amdgcn_s_setprio(1);
 #pragma unroll
     for (int d = 0; d < DB; ++d)
 #pragma unroll
-      for (int ks = 0; ks < 4; ++ks) {
-        u32x4 af = sV[buf][swz<VCH>(d * 32 + l32, ks * 2 + hh)];
-        oacc[d] = mfma32(af, pb[ks], oacc[d]);
-      }
+      for (int ks = 0; ks < 4; ++ks) oacc[d] = mfma32(stg[vf_base[ks] + d * 32 * VCH], pb[ks], oacc[d]);
+    __builtin_amdgcn_s_setprio(0);
 
-    if (n + 1 < n_tiles) store_tile(buf ^ 1);
+    wait_vmcnt<0>();  // tile n+1 has landed
     __syncthreads();
-    buf ^= 1;
+    st ^= 1;
   }
 
   // ---- epilogue
