@@ -55,14 +55,16 @@ SP_DEV int c_row_of(int r, int h) { return ((r >> 3) << 4) + (h << 3) + (r & 7);
 // read the same logical chunk of 8 different rows hit distinct banks.
 // `nch` = 16-byte chunks per row (8 or 16).
 template <int NCH>
-SP_DEV int swz(int row, int chunk) {
+SP_DEV int swz_chunk(int row, int chunk) {
   if constexpr (NCH >= 16) {
-    return row * NCH + (chunk ^ (row & 15));
+    return chunk ^ (row & 15);
   } else {
     // two 128-byte rows share one 256-byte bank window
-    return row * NCH + (chunk ^ ((row >> 1) & 7));
+    return chunk ^ ((row >> 1) & 7);
   }
 }
+template <int NCH>
+SP_DEV int swz(int row, int chunk) { return row * NCH + swz_chunk<NCH>(row, chunk); }
 
 SP_DEV float wave_max_xor32(float x) { return fmaxf(x, __shfl_xor(x, 32)); }
 SP_DEV float wave_sum_xor32(float x) { return x + __shfl_xor(x, 32); }

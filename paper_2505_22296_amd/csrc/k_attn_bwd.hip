@@ -33,42 +33,32 @@ constexpr int NT = 256;
 SP_DEV int swz4(int row, int chunk) { return row * 4 + (chunk ^ ((row >> 2) & 3)); }
 
 // ------------------------------------------------------------------- dQ
-// LDS stage: K and V tiles [32 keys][D] with a padded row stride, K^T tile
-// [D][32 keys] with the 4-chunk XOR swizzle; filled by DMA three tiles deep.
+// Workgroup = NWQ wavefronts = 32*NWQ query rows of one head.  LDS stage:
+// K and V tiles [32 keys][D] (chunk XOR swizzle swz<>) and the K^T tile
+// [D][32 keys] (swz4), filled by DMA in 1 KB blocks spread over the
+// wavefronts; NSTQ tiles resident, barrier every TPBQ tiles.
+constexpr int NWQ = kDqWaves, NTQ = 64 * NWQ, NSTQ = kDqStages, TPBQ = kDqTilesPerSync;
+static_assert(kDqBM == 32 * NWQ && NSTQ % TPBQ == 0 && NSTQ >= 2 * TPBQ, "dq tiling");
+
 template <int D>
 struct DqStage {
   static constexpr int BN = kDqBN;
-  static constexpr int KCH = D / 8, RS = KCH + 1;
-  static constexpr int RSLOT = BN * RS;
-  static constexpr int RB = (RSLOT + 63) / 64;  // 1 KB blocks of a padded row tile
-  static constexpr int TB = D / 16;             // 1 KB blocks of the K^T tile
-  static constexpr int NB = 2 * RB + TB, NBW = (NB + 3) / 4;
-  static constexpr int OFF_V = RB * 64, OFF_T = 2 * RB * 64, STAGE = OFF_T + TB * 64;
-  static constexpr int NST = 3;
-  static constexpr int JUNK = NST * STAGE, SMEM = JUNK + 64;
-  static constexpr int kind(int b) { return b < RB ? 0 : b < 2 * RB ? 1 : b < NB ? 2 : 3; }
-  static constexpr int lds_off(int b) {
-    return b < RB ? b * 64 : b < 2 * RB ? OFF_V + (b - RB) * 64 : OFF_T + (b - 2 * RB) * 64;
-  }
+  static constexpr int KCH = D / 8;
+  static constexpr int RB = BN * KCH / 64;       // 1 KB blocks of a row-major tile
+  static constexpr int TB = D * (BN / 8) / 64;   // 1 KB blocks of the K^T tile
+  static constexpr int NB = 2 * RB + TB;
+  static constexpr int NBW = (NB + NWQ - 1) / NWQ;  // blocks per wavefront (tail ones junk)
+  static constexpr int OFF_V = RB * 64, OFF_T = 2 * RB * 64, STAGE = NB * 64;
+  static constexpr int JUNK = NSTQ * STAGE, SMEM = JUNK + 64;
+  // 0 = K, 1 = V, 2 = K^T, 3 = unused slot (copied to the junk block)
+  static SP_DEV int kind(int b) { return b < RB ? 0 : b < 2 * RB ? 1 : b < NB ? 2 : 3; }
 };
 
-template <int D, int W>
-SP_DEV void dq_issue(const uint16_t* ksrc, const uint16_t* vsrc, const uint16_t* tsrc,
-                     const int (&off)[DqStage<D>::NBW], u32x4* stg, u32x4* junk) {
-  using S = DqStage<D>;
-#pragma unroll
-  for (int j = 0; j < S::NBW; ++j) {
-    const int b = W + 4 * j;
-    const int k = S::kind(b);
-    dma16((k == 1 ? vsrc : k == 2 ? tsrc : ksrc) + off[j], k == 3 ? junk : stg + S::lds_off(b));
-  }
-}
-
 template <int D>
-__global__ __launch_bounds__(NT, 2) void attn_dq_kernel(DqArgs a) {
+__global__ __launch_bounds__(NTQ, 1) void attn_dq_kernel(DqArgs a) {
   using S = DqStage<D>;
-  constexpr int BN = S::BN, KS = D / 16, DB = D / 32, KCH = S::KCH, RS = S::RS;
-  constexpr int NBW = S::NBW, NST = S::NST, STAGE = S::STAGE;
+  constexpr int BN = S::BN, KS = D / 16, DB = D / 32, KCH = S::KCH;
+  constexpr int NBW = S::NBW, STAGE = S::STAGE;
 
   __shared__ u32x4 smem[S::SMEM];
 
@@ -81,6 +71,10 @@ __global__ __launch_bounds__(NT, 2) void attn_dq_kernel(DqArgs a) {
   const int row = q0 + w * 32 + l32;
   const bool row_ok = row < q1;
   const int lrow = row_ok ? row : q0;
+  const int wave_rows = min(32, q1 - q0 - w * 32);
+  const int wave_kmax = wave_rows <= 0 ? -1
+                        : a.causal     ? min(k1, q0 + w * 32 + wave_rows + delta)
+                                       : k1;
 
   u32x4 qf[KS], df[KS];
   {
@@ -105,100 +99,123 @@ __global__ __launch_bounds__(NT, 2) void attn_dq_kernel(DqArgs a) {
   const int kt_first = k0 & ~7;
   const int n_tiles = (k1 > k0) ? (k1 - kt_first + BN - 1) / BN : 0;
 
+  // Per-lane, tile-independent element offsets of this wavefront's DMA blocks
+  // w + NWQ*j (the block kinds are wave-uniform).
   const int kstride = a.Hkv * D;
   int off[NBW], key_of[NBW];
 #pragma unroll
   for (int j = 0; j < NBW; ++j) {
-    const int b = w + 4 * j;
+    const int b = w + NWQ * j;
     const int k = S::kind(b);
     off[j] = 0;
     key_of[j] = 0;
     if (k == 0 || k == 1) {
       const int slot = (k == 0 ? b : b - S::RB) * 64 + lane;
-      const int r = min(slot / RS, BN - 1);
+      const int r = slot / KCH;
       key_of[j] = r;
-      off[j] = r * kstride + min(slot % RS, KCH - 1) * 8;
+      off[j] = r * kstride + swz_chunk<KCH>(r, slot % KCH) * 8;
     } else if (k == 2) {
-      const int dim = (b - 2 * S::RB) * 16 + lane / 4;
-      off[j] = dim * a.Tkp + ((lane % 4) ^ ((dim >> 2) & 3)) * 8;
+      const int slot = (b - 2 * S::RB) * 64 + lane;
+      const int dim = slot / 4;
+      off[j] = dim * a.Tkp + ((slot % 4) ^ ((dim >> 2) & 3)) * 8;
     }
   }
   const uint16_t* kbase = a.k + (int64_t)kvh * D;
   const uint16_t* vbase = a.v + (int64_t)kvh * D;
   const uint16_t* tbase = a.kt + (int64_t)kvh * D * a.Tkp;
-  auto issue = [&](int kt, int st) {
-    u32x4* stg = smem + st * STAGE;
+  auto issue = [&](int n) {
+    const int kt = kt_first + n * BN;
+    u32x4* stg = smem + (n % NSTQ) * STAGE;
     const int64_t rowoff = (int64_t)kt * kstride;
-    int o2[NBW];
     const bool tail = kt + BN > k1;  // keys past k1 (masked) are clamped to k1-1
 #pragma unroll
     for (int j = 0; j < NBW; ++j) {
-      const int k = S::kind(w + 4 * j);
-      o2[j] = off[j];
-      if ((k == 0 || k == 1) && tail)
-        o2[j] += (min(kt + key_of[j], k1 - 1) - kt - key_of[j]) * kstride;
-    }
-    switch (w) {
-      case 0: dq_issue<D, 0>(kbase + rowoff, vbase + rowoff, tbase + kt, o2, stg, smem + S::JUNK); break;
-      case 1: dq_issue<D, 1>(kbase + rowoff, vbase + rowoff, tbase + kt, o2, stg, smem + S::JUNK); break;
-      case 2: dq_issue<D, 2>(kbase + rowoff, vbase + rowoff, tbase + kt, o2, stg, smem + S::JUNK); break;
-      default: dq_issue<D, 3>(kbase + rowoff, vbase + rowoff, tbase + kt, o2, stg, smem + S::JUNK); break;
+      const int b = w + NWQ * j;
+      const int k = S::kind(b);
+      int o = off[j];
+      if ((k == 0 || k == 1) && tail) o += (min(kt + key_of[j], k1 - 1) - kt - key_of[j]) * kstride;
+      const uint16_t* src = k == 0 ? kbase + rowoff : k == 1 ? vbase + rowoff : k == 2 ? tbase + kt : kbase;
+      dma16(src + o, k == 3 ? smem + S::JUNK : stg + b * 64);
     }
   };
+  auto wait_tiles = [&](int pending) {
+    if constexpr (NSTQ - 2 * TPBQ >= 2) {
+      if (pending >= 2) { wait_vmcnt<2 * NBW>(); return; }
+    }
+    if constexpr (NSTQ - 2 * TPBQ >= 1) {
+      if (pending == 1) { wait_vmcnt<NBW>(); return; }
+    }
+    wait_vmcnt<0>();
+  };
 
-  // Three LDS stages, two tiles in flight: at the top of iteration n the
-  // barrier publishes tile n and retires every read of tile n-1, whose stage
-  // then receives tile n+2.
-  if (n_tiles > 0) issue(kt_first, 0);
-  if (n_tiles > 1) issue(kt_first + BN, 1);
-  const int kf_base = perm32(l32) * RS + hh;
-  const int t0_base = S::OFF_T + swz4(l32, hh), t1_base = S::OFF_T + swz4(l32, 2 + hh);
-  int st = 0;
-  for (int n = 0; n < n_tiles; ++n) {
-    const int kt = kt_first + n * BN;
-    if (n + 1 < n_tiles) wait_vmcnt<NBW>(); else wait_vmcnt<0>();
-    __syncthreads();
-    if (n + 2 < n_tiles) issue(kt + 2 * BN, st == 0 ? NST - 1 : st - 1);
-    const u32x4* stg = smem + st * STAGE;
-    st = (st == NST - 1) ? 0 : st + 1;
+  // lane-constant LDS chunk indices of the fragments
+  int kf_idx[KS];
+  {
+    const int kr = perm32(l32);
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) kf_idx[ks] = kr * KCH + swz_chunk<KCH>(kr, ks * 2 + hh);
+  }
+  const int t0_idx = S::OFF_T + swz4(l32, hh), t1_idx = S::OFF_T + swz4(l32, 2 + hh);
 
-    f32x16 s, dp;
+  for (int n = 0; n < NSTQ - TPBQ && n < n_tiles; ++n) issue(n);
+
+  for (int n0 = 0; n0 < n_tiles; n0 += NSTQ) {
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      s[r] = 0.f;
-      dp[r] = 0.f;
-    }
-    __builtin_amdgcn_s_setprio(1);
+    for (int u = 0; u < NSTQ; ++u) {
+      const int n = n0 + u;
+      if (n >= n_tiles) break;
+      if (u % TPBQ == 0) {
+        // tiles n .. n+TPBQ-1 landed; the stages of tiles n-TPBQ .. n-1 are
+        // free and receive tiles n+NSTQ-TPBQ ..
+        const int issued = min(n_tiles, n + NSTQ - TPBQ);
+        wait_tiles(issued - min(n_tiles, n + TPBQ));
+        __syncthreads();
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      s = mfma32(stg[kf_base + ks * 2], qf[ks], s);
-      dp = mfma32(stg[S::OFF_V + kf_base + ks * 2], df[ks], dp);
-    }
-    __builtin_amdgcn_s_setprio(0);
-    float ds[16];
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[r], c2, -l2));
-      ds[r] = p * (dp[r] - drow);
-    }
-    const bool need_mask = (kt < k0) | (kt + BN > k1) | (a.causal & (kt + BN - 1 > q0 + delta));
-    if (need_mask) {
+        for (int t = 0; t < TPBQ; ++t)
+          if (n + NSTQ - TPBQ + t < n_tiles) issue(n + NSTQ - TPBQ + t);
+      }
+      const int kt = kt_first + n * BN;
+      if (kt >= wave_kmax) continue;  // wholly past this wavefront's rows
+      const u32x4* stg = smem + u * STAGE;
+
+      f32x16 s, dp;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        int key = kt + c_row_of(r, hh);
-        bool ok = key >= k0 && key < k1 && (!a.causal || key <= row + delta);
-        ds[r] = ok ? ds[r] : 0.f;
+        s[r] = 0.f;
+        dp[r] = 0.f;
       }
-    }
-    u32x4 b0 = pack_bf16x8(ds[0], ds[1], ds[2], ds[3], ds[4], ds[5], ds[6], ds[7]);
-    u32x4 b1 = pack_bf16x8(ds[8], ds[9], ds[10], ds[11], ds[12], ds[13], ds[14], ds[15]);
-    __builtin_amdgcn_s_setprio(1);
+      __builtin_amdgcn_s_setprio(1);
 #pragma unroll
-    for (int d = 0; d < DB; ++d) {
-      acc[d] = mfma32(stg[t0_base + d * 128], b0, acc[d]);
-      acc[d] = mfma32(stg[t1_base + d * 128], b1, acc[d]);
+      for (int ks = 0; ks < KS; ++ks) {
+        s = mfma32(stg[kf_idx[ks]], qf[ks], s);
+        dp = mfma32(stg[S::OFF_V + kf_idx[ks]], df[ks], dp);
+      }
+      __builtin_amdgcn_s_setprio(0);
+      const bool need_mask = (kt < k0) | (kt + BN > k1) | (a.causal & (kt + BN - 1 > q0 + w * 32 + delta));
+      if (need_mask) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          int key = kt + c_row_of(r, hh);
+          bool ok = key >= k0 && key < k1 && (!a.causal || key <= row + delta);
+          s[r] = ok ? s[r] : neg_inf();
+        }
+      }
+      float ds[16];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[r], c2, -l2));
+        ds[r] = p * (dp[r] - drow);
+      }
+      u32x4 b0 = pack_bf16x8(ds[0], ds[1], ds[2], ds[3], ds[4], ds[5], ds[6], ds[7]);
+      u32x4 b1 = pack_bf16x8(ds[8], ds[9], ds[10], ds[11], ds[12], ds[13], ds[14], ds[15]);
+      __builtin_amdgcn_s_setprio(1);
+#pragma unroll
+      for (int d = 0; d < DB; ++d) {
+        acc[d] = mfma32(stg[t0_idx + d * 128], b0, acc[d]);
+        acc[d] = mfma32(stg[t1_idx + d * 128], b1, acc[d]);
+      }
+      __builtin_amdgcn_s_setprio(0);
     }
-    __builtin_amdgcn_s_setprio(0);
   }
 
   if (!row_ok) return;
@@ -447,14 +464,23 @@ void attn_dkdv_kernel(DkdvArgs a) {
     // chunk needs masking if it straddles the item's row range, the key
     // tile's end, or the causal diagonal of this wavefront's keys
     const int wk0 = k0 + w * 32;
-    const bool need_mask = (qc < qb) || (qc + BQ > qe) || (wk0 + 32 > k1) ||
-                           (a.causal && wk0 + 31 > qc + delta);
+    const bool need_mask = (qc < qb) | (qc + BQ > qe) | (wk0 + 32 > k1) |
+                           (a.causal & (wk0 + 31 > qc + delta));
     // visible chunk rows for this lane's key: lo <= row-in-chunk < hi
     int lo = qb - qc, hi = qe - qc;
     if (a.causal) lo = max(lo, key - delta - qc);
     if (!key_ok) hi = lo;
     lo -= hh * 8;
     hi -= hh * 8;
+    // masked scores become -inf, so P (and dS) vanish there; the block is
+    // branched over on all but edge and diagonal chunks
+    if (need_mask) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int br = (r >> 3) * 16 + (r & 7);  // chunk row minus hh*8
+        s[r] = (br >= lo && br < hi) ? s[r] : neg_inf();
+      }
+    }
     const f32x4* vL = (const f32x4*)(stg + OFF_LD);
     const f32x4* vD = vL + BQ / 4;
     u32x4 pb[2], db[2];
@@ -472,13 +498,8 @@ void attn_dkdv_kernel(DkdvArgs a) {
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
         const int r = half * 8 + i;
-        float pv = __builtin_amdgcn_exp2f(__builtin_fmaf(s[r], c2, -Lr[i]));
-        if (need_mask) {
-          const int br = half * 16 + i;  // chunk row minus hh*8
-          pv = (br >= lo && br < hi) ? pv : 0.f;
-        }
-        p[i] = pv;
-        if constexpr (DO_K) ds[i] = pv * (dp[r] - Dr[i]);
+        p[i] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[r], c2, -Lr[i]));
+        if constexpr (DO_K) ds[i] = p[i] * (dp[r] - Dr[i]);
       }
       if constexpr (DO_V) pb[half] = pack_bf16x8(p[0], p[1], p[2], p[3], p[4], p[5], p[6], p[7]);
       if constexpr (DO_K)
@@ -536,8 +557,8 @@ void attn_dkdv_kernel(DkdvArgs a) {
 
 hipError_t launch_attn_dq(const DqArgs& a, int n_items, int D, hipStream_t st) {
   if (n_items <= 0) return hipSuccess;
-  if (D == 128) return sp_launch(kKDq, attn_dq_kernel<128>, dim3(n_items), dim3(NT), st, a);
-  return sp_launch(kKDq, attn_dq_kernel<64>, dim3(n_items), dim3(NT), st, a);
+  if (D == 128) return sp_launch(kKDq, attn_dq_kernel<128>, dim3(n_items), dim3(NTQ), st, a);
+  return sp_launch(kKDq, attn_dq_kernel<64>, dim3(n_items), dim3(NTQ), st, a);
 }
 
 hipError_t launch_attn_dkdv(const DkdvArgs& a, int n_items, int D, hipStream_t st) {

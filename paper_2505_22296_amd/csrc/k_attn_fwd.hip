@@ -1,10 +1,12 @@
 // Attention forward for one SP rank's real heads on gfx950.
 //
-// One workgroup = 4 wavefronts = 128 query rows of one head (a work item from
+// One workgroup = 8 wavefronts = 256 query rows of one head (a work item from
 // the host block-skip scheduler); wavefront w owns rows q_begin + 32w ..
-// +32.  The key loop walks 64-key tiles of the segment, staged in LDS
-// (K row-major, V transposed) with double buffering and register
-// prefetch of the next tile.
+// +32.  The key loop walks 64-key tiles of the segment.  Tiles are copied
+// global -> LDS by DMA (K row-major, V transposed, both with an XOR swizzle
+// of their 16-byte chunks and no padding), four tiles resident: while a pair
+// of tiles is consumed the next pair lands, and the eight wavefronts meet at
+// a barrier once per pair.  Each tile is shared by all eight wavefronts.
 //
 // Per 64-key tile and wavefront:
 //   S^T = K Q^T      (32x32x16 bf16 MFMA; Q^T kept in registers as B operand)
@@ -16,7 +18,8 @@
 //                     consecutive keys, i.e. a B operand k-slice)
 // The running max is only raised when it grows by more than 2^8 (exact:
 // the final normalisation uses the same max).  Masking is evaluated only on
-// tiles that straddle a segment edge or the causal diagonal.
+// tiles that straddle a segment edge or the causal diagonal; a wavefront
+// skips the arithmetic of tiles that lie wholly past its causal diagonal.
 //
 // The ring variant (MERGE) folds the chunk's normalised (O_c, LSE_c) into
 // float32 accumulators with the log-sum-exp rule in the epilogue.
@@ -27,46 +30,35 @@ namespace spk {
 
 namespace {
 
-constexpr int BM = kFwdBM;  // 128 rows per workgroup
-constexpr int BN = kFwdBN;  // 64 keys per tile
-constexpr int NT = 256;
+constexpr int NW = kFwdWaves;         // wavefronts per workgroup
+constexpr int BM = kFwdBM;            // query rows per workgroup
+constexpr int BN = kFwdBN;            // keys per tile
+constexpr int NT = 64 * NW;
+constexpr int NST = kFwdStages;       // resident tiles
+constexpr int TPB = kFwdTilesPerSync; // tiles per barrier
+static_assert(BM == 32 * NW && NST % TPB == 0 && NST >= 2 * TPB, "fwd tiling");
 
-// LDS stage of the forward: K tile [BN][D] with a padded row stride (one base
-// address per lane, k-steps are immediate offsets) and V^T tile [D][BN] with
-// an XOR swizzle of its 8 chunks per row; both filled by DMA.
+// LDS stage of the forward: K tile [BN][D] and V^T tile [D][BN], both
+// row-major with the chunk XOR swizzle swz<>, filled by DMA in 1 KB blocks.
 template <int D>
 struct FwdStage {
-  static constexpr int KCH = D / 8, RS = KCH + 1;
-  static constexpr int KSLOT = BN * RS;
-  static constexpr int KB = (KSLOT + 63) / 64;  // 1 KB blocks of the K tile
-  static constexpr int VCH = BN / 8;            // chunks per V^T row
-  static constexpr int VB = D * VCH / 64;       // 1 KB blocks of the V^T tile
-  static constexpr int NB = KB + VB, NBW = (NB + 3) / 4;
-  static constexpr int OFF_V = KB * 64, STAGE = OFF_V + VB * 64;  // 16-byte chunks
-  static constexpr int NST = 2;
-  static constexpr int JUNK = NST * STAGE, SMEM = JUNK + 64;
-  static constexpr int kind(int b) { return b < KB ? 0 : b < NB ? 1 : 2; }
-  static constexpr int lds_off(int b) { return b < KB ? b * 64 : OFF_V + (b - KB) * 64; }
+  static constexpr int KCH = D / 8;            // chunks per K row
+  static constexpr int VCH = BN / 8;           // chunks per V^T row
+  static constexpr int KB = BN * KCH / 64;     // 1 KB blocks of the K tile
+  static constexpr int VB = D * VCH / 64;      // 1 KB blocks of the V^T tile
+  static constexpr int NB = KB + VB;
+  static constexpr int NBW = NB / NW;          // blocks per wavefront
+  static_assert(KB % NW == 0 && VB % NW == 0, "DMA blocks per wavefront");
+  static constexpr int OFF_V = KB * 64, STAGE = NB * 64;  // 16-byte chunks
+  static constexpr int SMEM = NST * STAGE;
 };
 
-template <int D, int W>
-SP_DEV void fwd_issue(const uint16_t* ksrc, const uint16_t* vsrc,
-                      const int (&off)[FwdStage<D>::NBW], u32x4* stg, u32x4* junk) {
-  using S = FwdStage<D>;
-#pragma unroll
-  for (int j = 0; j < S::NBW; ++j) {
-    const int b = W + 4 * j;
-    const int k = S::kind(b);
-    dma16((k == 1 ? vsrc : ksrc) + off[j], k == 2 ? junk : stg + S::lds_off(b));
-  }
-}
-
 template <int D, bool MERGE>
-__global__ __launch_bounds__(NT, 2) void attn_fwd_kernel(FwdArgs a) {
+__global__ __launch_bounds__(NT, 1) void attn_fwd_kernel(FwdArgs a) {
   using S = FwdStage<D>;
   constexpr int KS = D / 16;   // MFMA k-steps over D
   constexpr int DB = D / 32;   // 32-dim blocks of O^T
-  constexpr int KCH = S::KCH, RS = S::RS, VCH = S::VCH, NBW = S::NBW, STAGE = S::STAGE;
+  constexpr int KCH = S::KCH, VCH = S::VCH, NBW = S::NBW, NBK = NBW / 2, STAGE = S::STAGE;
 
   __shared__ u32x4 smem[S::SMEM];
 
@@ -78,6 +70,11 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_kernel(FwdArgs a) {
   const int lane = tid & 63, hh = lane >> 5, l32 = lane & 31;
   const int row = q0 + w * 32 + l32;
   const bool row_ok = row < q1;
+  // last key any row of this wavefront may see (tiles past it are skipped)
+  const int wave_rows = min(32, q1 - q0 - w * 32);
+  const int wave_kmax = wave_rows <= 0 ? -1
+                        : a.causal     ? min(k1, q0 + w * 32 + wave_rows + delta)
+                                       : k1;
 
   // Q^T as B operand: lane holds query row `row`, dims ks*16 + hh*8 + [0..7].
   u32x4 qf[KS];
@@ -101,139 +98,157 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_kernel(FwdArgs a) {
   const int kt_first = k0 & ~7;
   const int n_tiles = (k1 > k0) ? (k1 - kt_first + BN - 1) / BN : 0;
 
-  // per-lane, tile-independent element offsets of this wave's DMA slots
+  // Per-lane, tile-independent element offsets of this wavefront's DMA
+  // blocks: blocks w + NW*j, the first NBK of them in the K tile.
   const int kstride = a.Hkv * D;
-  int off[NBW], key_of[NBW];
+  int off[NBW], key_of[NBK];
 #pragma unroll
   for (int j = 0; j < NBW; ++j) {
-    const int b = w + 4 * j;
-    const int k = S::kind(b);
-    off[j] = 0;
-    key_of[j] = 0;
-    if (k == 0) {
-      const int slot = b * 64 + lane;
-      const int r = min(slot / RS, BN - 1);
+    const int slot = (w + NW * j) * 64 + lane;
+    if (j < NBK) {
+      const int r = slot / KCH, pc = slot % KCH;
       key_of[j] = r;
-      off[j] = r * kstride + min(slot % RS, KCH - 1) * 8;
-    } else if (k == 1) {
-      const int slot = (b - S::KB) * 64 + lane;
-      const int d = slot / VCH, pc = slot % VCH;
-      off[j] = d * a.Tkp + (pc ^ ((d >> 1) & 7)) * 8;
+      off[j] = r * kstride + swz_chunk<KCH>(r, pc) * 8;
+    } else {
+      const int vs = slot - S::OFF_V, d = vs / VCH, pc = vs % VCH;
+      off[j] = d * a.Tkp + swz_chunk<VCH>(d, pc) * 8;
     }
   }
   const uint16_t* kbase = a.k + (int64_t)kvh * D;
   const uint16_t* vbase = a.vt + (int64_t)kvh * D * a.Tkp;
-  auto issue = [&](int kt, int st) {
-    u32x4* stg = smem + st * STAGE;
+  auto issue = [&](int n) {
+    const int kt = kt_first + n * BN;
+    u32x4* stg = smem + (n % NST) * STAGE + w * 64;
     const uint16_t* ks_ = kbase + (int64_t)kt * kstride;
     const uint16_t* vs_ = vbase + kt;
-    int o2[NBW];
     const bool tail = kt + BN > k1;  // keys past k1 (masked) are clamped to k1-1
 #pragma unroll
     for (int j = 0; j < NBW; ++j) {
-      o2[j] = off[j];
-      if (S::kind(w + 4 * j) == 0 && tail)
-        o2[j] += (min(kt + key_of[j], k1 - 1) - kt - key_of[j]) * kstride;
-    }
-    switch (w) {
-      case 0: fwd_issue<D, 0>(ks_, vs_, o2, stg, smem + S::JUNK); break;
-      case 1: fwd_issue<D, 1>(ks_, vs_, o2, stg, smem + S::JUNK); break;
-      case 2: fwd_issue<D, 2>(ks_, vs_, o2, stg, smem + S::JUNK); break;
-      default: fwd_issue<D, 3>(ks_, vs_, o2, stg, smem + S::JUNK); break;
+      if (j < NBK) {
+        int o = off[j];
+        if (tail) o += (min(kt + key_of[j], k1 - 1) - kt - key_of[j]) * kstride;
+        dma16(ks_ + o, stg + NW * j * 64);
+      } else {
+        dma16(vs_ + off[j], stg + NW * j * 64);
+      }
     }
   };
+  // Wait until at most `pending` issued tiles are still in flight.
+  auto wait_tiles = [&](int pending) {
+    if constexpr (NST - 2 * TPB >= 2) {
+      if (pending >= 2) { wait_vmcnt<2 * NBW>(); return; }
+    }
+    if constexpr (NST - 2 * TPB >= 1) {
+      if (pending == 1) { wait_vmcnt<NBW>(); return; }
+    }
+    wait_vmcnt<0>();
+  };
 
-  if (n_tiles > 0) issue(kt_first, 0);
-  wait_vmcnt<0>();
-  __syncthreads();
+  // lane-constant LDS chunk indices of the fragments (the swizzle of a K row
+  // is the same for the two 32-key halves and of a V^T row for all 32-dim
+  // blocks, so those are immediate offsets)
+  int kf_idx[KS], vf_idx[4];
+  {
+    const int kr = perm32(l32);
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) kf_idx[ks] = kr * KCH + swz_chunk<KCH>(kr, ks * 2 + hh);
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) vf_idx[ks] = S::OFF_V + l32 * VCH + swz_chunk<VCH>(l32, ks * 2 + hh);
+  }
 
-  // lane-constant LDS chunk indices of the fragments
-  const int kf_base = perm32(l32) * RS + hh;
-  int vf_base[4];
-#pragma unroll
-  for (int ks = 0; ks < 4; ++ks) vf_base[ks] = S::OFF_V + l32 * VCH + ((ks * 2 + hh) ^ ((l32 >> 1) & 7));
+  for (int n = 0; n < NST - TPB && n < n_tiles; ++n) issue(n);
 
-  int st = 0;
-  for (int n = 0; n < n_tiles; ++n) {
-    const int kt = kt_first + n * BN;
-    const u32x4* stg = smem + st * STAGE;
-    if (n + 1 < n_tiles) issue(kt + BN, st ^ 1);
+  for (int n0 = 0; n0 < n_tiles; n0 += NST) {
+#pragma unroll
+    for (int u = 0; u < NST; ++u) {
+      const int n = n0 + u;
+      if (n >= n_tiles) break;
+      if (u % TPB == 0) {
+        // tiles n .. n+TPB-1 landed; every wavefront is done with the stages
+        // of tiles n-TPB .. n-1, which receive tiles n+NST-TPB ..
+        const int issued = min(n_tiles, n + NST - TPB);
+        wait_tiles(issued - min(n_tiles, n + TPB));
+        __syncthreads();
+#pragma unroll
+        for (int t = 0; t < TPB; ++t)
+          if (n + NST - TPB + t < n_tiles) issue(n + NST - TPB + t);
+      }
+      const int kt = kt_first + n * BN;
+      if (kt >= wave_kmax) continue;  // wholly past this wavefront's rows
+      const u32x4* stg = smem + u * STAGE;
 
-    // ---- S^T = K Q^T for the two 32-key halves of the tile
-    f32x16 s[2];
-#pragma unroll
-    for (int g = 0; g < 2; ++g)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) s[g][r] = 0.f;
-    __builtin_amdgcn_s_setprio(1);
-#pragma unroll
-    for (int g = 0; g < 2; ++g)
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) s[g] = mfma32(stg[kf_base + g * 32 * RS + ks * 2], qf[ks], s[g]);
-    __builtin_amdgcn_s_setprio(0);
-
-    // ---- mask (only on edge / diagonal tiles)
-    const bool need_mask = (kt < k0) || (kt + BN > k1) || (a.causal && kt + BN - 1 > q0 + delta);
-    if (need_mask) {
+      // ---- S^T = K Q^T for the two 32-key halves of the tile
+      f32x16 s[2];
 #pragma unroll
       for (int g = 0; g < 2; ++g)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          int key = kt + g * 32 + c_row_of(r, hh);
-          bool ok = key >= k0 && key < k1 && (!a.causal || key <= row + delta);
-          if (!ok) s[g][r] = neg_inf();
-        }
-    }
+        for (int r = 0; r < 16; ++r) s[g][r] = 0.f;
+      __builtin_amdgcn_s_setprio(1);
+#pragma unroll
+      for (int g = 0; g < 2; ++g)
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) s[g] = mfma32(stg[kf_idx[ks] + g * 32 * KCH], qf[ks], s[g]);
+      __builtin_amdgcn_s_setprio(0);
 
-    // ---- online softmax (lazy rescale)
-    // tree reductions keep the dependency chains short
-    float mx8[8];
+      // ---- mask (only on edge / diagonal tiles)
+      const bool need_mask = (kt < k0) | (kt + BN > k1) | (a.causal & (kt + BN - 1 > q0 + w * 32 + delta));
+      if (need_mask) {
 #pragma unroll
-    for (int i = 0; i < 8; ++i)
-      mx8[i] = fmaxf(fmaxf(s[0][i], s[0][i + 8]), fmaxf(s[1][i], s[1][i + 8]));
+        for (int g = 0; g < 2; ++g)
 #pragma unroll
-    for (int w2 = 4; w2 >= 1; w2 >>= 1)
+          for (int r = 0; r < 16; ++r) {
+            int key = kt + g * 32 + c_row_of(r, hh);
+            bool ok = key >= k0 && key < k1 && (!a.causal || key <= row + delta);
+            if (!ok) s[g][r] = neg_inf();
+          }
+      }
+
+      // ---- online softmax (lazy rescale); tree reductions keep the
+      // dependency chains short
+      float mx8[8];
 #pragma unroll
-      for (int i = 0; i < w2; ++i) mx8[i] = fmaxf(mx8[i], mx8[i + w2]);
-    const float mx = wave_max_xor32(mx8[0]);
-    const float m_new = fmaxf(m_run, mx);
-    const bool need = (m_new - m_run) * c2 > 8.f;  // NaN (both -inf) -> false
-    if (__ballot(need)) {
-      float alpha = need ? exp2f((m_run - m_new) * c2) : 1.f;
-      if (need) m_run = m_new;
-      l_part *= alpha;
+      for (int i = 0; i < 8; ++i)
+        mx8[i] = fmaxf(fmaxf(s[0][i], s[0][i + 8]), fmaxf(s[1][i], s[1][i + 8]));
+#pragma unroll
+      for (int w2 = 4; w2 >= 1; w2 >>= 1)
+#pragma unroll
+        for (int i = 0; i < w2; ++i) mx8[i] = fmaxf(mx8[i], mx8[i + w2]);
+      const float mx = wave_max_xor32(mx8[0]);
+      const float m_new = fmaxf(m_run, mx);
+      const bool need = (m_new - m_run) * c2 > 8.f;  // NaN (both -inf) -> false
+      if (__ballot(need)) {
+        float alpha = need ? exp2f((m_run - m_new) * c2) : 1.f;
+        if (need) m_run = m_new;
+        l_part *= alpha;
+#pragma unroll
+        for (int d = 0; d < DB; ++d)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) oacc[d][r] *= alpha;
+      }
+      const float msc = (m_run == neg_inf()) ? 0.f : m_run * c2;
+      u32x4 pb[4];
+      float ps[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int g = 0; g < 2; ++g) {
+        float p[16];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          p[r] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[g][r], c2, -msc));
+          ps[r & 3] += p[r];
+        }
+        pb[2 * g] = pack_bf16x8(p[0], p[1], p[2], p[3], p[4], p[5], p[6], p[7]);
+        pb[2 * g + 1] = pack_bf16x8(p[8], p[9], p[10], p[11], p[12], p[13], p[14], p[15]);
+      }
+      l_part += (ps[0] + ps[1]) + (ps[2] + ps[3]);
+
+      // ---- O^T += V^T P^T
+      __builtin_amdgcn_s_setprio(1);
 #pragma unroll
       for (int d = 0; d < DB; ++d)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) oacc[d][r] *= alpha;
+        for (int ks = 0; ks < 4; ++ks) oacc[d] = mfma32(stg[vf_idx[ks] + d * 32 * VCH], pb[ks], oacc[d]);
+      __builtin_amdgcn_s_setprio(0);
     }
-    const float msc = (m_run == neg_inf()) ? 0.f : m_run * c2;
-    u32x4 pb[4];
-    float ps[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int g = 0; g < 2; ++g) {
-      float p[16];
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        p[r] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[g][r], c2, -msc));
-        ps[r & 3] += p[r];
-      }
-      pb[2 * g] = pack_bf16x8(p[0], p[1], p[2], p[3], p[4], p[5], p[6], p[7]);
-      pb[2 * g + 1] = pack_bf16x8(p[8], p[9], p[10], p[11], p[12], p[13], p[14], p[15]);
-    }
-    l_part += (ps[0] + ps[1]) + (ps[2] + ps[3]);
-
-    // ---- O^T += V^T P^T
-    __builtin_amdgcn_s_setprio(1);
-#pragma unroll
-    for (int d = 0; d < DB; ++d)
-#pragma unroll
-      for (int ks = 0; ks < 4; ++ks) oacc[d] = mfma32(stg[vf_base[ks] + d * 32 * VCH], pb[ks], oacc[d]);
-    __builtin_amdgcn_s_setprio(0);
-
-    wait_vmcnt<0>();  // tile n+1 has landed
-    __syncthreads();
-    st ^= 1;
   }
 
   // ---- epilogue

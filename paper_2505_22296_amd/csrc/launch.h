@@ -120,10 +120,16 @@ hipError_t launch_attn_dkdv(const DkdvArgs& a, int n_items, int D, hipStream_t s
 
 // Tile sizes the host scheduler must use (rows per fwd/dq item, keys per
 // dk/dv item) and the padding of transposed copies.
-static constexpr int kFwdBM = 128;
+static constexpr int kFwdWaves = 8;                 // wavefronts per forward workgroup
+static constexpr int kFwdBM = 32 * kFwdWaves;
 static constexpr int kFwdBN = 64;
-static constexpr int kDqBM = 128;
+static constexpr int kFwdStages = 4;                // K/V tiles resident in LDS
+static constexpr int kFwdTilesPerSync = 2;          // tiles between workgroup barriers
+static constexpr int kDqWaves = 8;                  // wavefronts per dQ workgroup
+static constexpr int kDqBM = 32 * kDqWaves;
 static constexpr int kDqBN = 32;
+static constexpr int kDqStages = 4;
+static constexpr int kDqTilesPerSync = 2;
 static constexpr int kDkdvBN = 128;
 static constexpr int kDkdvBQ = 32;
 static constexpr int kTransposePad = 64;
