@@ -4,13 +4,13 @@
 //   dP = dO V^T,  dS = P (dP - D),  dQ = scale dS K,
 //   dK = scale dS^T Q,  dV = P^T dO.
 //
-// dq kernel (query-stationary): workgroup = 128 query rows of one head,
+// dq kernel (query-stationary): workgroup = 256 query rows of one head,
 //   wavefront w owns 32 rows; per 32-key tile (K, V row-major and K^T staged
 //   in LDS):
 //     S^T = K Q^T, dP^T = V dO^T     (Q, dO rows kept as B operands)
 //     dS^T = P^T (dP^T - D)          (row statistics are per lane)
 //     dQ^T += K^T dS^T               (dS^T C registers used directly as B)
-// dk/dv kernel (key-stationary): workgroup = 128 keys of one KV head and
+// dk/dv kernels (key-stationary): workgroup = 256 keys of one KV head and
 //   one query head, wavefront w owns 32 keys (K, V rows as B operands in
 //   registers); per 32-row query chunk, visited last to first (Q, dO
 //   row-major and Q^T, dO^T staged in LDS):
@@ -237,70 +237,47 @@ __global__ __launch_bounds__(NTQ, 1) void attn_dq_kernel(DqArgs a) {
     }
 }
 
-// Static description of one dK/dV stage: which tiles it holds and where.
+// ---------------------------------------------------------------- dK / dV
+// Workgroup = NWK wavefronts = 32*NWK keys of one KV head and one query head.
+// LDS stage (one 32-row query chunk): Q [32][D] (always), dO [32][D] (dK),
+// Q^T [D][32] (dK), dO^T [D][32] (dV), the chunk's LSE*log2(e) and D rows;
+// row-major tiles use swz<>, transposed ones swz4.  NSTK chunks resident,
+// barrier every TPBK chunks.
+constexpr int NWK = kDkdvWaves, NTK = 64 * NWK, TPBK = kDkdvChunksPerSync;
+static_assert(kDkdvBN == 32 * NWK, "dkdv tiling");
+
 template <int D, int MODE>
 struct DkdvStage {
-  static constexpr bool DO_V = MODE != 2, DO_K = MODE != 1;
+  static constexpr bool DO_V = MODE == 1, DO_K = MODE == 2;
   static constexpr int BQ = kDkdvBQ;
-  static constexpr int KCH = D / 8;             // 16-byte chunks per row
-  static constexpr int RS = KCH + 1;            // padded row stride (chunks)
-  static constexpr int QSLOT = BQ * RS;         // slots of a padded [BQ][D] tile
-  static constexpr int QB = (QSLOT + 63) / 64;  // 1 KB DMA blocks per padded tile
-  static constexpr int TBLK = D / 16;           // 1 KB blocks per [D][BQ] tile
-  // tiles in stage order: Q (always), dO (dK), Q^T (dK), dO^T (dV)
-  static constexpr int NQ = QB, NO = DO_K ? QB : 0, NQT = DO_K ? TBLK : 0,
-                       NOT = DO_V ? TBLK : 0;
+  static constexpr int KCH = D / 8;
+  static constexpr int RB = BQ * KCH / 64;      // 1 KB blocks of a row-major tile
+  static constexpr int TB = D * (BQ / 8) / 64;  // 1 KB blocks of a transposed tile
+  // tiles in stage order: Q, dO (dK), Q^T (dK), dO^T (dV)
+  static constexpr int NQ = RB, NO = DO_K ? RB : 0, NQT = DO_K ? TB : 0, NOT = DO_V ? TB : 0;
   static constexpr int NB = NQ + NO + NQT + NOT;
-  static constexpr int NBW = (NB + 3) / 4;      // DMA slots per wave (last ones may be junk)
+  static constexpr int NBW = (NB + NWK - 1) / NWK;  // blocks per wavefront (tail ones junk)
   static constexpr int OFF_O = NQ * 64, OFF_QT = OFF_O + NO * 64, OFF_OT = OFF_QT + NQT * 64,
                        OFF_LD = OFF_OT + NOT * 64, STAGE = OFF_LD + 16;  // 16-byte chunks
-  static constexpr int NST = 3;
-  static constexpr int JUNK = NST * STAGE;      // 1 KB sink for unused slots
-  static constexpr int SMEM = JUNK + 64;
-  // tile of block b: 0 Q, 1 dO, 2 Q^T, 3 dO^T, 4 none
-  static constexpr int kind(int b) {
+  static constexpr int NST = DO_K ? kDkStages : kDvStages;
+  static_assert(NST % TPBK == 0 && NST >= 2 * TPBK, "dkdv stages");
+  static constexpr int JUNK = NST * STAGE, SMEM = JUNK + 64;
+  // tile of block b: 0 Q, 1 dO, 2 Q^T, 3 dO^T, 4 none (junk)
+  static SP_DEV int kind(int b) {
     return b < NQ ? 0 : b < NQ + NO ? 1 : b < NQ + NO + NQT ? 2 : b < NB ? 3 : 4;
   }
-  static constexpr int first(int k) {
+  static SP_DEV int first(int k) {
     return k == 0 ? 0 : k == 1 ? NQ : k == 2 ? NQ + NO : NQ + NO + NQT;
   }
-  static constexpr int lds_off(int b) {  // chunk offset of block b inside a stage
-    return kind(b) == 0 ? b * 64
-         : kind(b) == 1 ? OFF_O + (b - NQ) * 64
-         : kind(b) == 2 ? OFF_QT + (b - NQ - NO) * 64
-         : kind(b) == 3 ? OFF_OT + (b - NQ - NO - NQT) * 64 : 0;
-  }
 };
 
-// Uniform per-chunk source pointers of the four tiles.
-struct DkdvSrc {
-  const uint16_t *q, *o, *qt, *ot;
-};
-
-// DMA of one stage by wave W: every slot is compile-time; the per-lane part of
-// each source address is `off[j]` (elements), the chunk part is in `src`.
-template <int D, int MODE, int W>
-SP_DEV void dkdv_issue(const DkdvSrc& src, const int (&off)[DkdvStage<D, MODE>::NBW], u32x4* stg,
-                       u32x4* junk) {
-  using S = DkdvStage<D, MODE>;
-#pragma unroll
-  for (int j = 0; j < S::NBW; ++j) {
-    const int b = W + 4 * j;
-    const int k = S::kind(b);
-    const uint16_t* base = k == 0 ? src.q : k == 1 ? src.o : k == 2 ? src.qt : k == 3 ? src.ot : src.q;
-    dma16(base + off[j], k == 4 ? junk : stg + S::lds_off(b));
-  }
-}
-
-// MODE 0: dK and dV together (one wave per SIMD: ~350 registers);
-// MODE 1: dV only (S, P, dV += dO^T P); MODE 2: dK only (S, dP, dS,
-// dK += Q^T dS).  The split kernels recompute S but fit two waves per SIMD.
+// MODE 1: dV (S, P, dV^T += dO^T P); MODE 2: dK (S, dP, dS, dK^T += Q^T dS).
+// The two kernels both recompute S but each fits two wavefronts per SIMD.
 template <int D, int MODE>
-__global__ __launch_bounds__(NT, MODE == 0 ? 1 : 2)
-void attn_dkdv_kernel(DkdvArgs a) {
+__global__ __launch_bounds__(NTK, 1) void attn_dkdv_kernel(DkdvArgs a) {
   using S = DkdvStage<D, MODE>;
   constexpr bool DO_V = S::DO_V, DO_K = S::DO_K;
-  constexpr int BQ = S::BQ, KS = D / 16, DB = D / 32, KCH = S::KCH, RS = S::RS;
+  constexpr int BQ = S::BQ, KS = D / 16, DB = D / 32, KCH = S::KCH;
   constexpr int NST = S::NST, STAGE = S::STAGE, NBW = S::NBW;
   constexpr int OFF_O = S::OFF_O, OFF_QT = S::OFF_QT, OFF_OT = S::OFF_OT, OFF_LD = S::OFF_LD;
 
@@ -312,7 +289,8 @@ void attn_dkdv_kernel(DkdvArgs a) {
   const int tid = threadIdx.x;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
   const int lane = tid & 63, hh = lane >> 5, l32 = lane & 31;
-  const int key = k0 + w * 32 + l32;  // this lane's key (column of S)
+  const int wk0 = k0 + w * 32;        // first key of this wavefront
+  const int key = wk0 + l32;          // this lane's key (column of S)
   const bool key_ok = key < k1;
 
   const int qc_first = qb & ~7;
@@ -325,25 +303,28 @@ void attn_dkdv_kernel(DkdvArgs a) {
   const uint16_t* oth = a.dot + (int64_t)head * D * a.Tqp;
   const float* lh = a.lse2 + (int64_t)head * a.T_q;
   const float* dh = a.delta + (int64_t)head * a.T_q;
+  // chunks starting at or below this row are invisible to all of this
+  // wavefront's keys (causal) -- their arithmetic is skipped
+  const int wave_qmin = wk0 >= k1 ? 0x7fffffff : a.causal ? wk0 - delta - BQ + 1 : -0x7fffffff;
 
-  // Per-lane, chunk-independent element offsets of this wave's DMA slots.
-  // Row-major slots: padded tile slot -> (row, chunk); the pad column repeats
-  // the last chunk and slots past the tile stay inside its 1 KB blocks.
+  // Per-lane, chunk-independent element offsets of this wavefront's DMA
+  // blocks w + NWK*j (block kinds are wave-uniform).
   int off[NBW], row_of[NBW];
 #pragma unroll
   for (int j = 0; j < NBW; ++j) {
-    const int b = w + 4 * j;
+    const int b = w + NWK * j;
     const int k = S::kind(b);
     off[j] = 0;
     row_of[j] = 0;
     if (k == 0 || k == 1) {
       const int slot = (b - S::first(k)) * 64 + lane;
-      const int r = min(slot / RS, BQ - 1);
+      const int r = slot / KCH;
       row_of[j] = r;
-      off[j] = r * hstride + min(slot % RS, KCH - 1) * 8;
+      off[j] = r * hstride + swz_chunk<KCH>(r, slot % KCH) * 8;
     } else if (k == 2 || k == 3) {
-      const int dim = (b - S::first(k)) * 16 + lane / 4;
-      off[j] = dim * a.Tqp + ((lane % 4) ^ ((dim >> 2) & 3)) * 8;
+      const int slot = (b - S::first(k)) * 64 + lane;
+      const int dim = slot / 4;
+      off[j] = dim * a.Tqp + ((slot % 4) ^ ((dim >> 2) & 3)) * 8;
     }
   }
 
@@ -351,36 +332,35 @@ void attn_dkdv_kernel(DkdvArgs a) {
   // ends at the same row, so blocks running together stream the same rows at
   // the same time and share them in L2.
   const int qc_last = qc_first + (n_chunks - 1) * BQ;
-  auto issue = [&](int n, int st) {
+  auto issue = [&](int n) {
     const int qc = qc_last - n * BQ;
-    u32x4* stg = smem + st * STAGE;
-    DkdvSrc src{qh + (int64_t)qc * hstride, oh + (int64_t)qc * hstride, qth + qc, oth + qc};
-    if (qc + BQ > a.T_q) {
-      // tail chunk: clamp rows past T_q to the last row (masked below)
-      int o2[NBW];
+    u32x4* stg = smem + (n % NST) * STAGE;
+    const bool tail = qc + BQ > a.T_q;  // rows past T_q are clamped to the last row (masked)
 #pragma unroll
-      for (int j = 0; j < NBW; ++j) {
-        const int k = S::kind(w + 4 * j);
-        o2[j] = off[j];
-        if (k == 0 || k == 1) o2[j] += (min(qc + row_of[j], Tq1) - qc - row_of[j]) * hstride;
-      }
-      switch (w) {
-        case 0: dkdv_issue<D, MODE, 0>(src, o2, stg, smem + S::JUNK); break;
-        case 1: dkdv_issue<D, MODE, 1>(src, o2, stg, smem + S::JUNK); break;
-        case 2: dkdv_issue<D, MODE, 2>(src, o2, stg, smem + S::JUNK); break;
-        default: dkdv_issue<D, MODE, 3>(src, o2, stg, smem + S::JUNK); break;
-      }
-    } else {
-      switch (w) {
-        case 0: dkdv_issue<D, MODE, 0>(src, off, stg, smem + S::JUNK); break;
-        case 1: dkdv_issue<D, MODE, 1>(src, off, stg, smem + S::JUNK); break;
-        case 2: dkdv_issue<D, MODE, 2>(src, off, stg, smem + S::JUNK); break;
-        default: dkdv_issue<D, MODE, 3>(src, off, stg, smem + S::JUNK); break;
-      }
+    for (int j = 0; j < NBW; ++j) {
+      const int b = w + NWK * j;
+      const int k = S::kind(b);
+      int o = off[j];
+      if ((k == 0 || k == 1) && tail) o += (min(qc + row_of[j], Tq1) - qc - row_of[j]) * hstride;
+      const uint16_t* src = k == 0   ? qh + (int64_t)qc * hstride
+                            : k == 1 ? oh + (int64_t)qc * hstride
+                            : k == 2 ? qth + qc
+                            : k == 3 ? oth + qc
+                                     : qh;
+      dma16(src + o, k == 4 ? smem + S::JUNK : stg + b * 64);
     }
-    // every wave copies the LSE / D rows (identical data): uniform DMA counts
+    // every wavefront copies the LSE / D rows (identical data): uniform DMA counts
     const int rr = min(qc + (lane & (BQ - 1)), Tq1);
     dma4((lane < BQ ? lh : dh) + rr, stg + OFF_LD);
+  };
+  auto wait_chunks = [&](int pending) {
+    if constexpr (NST - 2 * TPBK >= 2) {
+      if (pending >= 2) { wait_vmcnt<2 * (NBW + 1)>(); return; }
+    }
+    if constexpr (NST - 2 * TPBK >= 1) {
+      if (pending == 1) { wait_vmcnt<NBW + 1>(); return; }
+    }
+    wait_vmcnt<0>();
   };
 
   // K (and for dK: V) rows as B operands (col = key, k = dims).
@@ -393,162 +373,136 @@ void attn_dkdv_kernel(DkdvArgs a) {
       if constexpr (DO_K) vf[s] = *(const u32x4*)(a.v + koff + s * 16);
     }
   }
-  f32x16 dk[DO_K ? DB : 1], dv[DO_V ? DB : 1];
+  f32x16 acc[DB];  // dK^T or dV^T: lane = key, registers = dims
 #pragma unroll
   for (int d = 0; d < DB; ++d)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      if constexpr (DO_K) dk[d][r] = 0.f;
-      if constexpr (DO_V) dv[d][r] = 0.f;
-    }
+    for (int r = 0; r < 16; ++r) acc[d][r] = 0.f;
   const float c2 = a.scale_log2;
-  // lane-constant LDS chunk indices of the fragments (k-steps / dim blocks
-  // add compile-time offsets)
-  const int fq_base = perm32(l32) * RS + hh;
-  const int t0_base = swz4(l32, hh), t1_base = swz4(l32, 2 + hh);
+  // lane-constant LDS chunk indices of the fragments
+  int fq_idx[KS];
+  {
+    const int qr = perm32(l32);
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) fq_idx[ks] = qr * KCH + swz_chunk<KCH>(qr, ks * 2 + hh);
+  }
+  const int t0_idx = swz4(l32, hh), t1_idx = swz4(l32, 2 + hh);
+  constexpr int OFF_T = DO_K ? OFF_QT : OFF_OT;  // A operand of the accumulation
 
-  if (n_chunks > 0) issue(0, 0);
-  if (n_chunks > 1) issue(1, 1);
-  if (n_chunks > 1) wait_vmcnt<NBW + 1>(); else wait_vmcnt<0>();
-  __syncthreads();
+  for (int n = 0; n < NST - TPBK && n < n_chunks; ++n) issue(n);
 
-  int st = 0, st_next2 = 2;
-  for (int n = 0; n < n_chunks; ++n) {
-    const int qc = qc_last - n * BQ;
-    const u32x4* stg = smem + st * STAGE;
-    if (n + 2 < n_chunks) issue(n + 2, st_next2);
+  for (int n0 = 0; n0 < n_chunks; n0 += NST) {
+#pragma unroll
+    for (int u = 0; u < NST; ++u) {
+      const int n = n0 + u;
+      if (n >= n_chunks) break;
+      if (u % TPBK == 0) {
+        // chunks n .. n+TPBK-1 landed; the stages of chunks n-TPBK .. n-1
+        // are free and receive chunks n+NST-TPBK ..
+        const int issued = min(n_chunks, n + NST - TPBK);
+        wait_chunks(issued - min(n_chunks, n + TPBK));
+        __syncthreads();
+#pragma unroll
+        for (int t = 0; t < TPBK; ++t)
+          if (n + NST - TPBK + t < n_chunks) issue(n + NST - TPBK + t);
+      }
+      const int qc = qc_last - n * BQ;
+      if (qc < wave_qmin) continue;  // no row of the chunk sees this wavefront's keys
+      const u32x4* stg = smem + u * STAGE;
 
-    f32x16 s, dp;
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      s[r] = 0.f;
-      dp[r] = 0.f;
-    }
-    __builtin_amdgcn_s_setprio(1);
-    if constexpr (MODE == 2) {
-      // dK: registers are at the two-waves-per-SIMD limit; fragments are read
-      // next to their MFMAs and the compiler keeps a few in flight.
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        s = mfma32(stg[fq_base + ks * 2], kf[ks], s);
-        dp = mfma32(stg[OFF_O + fq_base + ks * 2], vf[ks], dp);
-      }
-    } else {
-      // all A fragments of S = Q K^T (and dP = dO V^T) first, then the MFMAs
-      u32x4 fq[KS], fo[DO_K ? KS : 1];
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        fq[ks] = stg[fq_base + ks * 2];
-        if constexpr (DO_K) fo[ks] = stg[OFF_O + fq_base + ks * 2];
-      }
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        s = mfma32(fq[ks], kf[ks], s);
-        if constexpr (DO_K) dp = mfma32(fo[ks], vf[ks], dp);
-      }
-    }
-    __builtin_amdgcn_s_setprio(0);
-    // A fragments of dV^T = dO^T P and dK^T = Q^T dS (read while the softmax runs)
-    u32x4 fv[DO_V ? DB : 1][2], fk[DO_K ? DB : 1][2];
-#pragma unroll
-    for (int d = 0; d < DB; ++d) {
-      if constexpr (DO_V) {
-        fv[d][0] = stg[OFF_OT + t0_base + d * 128];
-        fv[d][1] = stg[OFF_OT + t1_base + d * 128];
-      }
-      if constexpr (DO_K) {
-        fk[d][0] = stg[OFF_QT + t0_base + d * 128];
-        fk[d][1] = stg[OFF_QT + t1_base + d * 128];
-      }
-    }
-    // chunk needs masking if it straddles the item's row range, the key
-    // tile's end, or the causal diagonal of this wavefront's keys
-    const int wk0 = k0 + w * 32;
-    const bool need_mask = (qc < qb) | (qc + BQ > qe) | (wk0 + 32 > k1) |
-                           (a.causal & (wk0 + 31 > qc + delta));
-    // visible chunk rows for this lane's key: lo <= row-in-chunk < hi
-    int lo = qb - qc, hi = qe - qc;
-    if (a.causal) lo = max(lo, key - delta - qc);
-    if (!key_ok) hi = lo;
-    lo -= hh * 8;
-    hi -= hh * 8;
-    // masked scores become -inf, so P (and dS) vanish there; the block is
-    // branched over on all but edge and diagonal chunks
-    if (need_mask) {
+      f32x16 s, dp;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int br = (r >> 3) * 16 + (r & 7);  // chunk row minus hh*8
-        s[r] = (br >= lo && br < hi) ? s[r] : neg_inf();
+        s[r] = 0.f;
+        dp[r] = 0.f;
       }
-    }
-    const f32x4* vL = (const f32x4*)(stg + OFF_LD);
-    const f32x4* vD = vL + BQ / 4;
-    u32x4 pb[2], db[2];
+      __builtin_amdgcn_s_setprio(1);
 #pragma unroll
-    for (int half = 0; half < 2; ++half) {
-      const f32x4 La = vL[half * 4 + hh * 2], Lb = vL[half * 4 + hh * 2 + 1];
-      const float Lr[8] = {La[0], La[1], La[2], La[3], Lb[0], Lb[1], Lb[2], Lb[3]};
-      float Dr[8];
-      if constexpr (DO_K) {
-        const f32x4 Da = vD[half * 4 + hh * 2], Db = vD[half * 4 + hh * 2 + 1];
-        Dr[0] = Da[0]; Dr[1] = Da[1]; Dr[2] = Da[2]; Dr[3] = Da[3];
-        Dr[4] = Db[0]; Dr[5] = Db[1]; Dr[6] = Db[2]; Dr[7] = Db[3];
+      for (int ks = 0; ks < KS; ++ks) {
+        s = mfma32(stg[fq_idx[ks]], kf[ks], s);
+        if constexpr (DO_K) dp = mfma32(stg[OFF_O + fq_idx[ks]], vf[ks], dp);
       }
-      float p[8], ds[8];
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const int r = half * 8 + i;
-        p[i] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[r], c2, -Lr[i]));
-        if constexpr (DO_K) ds[i] = p[i] * (dp[r] - Dr[i]);
-      }
-      if constexpr (DO_V) pb[half] = pack_bf16x8(p[0], p[1], p[2], p[3], p[4], p[5], p[6], p[7]);
-      if constexpr (DO_K)
-        db[half] = pack_bf16x8(ds[0], ds[1], ds[2], ds[3], ds[4], ds[5], ds[6], ds[7]);
-    }
-    __builtin_amdgcn_s_setprio(1);
-#pragma unroll
-    for (int d = 0; d < DB; ++d) {
+      __builtin_amdgcn_s_setprio(0);
+      // A fragments of the accumulation: for dV read while the softmax runs;
+      // dK is at the register limit and reads them next to their MFMAs
+      u32x4 fa[DO_V ? DB : 1][2];
       if constexpr (DO_V) {
-        dv[d] = mfma32(fv[d][0], pb[0], dv[d]);
-        dv[d] = mfma32(fv[d][1], pb[1], dv[d]);
+#pragma unroll
+        for (int d = 0; d < DB; ++d) {
+          fa[d][0] = stg[OFF_T + t0_idx + d * 128];
+          fa[d][1] = stg[OFF_T + t1_idx + d * 128];
+        }
       }
-      if constexpr (DO_K) {
-        dk[d] = mfma32(fk[d][0], db[0], dk[d]);
-        dk[d] = mfma32(fk[d][1], db[1], dk[d]);
+      // the chunk needs masking if it straddles the item's row range, the key
+      // tile's end, or the causal diagonal of this wavefront's keys
+      const bool need_mask = (qc < qb) | (qc + BQ > qe) | (wk0 + 32 > k1) |
+                             (a.causal & (wk0 + 31 > qc + delta));
+      if (need_mask) {
+        // visible chunk rows for this lane's key: lo <= row-in-chunk < hi
+        int lo = qb - qc, hi = qe - qc;
+        if (a.causal) lo = max(lo, key - delta - qc);
+        if (!key_ok) hi = lo;
+        lo -= hh * 8;
+        hi -= hh * 8;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int br = (r >> 3) * 16 + (r & 7);  // chunk row minus hh*8
+          s[r] = (br >= lo && br < hi) ? s[r] : neg_inf();
+        }
       }
+      const f32x4* vL = (const f32x4*)(stg + OFF_LD);
+      const f32x4* vD = vL + BQ / 4;
+      u32x4 pb[2];
+#pragma unroll
+      for (int half = 0; half < 2; ++half) {
+        const f32x4 La = vL[half * 4 + hh * 2], Lb = vL[half * 4 + hh * 2 + 1];
+        const float Lr[8] = {La[0], La[1], La[2], La[3], Lb[0], Lb[1], Lb[2], Lb[3]};
+        float Dr[8];
+        if constexpr (DO_K) {
+          const f32x4 Da = vD[half * 4 + hh * 2], Db = vD[half * 4 + hh * 2 + 1];
+          Dr[0] = Da[0]; Dr[1] = Da[1]; Dr[2] = Da[2]; Dr[3] = Da[3];
+          Dr[4] = Db[0]; Dr[5] = Db[1]; Dr[6] = Db[2]; Dr[7] = Db[3];
+        }
+        float x[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          const int r = half * 8 + i;
+          const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[r], c2, -Lr[i]));
+          if constexpr (DO_K) x[i] = p * (dp[r] - Dr[i]);  // dS
+          else x[i] = p;                                    // P
+        }
+        pb[half] = pack_bf16x8(x[0], x[1], x[2], x[3], x[4], x[5], x[6], x[7]);
+      }
+      __builtin_amdgcn_s_setprio(1);
+#pragma unroll
+      for (int d = 0; d < DB; ++d) {
+        if constexpr (DO_V) {
+          acc[d] = mfma32(fa[d][0], pb[0], acc[d]);
+          acc[d] = mfma32(fa[d][1], pb[1], acc[d]);
+        } else {
+          acc[d] = mfma32(stg[OFF_T + t0_idx + d * 128], pb[0], acc[d]);
+          acc[d] = mfma32(stg[OFF_T + t1_idx + d * 128], pb[1], acc[d]);
+        }
+      }
+      __builtin_amdgcn_s_setprio(0);
     }
-    __builtin_amdgcn_s_setprio(0);
-
-    // chunk n+1 must have landed (chunk n+2 may still be in flight)
-    if (n + 2 < n_chunks) wait_vmcnt<NBW + 1>(); else wait_vmcnt<0>();
-    __syncthreads();
-    st = (st == NST - 1) ? 0 : st + 1;
-    st_next2 = (st_next2 == NST - 1) ? 0 : st_next2 + 1;
   }
 
   if (!key_ok) return;
-  const float sc = a.scale;
+  const float sc = DO_K ? a.scale : 1.f;
 #pragma unroll
   for (int d = 0; d < DB; ++d)
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int dim = d * 32 + j * 8 + hh * 4;
+      const float x0 = acc[d][j * 4] * sc, x1 = acc[d][j * 4 + 1] * sc;
+      const float x2 = acc[d][j * 4 + 2] * sc, x3 = acc[d][j * 4 + 3] * sc;
       if (a.direct) {
         const int64_t o = ((int64_t)key * a.Hkv + kvh) * D + dim;
-        if constexpr (DO_K)
-          *(u32x2*)(a.dk + o) = pack_bf16x4(dk[d][j * 4] * sc, dk[d][j * 4 + 1] * sc,
-                                            dk[d][j * 4 + 2] * sc, dk[d][j * 4 + 3] * sc);
-        if constexpr (DO_V)
-          *(u32x2*)(a.dv + o) = pack_bf16x4(dv[d][j * 4], dv[d][j * 4 + 1], dv[d][j * 4 + 2],
-                                            dv[d][j * 4 + 3]);
+        *(u32x2*)((DO_K ? a.dk : a.dv) + o) = pack_bf16x4(x0, x1, x2, x3);
       } else {
         const int64_t o = ((int64_t)head * a.T_k + key) * D + dim;
-        if constexpr (DO_K)
-          *(float4*)(a.part_k + o) = make_float4(dk[d][j * 4] * sc, dk[d][j * 4 + 1] * sc,
-                                                 dk[d][j * 4 + 2] * sc, dk[d][j * 4 + 3] * sc);
-        if constexpr (DO_V)
-          *(float4*)(a.part_v + o) =
-              make_float4(dv[d][j * 4], dv[d][j * 4 + 1], dv[d][j * 4 + 2], dv[d][j * 4 + 3]);
+        *(float4*)((DO_K ? a.part_k : a.part_v) + o) = make_float4(x0, x1, x2, x3);
       }
     }
 }
@@ -563,8 +517,8 @@ hipError_t launch_attn_dq(const DqArgs& a, int n_items, int D, hipStream_t st) {
 
 hipError_t launch_attn_dkdv(const DkdvArgs& a, int n_items, int D, hipStream_t st) {
   if (n_items <= 0) return hipSuccess;
-  // dV and dK as two kernels (each fits two waves per SIMD)
-  const dim3 g(n_items), b(NT);
+  // dV and dK as two kernels (each fits two wavefronts per SIMD)
+  const dim3 g(n_items), b(NTK);
   hipError_t e;
   if (D == 128) {
     if ((e = sp_launch(kKDv, attn_dkdv_kernel<128, 1>, g, b, st, a)) != hipSuccess) return e;

@@ -130,8 +130,12 @@ static constexpr int kDqBM = 32 * kDqWaves;
 static constexpr int kDqBN = 32;
 static constexpr int kDqStages = 4;
 static constexpr int kDqTilesPerSync = 2;
-static constexpr int kDkdvBN = 128;
+static constexpr int kDkdvWaves = 8;                // wavefronts per dK / dV workgroup
+static constexpr int kDkdvBN = 32 * kDkdvWaves;
 static constexpr int kDkdvBQ = 32;
+static constexpr int kDkStages = 4;
+static constexpr int kDvStages = 4;
+static constexpr int kDkdvChunksPerSync = 2;
 static constexpr int kTransposePad = 64;
 
 }  // namespace spk
