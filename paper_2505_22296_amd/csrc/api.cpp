@@ -38,10 +38,8 @@ struct Problem {
   std::vector<int> kv_of;    // per real local head
   std::vector<int> kv_lo, kv_hi;  // per local KV head: real heads [lo, hi) reading it
   bool direct = true;        // every KV head read by at most one real local head
-  int64_t Tqp = 0, Tkp = 0;  // padded lengths of transposed copies
 };
 
-inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 
 sp_status validate(const sp_attn_desc* d, Problem& p) {
   if (!d) return SP_ERR_INVALID_ARG;
@@ -120,8 +118,6 @@ sp_status validate(const sp_attn_desc* d, Problem& p) {
       p.segs.push_back(g);
     }
   }
-  p.Tqp = round_up(std::max(d->T_q, 1), 8) + spk::kTransposePad;
-  p.Tkp = round_up(std::max(d->T_k, 1), 8) + spk::kTransposePad;
   return SP_OK;
 }
 
@@ -187,8 +183,7 @@ void schedule_keys(const sp_attn_desc* d, const Problem& p, int BNK, int BQ,
 
 // Workspace layout.
 struct Layout {
-  size_t items_dq = 0, items_kv = 0, vt = 0, delta = 0, lse2 = 0, qt = 0, dot = 0, kt = 0,
-         part_k = 0, part_v = 0, total = 0;
+  size_t items_dq = 0, items_kv = 0, delta = 0, lse2 = 0, part_k = 0, part_v = 0, total = 0;
 };
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
@@ -205,15 +200,11 @@ Layout layout_for(const sp_attn_desc* d, const Problem& p, int op, size_t n_item
   const size_t D = p.D;
   if (op == SP_OP_FWD || op == SP_OP_RING_STEP) {
     L.items_dq = take(n_items_a * kItemInts * 4);
-    L.vt = take((size_t)d->Hkv_loc * D * p.Tkp * 2);
   } else {
     L.items_dq = take(n_items_a * kItemInts * 4);
     L.items_kv = take(n_items_b * kItemInts * 4);
     L.delta = take((size_t)std::max(p.n_real, 1) * d->T_q * 4);
     L.lse2 = take((size_t)std::max(p.n_real, 1) * d->T_q * 4);
-    L.qt = take((size_t)std::max(p.n_real, 1) * D * p.Tqp * 2);
-    L.dot = take((size_t)std::max(p.n_real, 1) * D * p.Tqp * 2);
-    L.kt = take((size_t)d->Hkv_loc * D * p.Tkp * 2);
     if (!p.direct) {
       L.part_k = take((size_t)p.n_real * d->T_k * D * 4);
       L.part_v = take((size_t)p.n_real * d->T_k * D * 4);
@@ -400,19 +391,17 @@ static sp_status fwd_common(const sp_attn_desc* d, const void* q, const void* k,
   const int n_items = (int)(items.size() / kItemInts);
   if (n_items > 0) {
     if ((s = upload(at(ws, L.items_dq), items, st)) != SP_OK) return s;
-    SP_HIP(spk::launch_transpose(v, at(ws, L.vt), d->T_k, (int)p.Tkp, d->Hkv_loc, 0, d->Hkv_loc,
-                                 p.D, st));
     spk::FwdArgs a{};
     a.q = (const uint16_t*)q;
     a.k = (const uint16_t*)k;
-    a.vt = (const uint16_t*)at(ws, L.vt);
+    a.v = (const uint16_t*)v;
     a.o = (uint16_t*)o;
     a.lse = lse;
     a.o_acc = o_acc;
     a.lse_acc = lse_acc;
     a.o_out = (uint16_t*)o_out;
     a.items = (const int32_t*)at(ws, L.items_dq);
-    a.T_q = d->T_q; a.T_k = d->T_k; a.Tkp = (int)p.Tkp; a.H = d->H_loc; a.Hkv = d->Hkv_loc;
+    a.T_q = d->T_q; a.T_k = d->T_k; a.H = d->H_loc; a.Hkv = d->Hkv_loc;
     a.scale_log2 = d->softmax_scale * 1.4426950408889634f;
     a.causal = d->causal;
     a.init = init;
@@ -471,30 +460,25 @@ sp_status sp_attn_bwd(const sp_attn_desc* d, const void* q, const void* k, const
     float* delta = (float*)at(ws, L.delta);
     float* lse2 = (float*)at(ws, L.lse2);
     SP_HIP(spk::launch_rowdot(o, dout, lse, delta, lse2, d->T_q, d->H_loc, p.n_real, D, st));
-    SP_HIP(spk::launch_transpose(q, at(ws, L.qt), d->T_q, (int)p.Tqp, d->H_loc, 0, p.n_real, D, st));
-    SP_HIP(spk::launch_transpose(dout, at(ws, L.dot), d->T_q, (int)p.Tqp, d->H_loc, 0, p.n_real, D,
-                                 st));
-    SP_HIP(spk::launch_transpose(k, at(ws, L.kt), d->T_k, (int)p.Tkp, d->Hkv_loc, 0, d->Hkv_loc, D,
-                                 st));
     const float sl2 = d->softmax_scale * 1.4426950408889634f;
     spk::DqArgs a{};
     a.q = (const uint16_t*)q; a.k = (const uint16_t*)k; a.v = (const uint16_t*)v;
-    a.kt = (const uint16_t*)at(ws, L.kt); a.dout = (const uint16_t*)dout;
+    a.dout = (const uint16_t*)dout;
     a.lse = lse; a.delta = delta; a.dq = (uint16_t*)dq; a.dq_acc = dq_acc;
     a.items = (const int32_t*)at(ws, L.items_dq);
-    a.T_q = d->T_q; a.T_k = d->T_k; a.Tkp = (int)p.Tkp; a.H = d->H_loc; a.Hkv = d->Hkv_loc;
+    a.T_q = d->T_q; a.T_k = d->T_k; a.H = d->H_loc; a.Hkv = d->Hkv_loc;
     a.scale_log2 = sl2; a.scale = d->softmax_scale; a.causal = d->causal;
     SP_HIP(spk::launch_attn_dq(a, (int)na, D, st));
 
     spk::DkdvArgs b{};
-    b.q = (const uint16_t*)q; b.qt = (const uint16_t*)at(ws, L.qt);
-    b.dout = (const uint16_t*)dout; b.dot = (const uint16_t*)at(ws, L.dot);
+    b.q = (const uint16_t*)q;
+    b.dout = (const uint16_t*)dout;
     b.lse2 = lse2; b.delta = delta; b.k = (const uint16_t*)k; b.v = (const uint16_t*)v;
     b.dk = (uint16_t*)dk; b.dv = (uint16_t*)dv;
     b.part_k = p.direct ? nullptr : (float*)at(ws, L.part_k);
     b.part_v = p.direct ? nullptr : (float*)at(ws, L.part_v);
     b.items = (const int32_t*)at(ws, L.items_kv);
-    b.T_q = d->T_q; b.T_k = d->T_k; b.Tqp = (int)p.Tqp; b.H = d->H_loc; b.Hkv = d->Hkv_loc;
+    b.T_q = d->T_q; b.T_k = d->T_k; b.H = d->H_loc; b.Hkv = d->Hkv_loc;
     b.scale_log2 = sl2; b.scale = d->softmax_scale; b.causal = d->causal; b.direct = p.direct;
     SP_HIP(spk::launch_attn_dkdv(b, (int)nb, D, st));
     if (!p.direct) {

@@ -66,6 +66,50 @@ SP_DEV int swz_chunk(int row, int chunk) {
 template <int NCH>
 SP_DEV int swz(int row, int chunk) { return row * NCH + swz_chunk<NCH>(row, chunk); }
 
+// ---- Blocked LDS tiles: a [ROWS][D] bf16 tile is stored as D/32 sub-tiles
+// [ROWS][32] (64-byte rows, four 16-byte chunks), chunk c of row r at
+// position c ^ ((r >> 2) & 3).  Sixteen consecutive rows at one logical chunk
+// and four consecutive rows x four chunks both hit distinct banks, so plain
+// fragment reads (rows on lanes) and transposed reads (ds_read_b64_tr_b16,
+// tile rows become the k index) are conflict-free; the sub-tile index is an
+// immediate offset.
+SP_DEV int blk_chunk(int row, int chunk) { return chunk ^ ((row >> 2) & 3); }
+
+// Chunk index (16-byte units) of tile row `row`, logical 16-byte chunk
+// `chunk` of D, in a blocked tile of ROWS rows.
+template <int ROWS>
+SP_DEV int blk_idx(int row, int chunk) {
+  return (chunk >> 2) * (ROWS * 4) + row * 4 + blk_chunk(row, chunk & 3);
+}
+
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+
+// gfx950 ds_read_b64_tr_b16 (lane layout measured on the GPU): within each
+// group of 16 lanes, output lane j element e is input lane 4e + j/4's
+// element j%4, where every input lane reads 4 consecutive 16-bit values.
+SP_DEV u32x2 lds_tr16(const void* p) {
+  s16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)p);
+  return __builtin_bit_cast(u32x2, v);
+}
+
+// Per-lane element offset (within one sub-tile of a blocked tile) of the
+// transposed MFMA A-operand read: the fragment A[m][k] = T[k][m] (m = 32
+// columns of the sub-tile, k = 16 tile rows from row 0) is two tr16 reads at
+// this offset and at +4 rows; k-steps add 16 rows, sub-tiles ROWS*32 elements.
+SP_DEV int blk_tr_off(int lane) {
+  const int grp = lane >> 4, j = lane & 15;
+  const int row = (grp >> 1) * 8 + (j >> 2);         // + 4 for the second read
+  const int col = (grp & 1) * 16 + 4 * (j & 3);
+  return row * 32 + blk_chunk(row, col >> 3) * 8 + (col & 7);
+}
+// The second read's rows are 4 further on, which flips bit 0 of (row >> 2).
+SP_DEV int blk_tr_off2(int lane) {
+  const int grp = lane >> 4, j = lane & 15;
+  const int row = (grp >> 1) * 8 + 4 + (j >> 2);
+  const int col = (grp & 1) * 16 + 4 * (j & 3);
+  return row * 32 + blk_chunk(row, col >> 3) * 8 + (col & 7);
+}
+
 SP_DEV float wave_max_xor32(float x) { return fmaxf(x, __shfl_xor(x, 32)); }
 SP_DEV float wave_sum_xor32(float x) { return x + __shfl_xor(x, 32); }
 

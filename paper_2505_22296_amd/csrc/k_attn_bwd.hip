@@ -5,18 +5,19 @@
 //   dK = scale dS^T Q,  dV = P^T dO.
 //
 // dq kernel (query-stationary): workgroup = 256 query rows of one head,
-//   wavefront w owns 32 rows; per 32-key tile (K, V row-major and K^T staged
-//   in LDS):
+//   wavefront w owns 32 rows; per 32-key tile (K, V staged in LDS):
 //     S^T = K Q^T, dP^T = V dO^T     (Q, dO rows kept as B operands)
 //     dS^T = P^T (dP^T - D)          (row statistics are per lane)
-//     dQ^T += K^T dS^T               (dS^T C registers used directly as B)
+//     dQ^T += K^T dS^T               (K^T by transposing LDS reads; dS^T C
+//                                     registers used directly as B)
 // dk/dv kernels (key-stationary): workgroup = 256 keys of one KV head and
 //   one query head, wavefront w owns 32 keys (K, V rows as B operands in
-//   registers); per 32-row query chunk, visited last to first (Q, dO
-//   row-major and Q^T, dO^T staged in LDS):
+//   registers); per 32-row query chunk, visited last to first (Q, dO staged
+//   in LDS):
 //     S = Q K^T, dP = dO V^T          (Q, dO rows loaded in perm32 order)
 //     dS = P (dP - D)
-//     dV^T += dO^T P, dK^T += Q^T dS (P, dS C registers used directly as B)
+//     dV^T += dO^T P, dK^T += Q^T dS (dO^T, Q^T by transposing LDS reads;
+//                                     P, dS C registers used directly as B)
 //   With one query head per KV head the results are written as bf16; under
 //   GQA each query head writes a float32 partial that a reduction kernel
 //   sums over the group in ascending head order.
@@ -29,36 +30,33 @@ namespace {
 
 constexpr int NT = 256;
 
-// 4-chunk rows (32 bf16) share a 256-byte bank window in groups of four.
-SP_DEV int swz4(int row, int chunk) { return row * 4 + (chunk ^ ((row >> 2) & 3)); }
-
 // ------------------------------------------------------------------- dQ
 // Workgroup = NWQ wavefronts = 32*NWQ query rows of one head.  LDS stage:
-// K and V tiles [32 keys][D] (chunk XOR swizzle swz<>) and the K^T tile
-// [D][32 keys] (swz4), filled by DMA in 1 KB blocks spread over the
-// wavefronts; NSTQ tiles resident, barrier every TPBQ tiles.
+// K and V tiles [32 keys][D] in the blocked layout of dev_common.h (K^T
+// fragments are transposing reads of the K tile), filled by DMA in 1 KB
+// blocks spread over the wavefronts; NSTQ tiles resident, barrier every
+// TPBQ tiles.
 constexpr int NWQ = kDqWaves, NTQ = 64 * NWQ, NSTQ = kDqStages, TPBQ = kDqTilesPerSync;
 static_assert(kDqBM == 32 * NWQ && NSTQ % TPBQ == 0 && NSTQ >= 2 * TPBQ, "dq tiling");
 
 template <int D>
 struct DqStage {
   static constexpr int BN = kDqBN;
-  static constexpr int KCH = D / 8;
-  static constexpr int RB = BN * KCH / 64;       // 1 KB blocks of a row-major tile
-  static constexpr int TB = D * (BN / 8) / 64;   // 1 KB blocks of the K^T tile
-  static constexpr int NB = 2 * RB + TB;
+  static constexpr int SUB = BN * 4;             // chunks per sub-tile [BN][32]
+  static constexpr int RB = BN * (D / 8) / 64;   // 1 KB blocks of a tile
+  static constexpr int NB = 2 * RB;
   static constexpr int NBW = (NB + NWQ - 1) / NWQ;  // blocks per wavefront (tail ones junk)
-  static constexpr int OFF_V = RB * 64, OFF_T = 2 * RB * 64, STAGE = NB * 64;
+  static constexpr int OFF_V = RB * 64, STAGE = NB * 64;
   static constexpr int JUNK = NSTQ * STAGE, SMEM = JUNK + 64;
-  // 0 = K, 1 = V, 2 = K^T, 3 = unused slot (copied to the junk block)
-  static SP_DEV int kind(int b) { return b < RB ? 0 : b < 2 * RB ? 1 : b < NB ? 2 : 3; }
+  // 0 = K, 1 = V, 2 = unused slot (copied to the junk block)
+  static SP_DEV int kind(int b) { return b < RB ? 0 : b < NB ? 1 : 2; }
 };
 
 template <int D>
 __global__ __launch_bounds__(NTQ, 1) void attn_dq_kernel(DqArgs a) {
   using S = DqStage<D>;
-  constexpr int BN = S::BN, KS = D / 16, DB = D / 32, KCH = S::KCH;
-  constexpr int NBW = S::NBW, STAGE = S::STAGE;
+  constexpr int BN = S::BN, KS = D / 16, DB = D / 32;
+  constexpr int NBW = S::NBW, STAGE = S::STAGE, SUB = S::SUB;
 
   __shared__ u32x4 smem[S::SMEM];
 
@@ -100,29 +98,21 @@ __global__ __launch_bounds__(NTQ, 1) void attn_dq_kernel(DqArgs a) {
   const int n_tiles = (k1 > k0) ? (k1 - kt_first + BN - 1) / BN : 0;
 
   // Per-lane, tile-independent element offsets of this wavefront's DMA blocks
-  // w + NWQ*j (the block kinds are wave-uniform).
+  // w + NWQ*j (the block kinds are wave-uniform; K and V share shape and
+  // source row stride).
   const int kstride = a.Hkv * D;
   int off[NBW], key_of[NBW];
 #pragma unroll
   for (int j = 0; j < NBW; ++j) {
     const int b = w + NWQ * j;
     const int k = S::kind(b);
-    off[j] = 0;
-    key_of[j] = 0;
-    if (k == 0 || k == 1) {
-      const int slot = (k == 0 ? b : b - S::RB) * 64 + lane;
-      const int r = slot / KCH;
-      key_of[j] = r;
-      off[j] = r * kstride + swz_chunk<KCH>(r, slot % KCH) * 8;
-    } else if (k == 2) {
-      const int slot = (b - 2 * S::RB) * 64 + lane;
-      const int dim = slot / 4;
-      off[j] = dim * a.Tkp + ((slot % 4) ^ ((dim >> 2) & 3)) * 8;
-    }
+    const int t = (k == 1 ? b - S::RB : k == 0 ? b : 0) * 64 + lane;
+    const int ts = t % SUB, r = ts / 4;
+    key_of[j] = r;
+    off[j] = r * kstride + (t / SUB) * 32 + blk_chunk(r, ts % 4) * 8;
   }
   const uint16_t* kbase = a.k + (int64_t)kvh * D;
   const uint16_t* vbase = a.v + (int64_t)kvh * D;
-  const uint16_t* tbase = a.kt + (int64_t)kvh * D * a.Tkp;
   auto issue = [&](int n) {
     const int kt = kt_first + n * BN;
     u32x4* stg = smem + (n % NSTQ) * STAGE;
@@ -133,9 +123,8 @@ __global__ __launch_bounds__(NTQ, 1) void attn_dq_kernel(DqArgs a) {
       const int b = w + NWQ * j;
       const int k = S::kind(b);
       int o = off[j];
-      if ((k == 0 || k == 1) && tail) o += (min(kt + key_of[j], k1 - 1) - kt - key_of[j]) * kstride;
-      const uint16_t* src = k == 0 ? kbase + rowoff : k == 1 ? vbase + rowoff : k == 2 ? tbase + kt : kbase;
-      dma16(src + o, k == 3 ? smem + S::JUNK : stg + b * 64);
+      if (tail) o += (min(kt + key_of[j], k1 - 1) - kt - key_of[j]) * kstride;
+      dma16((k == 1 ? vbase : kbase) + rowoff + o, k == 2 ? smem + S::JUNK : stg + b * 64);
     }
   };
   auto wait_tiles = [&](int pending) {
@@ -148,14 +137,10 @@ __global__ __launch_bounds__(NTQ, 1) void attn_dq_kernel(DqArgs a) {
     wait_vmcnt<0>();
   };
 
-  // lane-constant LDS chunk indices of the fragments
-  int kf_idx[KS];
-  {
-    const int kr = perm32(l32);
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) kf_idx[ks] = kr * KCH + swz_chunk<KCH>(kr, ks * 2 + hh);
-  }
-  const int t0_idx = S::OFF_T + swz4(l32, hh), t1_idx = S::OFF_T + swz4(l32, 2 + hh);
+  // lane-constant LDS offsets of the fragments (see the forward kernel)
+  const int kr = perm32(l32);
+  const int kf0 = kr * 4 + blk_chunk(kr, hh), kf1 = kr * 4 + blk_chunk(kr, 2 + hh);
+  const int kt0 = blk_tr_off(lane), kt1 = blk_tr_off2(lane);
 
   for (int n = 0; n < NSTQ - TPBQ && n < n_tiles; ++n) issue(n);
 
@@ -187,8 +172,9 @@ __global__ __launch_bounds__(NTQ, 1) void attn_dq_kernel(DqArgs a) {
       __builtin_amdgcn_s_setprio(1);
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
-        s = mfma32(stg[kf_idx[ks]], qf[ks], s);
-        dp = mfma32(stg[S::OFF_V + kf_idx[ks]], df[ks], dp);
+        const int fo = (ks >> 1) * SUB + ((ks & 1) ? kf1 : kf0);
+        s = mfma32(stg[fo], qf[ks], s);
+        dp = mfma32(stg[S::OFF_V + fo], df[ks], dp);
       }
       __builtin_amdgcn_s_setprio(0);
       const bool need_mask = (kt < k0) | (kt + BN > k1) | (a.causal & (kt + BN - 1 > q0 + w * 32 + delta));
@@ -209,10 +195,15 @@ __global__ __launch_bounds__(NTQ, 1) void attn_dq_kernel(DqArgs a) {
       u32x4 b0 = pack_bf16x8(ds[0], ds[1], ds[2], ds[3], ds[4], ds[5], ds[6], ds[7]);
       u32x4 b1 = pack_bf16x8(ds[8], ds[9], ds[10], ds[11], ds[12], ds[13], ds[14], ds[15]);
       __builtin_amdgcn_s_setprio(1);
+      const uint16_t* stg16 = (const uint16_t*)stg;
 #pragma unroll
       for (int d = 0; d < DB; ++d) {
-        acc[d] = mfma32(stg[t0_idx + d * 128], b0, acc[d]);
-        acc[d] = mfma32(stg[t1_idx + d * 128], b1, acc[d]);
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+          const int o = d * SUB * 8 + ks * 16 * 32;
+          const u32x2 lo = lds_tr16(stg16 + kt0 + o), hi = lds_tr16(stg16 + kt1 + o);
+          acc[d] = mfma32(u32x4{lo[0], lo[1], hi[0], hi[1]}, ks ? b1 : b0, acc[d]);
+        }
       }
       __builtin_amdgcn_s_setprio(0);
     }
@@ -239,9 +230,9 @@ __global__ __launch_bounds__(NTQ, 1) void attn_dq_kernel(DqArgs a) {
 
 // ---------------------------------------------------------------- dK / dV
 // Workgroup = NWK wavefronts = 32*NWK keys of one KV head and one query head.
-// LDS stage (one 32-row query chunk): Q [32][D] (always), dO [32][D] (dK),
-// Q^T [D][32] (dK), dO^T [D][32] (dV), the chunk's LSE*log2(e) and D rows;
-// row-major tiles use swz<>, transposed ones swz4.  NSTK chunks resident,
+// LDS stage (one 32-row query chunk): Q and dO tiles [32][D] in the blocked
+// layout of dev_common.h (Q^T and dO^T fragments are transposing reads of
+// them) and the chunk's LSE*log2(e) and D rows.  NST chunks resident,
 // barrier every TPBK chunks.
 constexpr int NWK = kDkdvWaves, NTK = 64 * NWK, TPBK = kDkdvChunksPerSync;
 static_assert(kDkdvBN == 32 * NWK, "dkdv tiling");
@@ -250,25 +241,16 @@ template <int D, int MODE>
 struct DkdvStage {
   static constexpr bool DO_V = MODE == 1, DO_K = MODE == 2;
   static constexpr int BQ = kDkdvBQ;
-  static constexpr int KCH = D / 8;
-  static constexpr int RB = BQ * KCH / 64;      // 1 KB blocks of a row-major tile
-  static constexpr int TB = D * (BQ / 8) / 64;  // 1 KB blocks of a transposed tile
-  // tiles in stage order: Q, dO (dK), Q^T (dK), dO^T (dV)
-  static constexpr int NQ = RB, NO = DO_K ? RB : 0, NQT = DO_K ? TB : 0, NOT = DO_V ? TB : 0;
-  static constexpr int NB = NQ + NO + NQT + NOT;
+  static constexpr int SUB = BQ * 4;            // chunks per sub-tile [BQ][32]
+  static constexpr int RB = BQ * (D / 8) / 64;  // 1 KB blocks of a tile
+  static constexpr int NB = 2 * RB;             // Q, dO
   static constexpr int NBW = (NB + NWK - 1) / NWK;  // blocks per wavefront (tail ones junk)
-  static constexpr int OFF_O = NQ * 64, OFF_QT = OFF_O + NO * 64, OFF_OT = OFF_QT + NQT * 64,
-                       OFF_LD = OFF_OT + NOT * 64, STAGE = OFF_LD + 16;  // 16-byte chunks
+  static constexpr int OFF_O = RB * 64, OFF_LD = NB * 64, STAGE = OFF_LD + 16;  // 16-byte chunks
   static constexpr int NST = DO_K ? kDkStages : kDvStages;
   static_assert(NST % TPBK == 0 && NST >= 2 * TPBK, "dkdv stages");
   static constexpr int JUNK = NST * STAGE, SMEM = JUNK + 64;
-  // tile of block b: 0 Q, 1 dO, 2 Q^T, 3 dO^T, 4 none (junk)
-  static SP_DEV int kind(int b) {
-    return b < NQ ? 0 : b < NQ + NO ? 1 : b < NQ + NO + NQT ? 2 : b < NB ? 3 : 4;
-  }
-  static SP_DEV int first(int k) {
-    return k == 0 ? 0 : k == 1 ? NQ : k == 2 ? NQ + NO : NQ + NO + NQT;
-  }
+  // tile of block b: 0 Q, 1 dO, 2 none (junk)
+  static SP_DEV int kind(int b) { return b < RB ? 0 : b < NB ? 1 : 2; }
 };
 
 // MODE 1: dV (S, P, dV^T += dO^T P); MODE 2: dK (S, dP, dS, dK^T += Q^T dS).
@@ -277,9 +259,9 @@ template <int D, int MODE>
 __global__ __launch_bounds__(NTK, 1) void attn_dkdv_kernel(DkdvArgs a) {
   using S = DkdvStage<D, MODE>;
   constexpr bool DO_V = S::DO_V, DO_K = S::DO_K;
-  constexpr int BQ = S::BQ, KS = D / 16, DB = D / 32, KCH = S::KCH;
+  constexpr int BQ = S::BQ, KS = D / 16, DB = D / 32, SUB = S::SUB;
   constexpr int NST = S::NST, STAGE = S::STAGE, NBW = S::NBW;
-  constexpr int OFF_O = S::OFF_O, OFF_QT = S::OFF_QT, OFF_OT = S::OFF_OT, OFF_LD = S::OFF_LD;
+  constexpr int OFF_O = S::OFF_O, OFF_LD = S::OFF_LD;
 
   __shared__ u32x4 smem[S::SMEM];
 
@@ -299,8 +281,6 @@ __global__ __launch_bounds__(NTK, 1) void attn_dkdv_kernel(DkdvArgs a) {
   const int hstride = a.H * D;  // elements between consecutive rows
   const uint16_t* qh = a.q + (int64_t)head * D;
   const uint16_t* oh = a.dout + (int64_t)head * D;
-  const uint16_t* qth = a.qt + (int64_t)head * D * a.Tqp;
-  const uint16_t* oth = a.dot + (int64_t)head * D * a.Tqp;
   const float* lh = a.lse2 + (int64_t)head * a.T_q;
   const float* dh = a.delta + (int64_t)head * a.T_q;
   // chunks starting at or below this row are invisible to all of this
@@ -308,24 +288,17 @@ __global__ __launch_bounds__(NTK, 1) void attn_dkdv_kernel(DkdvArgs a) {
   const int wave_qmin = wk0 >= k1 ? 0x7fffffff : a.causal ? wk0 - delta - BQ + 1 : -0x7fffffff;
 
   // Per-lane, chunk-independent element offsets of this wavefront's DMA
-  // blocks w + NWK*j (block kinds are wave-uniform).
+  // blocks w + NWK*j (block kinds are wave-uniform; Q and dO share shape and
+  // source row stride).
   int off[NBW], row_of[NBW];
 #pragma unroll
   for (int j = 0; j < NBW; ++j) {
     const int b = w + NWK * j;
     const int k = S::kind(b);
-    off[j] = 0;
-    row_of[j] = 0;
-    if (k == 0 || k == 1) {
-      const int slot = (b - S::first(k)) * 64 + lane;
-      const int r = slot / KCH;
-      row_of[j] = r;
-      off[j] = r * hstride + swz_chunk<KCH>(r, slot % KCH) * 8;
-    } else if (k == 2 || k == 3) {
-      const int slot = (b - S::first(k)) * 64 + lane;
-      const int dim = slot / 4;
-      off[j] = dim * a.Tqp + ((slot % 4) ^ ((dim >> 2) & 3)) * 8;
-    }
+    const int t = (k == 1 ? b - S::RB : k == 0 ? b : 0) * 64 + lane;
+    const int ts = t % SUB, r = ts / 4;
+    row_of[j] = r;
+    off[j] = r * hstride + (t / SUB) * 32 + blk_chunk(r, ts % 4) * 8;
   }
 
   // Chunks are visited from the segment end backwards: every item of a segment
@@ -341,13 +314,8 @@ __global__ __launch_bounds__(NTK, 1) void attn_dkdv_kernel(DkdvArgs a) {
       const int b = w + NWK * j;
       const int k = S::kind(b);
       int o = off[j];
-      if ((k == 0 || k == 1) && tail) o += (min(qc + row_of[j], Tq1) - qc - row_of[j]) * hstride;
-      const uint16_t* src = k == 0   ? qh + (int64_t)qc * hstride
-                            : k == 1 ? oh + (int64_t)qc * hstride
-                            : k == 2 ? qth + qc
-                            : k == 3 ? oth + qc
-                                     : qh;
-      dma16(src + o, k == 4 ? smem + S::JUNK : stg + b * 64);
+      if (tail) o += (min(qc + row_of[j], Tq1) - qc - row_of[j]) * hstride;
+      dma16((k == 1 ? oh : qh) + (int64_t)qc * hstride + o, k == 2 ? smem + S::JUNK : stg + b * 64);
     }
     // every wavefront copies the LSE / D rows (identical data): uniform DMA counts
     const int rr = min(qc + (lane & (BQ - 1)), Tq1);
@@ -379,15 +347,12 @@ __global__ __launch_bounds__(NTK, 1) void attn_dkdv_kernel(DkdvArgs a) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) acc[d][r] = 0.f;
   const float c2 = a.scale_log2;
-  // lane-constant LDS chunk indices of the fragments
-  int fq_idx[KS];
-  {
-    const int qr = perm32(l32);
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) fq_idx[ks] = qr * KCH + swz_chunk<KCH>(qr, ks * 2 + hh);
-  }
-  const int t0_idx = swz4(l32, hh), t1_idx = swz4(l32, 2 + hh);
-  constexpr int OFF_T = DO_K ? OFF_QT : OFF_OT;  // A operand of the accumulation
+  // lane-constant LDS offsets of the fragments (see the forward kernel); the
+  // accumulation's A operand is a transposing read of dO (dV) or Q (dK)
+  const int qr = perm32(l32);
+  const int qf0 = qr * 4 + blk_chunk(qr, hh), qf1 = qr * 4 + blk_chunk(qr, 2 + hh);
+  constexpr int OFF_T = DO_K ? 0 : OFF_O * 8;  // element offset of the transposed tile
+  const int tr0 = OFF_T + blk_tr_off(lane), tr1 = OFF_T + blk_tr_off2(lane);
 
   for (int n = 0; n < NST - TPBK && n < n_chunks; ++n) issue(n);
 
@@ -419,18 +384,25 @@ __global__ __launch_bounds__(NTK, 1) void attn_dkdv_kernel(DkdvArgs a) {
       __builtin_amdgcn_s_setprio(1);
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
-        s = mfma32(stg[fq_idx[ks]], kf[ks], s);
-        if constexpr (DO_K) dp = mfma32(stg[OFF_O + fq_idx[ks]], vf[ks], dp);
+        const int fo = (ks >> 1) * SUB + ((ks & 1) ? qf1 : qf0);
+        s = mfma32(stg[fo], kf[ks], s);
+        if constexpr (DO_K) dp = mfma32(stg[OFF_O + fo], vf[ks], dp);
       }
       __builtin_amdgcn_s_setprio(0);
       // A fragments of the accumulation: for dV read while the softmax runs;
       // dK is at the register limit and reads them next to their MFMAs
+      const uint16_t* stg16 = (const uint16_t*)stg;
+      auto tr_frag = [&](int d, int ks) {
+        const int o = d * SUB * 8 + ks * 16 * 32;
+        const u32x2 lo = lds_tr16(stg16 + tr0 + o), hi = lds_tr16(stg16 + tr1 + o);
+        return u32x4{lo[0], lo[1], hi[0], hi[1]};
+      };
       u32x4 fa[DO_V ? DB : 1][2];
       if constexpr (DO_V) {
 #pragma unroll
         for (int d = 0; d < DB; ++d) {
-          fa[d][0] = stg[OFF_T + t0_idx + d * 128];
-          fa[d][1] = stg[OFF_T + t1_idx + d * 128];
+          fa[d][0] = tr_frag(d, 0);
+          fa[d][1] = tr_frag(d, 1);
         }
       }
       // the chunk needs masking if it straddles the item's row range, the key
@@ -480,8 +452,8 @@ __global__ __launch_bounds__(NTK, 1) void attn_dkdv_kernel(DkdvArgs a) {
           acc[d] = mfma32(fa[d][0], pb[0], acc[d]);
           acc[d] = mfma32(fa[d][1], pb[1], acc[d]);
         } else {
-          acc[d] = mfma32(stg[OFF_T + t0_idx + d * 128], pb[0], acc[d]);
-          acc[d] = mfma32(stg[OFF_T + t1_idx + d * 128], pb[1], acc[d]);
+          acc[d] = mfma32(tr_frag(d, 0), pb[0], acc[d]);
+          acc[d] = mfma32(tr_frag(d, 1), pb[1], acc[d]);
         }
       }
       __builtin_amdgcn_s_setprio(0);

@@ -2,20 +2,22 @@
 //
 // One workgroup = 8 wavefronts = 256 query rows of one head (a work item from
 // the host block-skip scheduler); wavefront w owns rows q_begin + 32w ..
-// +32.  The key loop walks 64-key tiles of the segment.  Tiles are copied
-// global -> LDS by DMA (K row-major, V transposed, both with an XOR swizzle
-// of their 16-byte chunks and no padding), four tiles resident: while a pair
-// of tiles is consumed the next pair lands, and the eight wavefronts meet at
-// a barrier once per pair.  Each tile is shared by all eight wavefronts.
+// +32.  The key loop walks 64-key tiles of the segment.  K and V tiles are
+// copied global -> LDS by DMA into the blocked layout of dev_common.h (no
+// padding, no transposed copy: V^T fragments come from transposing LDS
+// reads), four tiles resident: while a pair of tiles is consumed the next
+// pair lands, and the eight wavefronts meet at a barrier once per pair.  Each
+// tile is shared by all eight wavefronts.
 //
 // Per 64-key tile and wavefront:
 //   S^T = K Q^T      (32x32x16 bf16 MFMA; Q^T kept in registers as B operand)
 //   online softmax   (fp32; the 32x32 C layout gives each lane one query row,
 //                     16 keys per tile half; the row max needs one exchange
 //                     with lane l^32)
-//   O^T += V^T P^T   (P^T from the C registers directly: K rows are loaded in
-//                     perm32 order so each lane half's C registers are 8
-//                     consecutive keys, i.e. a B operand k-slice)
+//   O^T += V^T P^T   (V^T by ds_read_b64_tr_b16 from the V tile; P^T from the
+//                     C registers directly: K rows are loaded in perm32 order
+//                     so each lane half's C registers are 8 consecutive keys,
+//                     i.e. a B operand k-slice)
 // The running max is only raised when it grows by more than 2^8 (exact:
 // the final normalisation uses the same max).  Masking is evaluated only on
 // tiles that straddle a segment edge or the causal diagonal; a wavefront
@@ -38,17 +40,15 @@ constexpr int NST = kFwdStages;       // resident tiles
 constexpr int TPB = kFwdTilesPerSync; // tiles per barrier
 static_assert(BM == 32 * NW && NST % TPB == 0 && NST >= 2 * TPB, "fwd tiling");
 
-// LDS stage of the forward: K tile [BN][D] and V^T tile [D][BN], both
-// row-major with the chunk XOR swizzle swz<>, filled by DMA in 1 KB blocks.
+// LDS stage of the forward: K and V tiles [BN][D] in the blocked layout
+// (D/32 sub-tiles [BN][32]), filled by DMA in 1 KB blocks.
 template <int D>
 struct FwdStage {
-  static constexpr int KCH = D / 8;            // chunks per K row
-  static constexpr int VCH = BN / 8;           // chunks per V^T row
-  static constexpr int KB = BN * KCH / 64;     // 1 KB blocks of the K tile
-  static constexpr int VB = D * VCH / 64;      // 1 KB blocks of the V^T tile
-  static constexpr int NB = KB + VB;
+  static constexpr int SUB = BN * 4;           // chunks per sub-tile
+  static constexpr int KB = BN * (D / 8) / 64; // 1 KB blocks per tile
+  static constexpr int NB = 2 * KB;
   static constexpr int NBW = NB / NW;          // blocks per wavefront
-  static_assert(KB % NW == 0 && VB % NW == 0, "DMA blocks per wavefront");
+  static_assert(KB % NW == 0, "DMA blocks per wavefront");
   static constexpr int OFF_V = KB * 64, STAGE = NB * 64;  // 16-byte chunks
   static constexpr int SMEM = NST * STAGE;
 };
@@ -58,7 +58,7 @@ __global__ __launch_bounds__(NT, 1) void attn_fwd_kernel(FwdArgs a) {
   using S = FwdStage<D>;
   constexpr int KS = D / 16;   // MFMA k-steps over D
   constexpr int DB = D / 32;   // 32-dim blocks of O^T
-  constexpr int KCH = S::KCH, VCH = S::VCH, NBW = S::NBW, NBK = NBW / 2, STAGE = S::STAGE;
+  constexpr int NBW = S::NBW, NBK = NBW / 2, STAGE = S::STAGE, SUB = S::SUB;
 
   __shared__ u32x4 smem[S::SMEM];
 
@@ -99,38 +99,30 @@ __global__ __launch_bounds__(NT, 1) void attn_fwd_kernel(FwdArgs a) {
   const int n_tiles = (k1 > k0) ? (k1 - kt_first + BN - 1) / BN : 0;
 
   // Per-lane, tile-independent element offsets of this wavefront's DMA
-  // blocks: blocks w + NW*j, the first NBK of them in the K tile.
+  // blocks w + NW*j: the first NBK of them in the K tile, the rest in V;
+  // both tiles have the same shape and source row stride.
   const int kstride = a.Hkv * D;
-  int off[NBW], key_of[NBK];
+  int off[NBK], key_of[NBK];
 #pragma unroll
-  for (int j = 0; j < NBW; ++j) {
-    const int slot = (w + NW * j) * 64 + lane;
-    if (j < NBK) {
-      const int r = slot / KCH, pc = slot % KCH;
-      key_of[j] = r;
-      off[j] = r * kstride + swz_chunk<KCH>(r, pc) * 8;
-    } else {
-      const int vs = slot - S::OFF_V, d = vs / VCH, pc = vs % VCH;
-      off[j] = d * a.Tkp + swz_chunk<VCH>(d, pc) * 8;
-    }
+  for (int j = 0; j < NBK; ++j) {
+    const int t = (w + NW * j) * 64 + lane;   // chunk slot within the tile
+    const int ts = t % S::SUB, r = ts / 4;
+    key_of[j] = r;
+    off[j] = r * kstride + (t / S::SUB) * 32 + blk_chunk(r, ts % 4) * 8;
   }
   const uint16_t* kbase = a.k + (int64_t)kvh * D;
-  const uint16_t* vbase = a.vt + (int64_t)kvh * D * a.Tkp;
+  const uint16_t* vbase = a.v + (int64_t)kvh * D;
   auto issue = [&](int n) {
     const int kt = kt_first + n * BN;
     u32x4* stg = smem + (n % NST) * STAGE + w * 64;
-    const uint16_t* ks_ = kbase + (int64_t)kt * kstride;
-    const uint16_t* vs_ = vbase + kt;
+    const int64_t rowoff = (int64_t)kt * kstride;
     const bool tail = kt + BN > k1;  // keys past k1 (masked) are clamped to k1-1
 #pragma unroll
-    for (int j = 0; j < NBW; ++j) {
-      if (j < NBK) {
-        int o = off[j];
-        if (tail) o += (min(kt + key_of[j], k1 - 1) - kt - key_of[j]) * kstride;
-        dma16(ks_ + o, stg + NW * j * 64);
-      } else {
-        dma16(vs_ + off[j], stg + NW * j * 64);
-      }
+    for (int j = 0; j < NBK; ++j) {
+      int o = off[j];
+      if (tail) o += (min(kt + key_of[j], k1 - 1) - kt - key_of[j]) * kstride;
+      dma16(kbase + rowoff + o, stg + NW * j * 64);
+      dma16(vbase + rowoff + o, stg + S::OFF_V + NW * j * 64);
     }
   };
   // Wait until at most `pending` issued tiles are still in flight.
@@ -144,17 +136,13 @@ __global__ __launch_bounds__(NT, 1) void attn_fwd_kernel(FwdArgs a) {
     wait_vmcnt<0>();
   };
 
-  // lane-constant LDS chunk indices of the fragments (the swizzle of a K row
-  // is the same for the two 32-key halves and of a V^T row for all 32-dim
-  // blocks, so those are immediate offsets)
-  int kf_idx[KS], vf_idx[4];
-  {
-    const int kr = perm32(l32);
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) kf_idx[ks] = kr * KCH + swz_chunk<KCH>(kr, ks * 2 + hh);
-#pragma unroll
-    for (int ks = 0; ks < 4; ++ks) vf_idx[ks] = S::OFF_V + l32 * VCH + swz_chunk<VCH>(l32, ks * 2 + hh);
-  }
+  // Lane-constant LDS offsets of the fragments.  K fragment (g, ks): tile row
+  // g*32 + perm32(l32), logical chunk 2ks + hh -> sub-tile ks/2 (immediate)
+  // and one of two lane bases (ks even / odd).  V^T fragments: transposing
+  // reads at two lane offsets; dim block, k-step and stage are immediates.
+  const int kr = perm32(l32);
+  const int kf0 = kr * 4 + blk_chunk(kr, hh), kf1 = kr * 4 + blk_chunk(kr, 2 + hh);
+  const int vt0 = S::OFF_V * 8 + blk_tr_off(lane), vt1 = S::OFF_V * 8 + blk_tr_off2(lane);
 
   for (int n = 0; n < NST - TPB && n < n_tiles; ++n) issue(n);
 
@@ -187,7 +175,8 @@ __global__ __launch_bounds__(NT, 1) void attn_fwd_kernel(FwdArgs a) {
 #pragma unroll
       for (int g = 0; g < 2; ++g)
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) s[g] = mfma32(stg[kf_idx[ks] + g * 32 * KCH], qf[ks], s[g]);
+        for (int ks = 0; ks < KS; ++ks)
+          s[g] = mfma32(stg[(ks >> 1) * SUB + g * 128 + ((ks & 1) ? kf1 : kf0)], qf[ks], s[g]);
       __builtin_amdgcn_s_setprio(0);
 
       // ---- mask (only on edge / diagonal tiles)
@@ -243,10 +232,15 @@ __global__ __launch_bounds__(NT, 1) void attn_fwd_kernel(FwdArgs a) {
 
       // ---- O^T += V^T P^T
       __builtin_amdgcn_s_setprio(1);
+      const uint16_t* stg16 = (const uint16_t*)stg;
 #pragma unroll
       for (int d = 0; d < DB; ++d)
 #pragma unroll
-        for (int ks = 0; ks < 4; ++ks) oacc[d] = mfma32(stg[vf_idx[ks] + d * 32 * VCH], pb[ks], oacc[d]);
+        for (int ks = 0; ks < 4; ++ks) {
+          const int o = d * SUB * 8 + ks * 16 * 32;
+          const u32x2 lo = lds_tr16(stg16 + vt0 + o), hi = lds_tr16(stg16 + vt1 + o);
+          oacc[d] = mfma32(u32x4{lo[0], lo[1], hi[0], hi[1]}, pb[ks], oacc[d]);
+        }
       __builtin_amdgcn_s_setprio(0);
     }
   }

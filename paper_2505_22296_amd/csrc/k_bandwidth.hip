@@ -3,9 +3,8 @@
 //     around the all-to-all layout of Section 4),
 //   * the log-sum-exp merge of two partial attention results (ring combine,
 //     Section 2.1),
-//   * fills, bf16 casts, 8x8 register transposes feeding the attention
-//     kernels' transposed operands, the backward's row dot D_i = dO_i . O_i,
-//     and the GQA reduction of per-query-head dK/dV partials.
+//   * fills, bf16 casts, the backward's row dot D_i = dO_i . O_i, and the
+//     GQA reduction of per-query-head dK/dV partials.
 // All accesses are 16-byte vectors; consecutive lanes touch consecutive
 // 16-byte chunks of a row.
 #include "dev_common.h"
@@ -225,53 +224,6 @@ hipError_t launch_f32_to_bf16(const float* s, void* d, int64_t n, hipStream_t st
   if (n <= 0) return hipSuccess;
   hipLaunchKernelGGL(f32_to_bf16_kernel, dim3(grid_for((n + 7) / 8)), dim3(kBlock), 0, st, s,
                      (uint16_t*)d, n);
-  return hipGetLastError();
-}
-
-// ---------------------------------------------------------------- transpose
-// dst[y][d][t] = src[t][h0 + y][d] for t < T, 0 for T <= t < Tp.
-// Each lane moves an 8-token x 8-dim block through registers.
-template <int D>
-__global__ __launch_bounds__(kBlock) void transpose_kernel(const uint16_t* __restrict__ src,
-                                                           uint16_t* __restrict__ dst, int T,
-                                                           int Tp, int H, int h0) {
-  constexpr int NC = D / 8;             // 8-dim chunks per token row
-  constexpr int TPB = (kBlock / NC) * 8;  // tokens per block
-  const int y = blockIdx.y;
-  const int h = h0 + y;
-  const int lane = threadIdx.x;
-  const int dc = lane % NC;
-  const int t0 = blockIdx.x * TPB + (lane / NC) * 8;
-  if (t0 >= Tp) return;
-  uint16_t a[8][8];
-  for (int r = 0; r < 8; ++r) {
-    int t = t0 + r;
-    u32x4 v = {0u, 0u, 0u, 0u};
-    if (t < T) v = *(const u32x4*)(src + ((int64_t)t * H + h) * D + dc * 8);
-    for (int i = 0; i < 4; ++i) {
-      a[r][2 * i] = (uint16_t)(v[i] & 0xffffu);
-      a[r][2 * i + 1] = (uint16_t)(v[i] >> 16);
-    }
-  }
-  uint16_t* out = dst + (int64_t)y * D * Tp;
-  for (int d = 0; d < 8; ++d) {
-    u32x4 w;
-    for (int i = 0; i < 4; ++i) w[i] = (uint32_t)a[2 * i][d] | ((uint32_t)a[2 * i + 1][d] << 16);
-    *(u32x4*)(out + (int64_t)(dc * 8 + d) * Tp + t0) = w;
-  }
-}
-
-hipError_t launch_transpose(const void* src, void* dst, int T, int Tp, int H, int h0, int nh, int D,
-                            hipStream_t st) {
-  if (nh <= 0 || Tp <= 0) return hipSuccess;
-  const int tpb = (kBlock / (D / 8)) * 8;
-  dim3 grid((Tp + tpb - 1) / tpb, nh);
-  if (D == 128)
-    hipLaunchKernelGGL(transpose_kernel<128>, grid, dim3(kBlock), 0, st, (const uint16_t*)src,
-                       (uint16_t*)dst, T, Tp, H, h0);
-  else
-    hipLaunchKernelGGL(transpose_kernel<64>, grid, dim3(kBlock), 0, st, (const uint16_t*)src,
-                       (uint16_t*)dst, T, Tp, H, h0);
   return hipGetLastError();
 }
 

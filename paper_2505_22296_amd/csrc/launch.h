@@ -53,14 +53,14 @@ static constexpr int kItemInts = 8;
 struct FwdArgs {
   const uint16_t* q;   // [T_q, H, D]
   const uint16_t* k;   // [T_k, Hkv, D]
-  const uint16_t* vt;  // [Hkv, D, Tkp] (V transposed, zero past T_k)
+  const uint16_t* v;   // [T_k, Hkv, D]
   uint16_t* o;         // [T_q, H, D] (plain forward)
   float* lse;          // [H, T_q]
   float* o_acc;        // ring: [T_q, H, D] float32 in/out
   float* lse_acc;      // ring: [H, T_q] in/out
   uint16_t* o_out;     // ring: optional bf16 copy of the merged O
   const int32_t* items;
-  int T_q, T_k, Tkp, H, Hkv;
+  int T_q, T_k, H, Hkv;
   float scale_log2;    // softmax_scale * log2(e)
   int causal, init;
 };
@@ -69,23 +69,20 @@ struct DqArgs {
   const uint16_t* q;     // [T_q, H, D]
   const uint16_t* k;     // [T_k, Hkv, D]
   const uint16_t* v;     // [T_k, Hkv, D]
-  const uint16_t* kt;    // [Hkv, D, Tkp]
   const uint16_t* dout;  // [T_q, H, D]
   const float* lse;      // [H, T_q]
   const float* delta;    // [n_real, T_q]
   uint16_t* dq;          // bf16 [T_q, H, D] or null
   float* dq_acc;         // float32 [T_q, H, D] (+=) or null
   const int32_t* items;
-  int T_q, T_k, Tkp, H, Hkv;
+  int T_q, T_k, H, Hkv;
   float scale_log2, scale;
   int causal;
 };
 
 struct DkdvArgs {
   const uint16_t* q;     // [T_q, H, D]
-  const uint16_t* qt;    // [n_real, D, Tqp]
   const uint16_t* dout;  // [T_q, H, D]
-  const uint16_t* dot;   // [n_real, D, Tqp]
   const float* lse2;     // [n_real, T_q]: LSE * log2(e), +inf for rows without keys
   const float* delta;    // [n_real, T_q]
   const uint16_t* k;     // [T_k, Hkv, D]
@@ -95,7 +92,7 @@ struct DkdvArgs {
   float* part_k;         // float32 [n_real, T_k, D] (GQA partial mode)
   float* part_v;
   const int32_t* items;
-  int T_q, T_k, Tqp, H, Hkv;
+  int T_q, T_k, H, Hkv;
   float scale_log2, scale;
   int causal, direct;
 };
@@ -108,8 +105,6 @@ hipError_t launch_zero_heads_bf16(void* x, int T, int H, int D, int h0, int h1, 
 hipError_t launch_zero_heads_f32(float* x, int T, int H, int D, int h0, int h1, hipStream_t st);
 hipError_t launch_fill_f32(float* x, int64_t n, float v, hipStream_t st);
 hipError_t launch_f32_to_bf16(const float* s, void* d, int64_t n, hipStream_t st);
-hipError_t launch_transpose(const void* src, void* dst, int T, int Tp, int H, int h0, int nh, int D,
-                            hipStream_t st);
 hipError_t launch_rowdot(const void* o, const void* dout, const float* lse, float* delta,
                          float* lse2, int T, int H, int nh, int D, hipStream_t st);
 hipError_t launch_reduce_kv(const float* part, void* out, const ReduceArgs& a, hipStream_t st);
@@ -119,7 +114,7 @@ hipError_t launch_attn_dq(const DqArgs& a, int n_items, int D, hipStream_t st);
 hipError_t launch_attn_dkdv(const DkdvArgs& a, int n_items, int D, hipStream_t st);
 
 // Tile sizes the host scheduler must use (rows per fwd/dq item, keys per
-// dk/dv item) and the padding of transposed copies.
+// dk/dv item) and the kernels' LDS pipelines.
 static constexpr int kFwdWaves = 8;                 // wavefronts per forward workgroup
 static constexpr int kFwdBM = 32 * kFwdWaves;
 static constexpr int kFwdBN = 64;
@@ -136,6 +131,5 @@ static constexpr int kDkdvBQ = 32;
 static constexpr int kDkStages = 4;
 static constexpr int kDvStages = 4;
 static constexpr int kDkdvChunksPerSync = 2;
-static constexpr int kTransposePad = 64;
 
 }  // namespace spk
