@@ -6,6 +6,7 @@
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
@@ -130,4 +131,18 @@ template <int N>
 SP_DEV void wait_vmcnt() {
   static_assert(N >= 0 && N < 64, "vmcnt range");
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+// Wait until at most `pending` (0 <= pending <= P) batches of PER copies are
+// still in flight (the wave issues the same number of copies per batch).
+template <int PER, int P>
+SP_DEV void wait_batches(int pending) {
+  if constexpr (P > 0) {
+    if (pending >= P) {
+      wait_vmcnt<P * PER>();
+      return;
+    }
+    wait_batches<PER, P - 1>(pending);
+  } else {
+    wait_vmcnt<0>();
+  }
 }

@@ -127,16 +127,6 @@ __global__ __launch_bounds__(NTQ, 1) void attn_dq_kernel(DqArgs a) {
       dma16((k == 1 ? vbase : kbase) + rowoff + o, k == 2 ? smem + S::JUNK : stg + b * 64);
     }
   };
-  auto wait_tiles = [&](int pending) {
-    if constexpr (NSTQ - 2 * TPBQ >= 2) {
-      if (pending >= 2) { wait_vmcnt<2 * NBW>(); return; }
-    }
-    if constexpr (NSTQ - 2 * TPBQ >= 1) {
-      if (pending == 1) { wait_vmcnt<NBW>(); return; }
-    }
-    wait_vmcnt<0>();
-  };
-
   // lane-constant LDS offsets of the fragments (see the forward kernel)
   const int kr = perm32(l32);
   const int kf0 = kr * 4 + blk_chunk(kr, hh), kf1 = kr * 4 + blk_chunk(kr, 2 + hh);
@@ -153,7 +143,7 @@ __global__ __launch_bounds__(NTQ, 1) void attn_dq_kernel(DqArgs a) {
         // tiles n .. n+TPBQ-1 landed; the stages of tiles n-TPBQ .. n-1 are
         // free and receive tiles n+NSTQ-TPBQ ..
         const int issued = min(n_tiles, n + NSTQ - TPBQ);
-        wait_tiles(issued - min(n_tiles, n + TPBQ));
+        wait_batches<NBW, NSTQ - 2 * TPBQ>(issued - min(n_tiles, n + TPBQ));
         __syncthreads();
 #pragma unroll
         for (int t = 0; t < TPBQ; ++t)
@@ -321,16 +311,6 @@ __global__ __launch_bounds__(NTK, 1) void attn_dkdv_kernel(DkdvArgs a) {
     const int rr = min(qc + (lane & (BQ - 1)), Tq1);
     dma4((lane < BQ ? lh : dh) + rr, stg + OFF_LD);
   };
-  auto wait_chunks = [&](int pending) {
-    if constexpr (NST - 2 * TPBK >= 2) {
-      if (pending >= 2) { wait_vmcnt<2 * (NBW + 1)>(); return; }
-    }
-    if constexpr (NST - 2 * TPBK >= 1) {
-      if (pending == 1) { wait_vmcnt<NBW + 1>(); return; }
-    }
-    wait_vmcnt<0>();
-  };
-
   // K (and for dK: V) rows as B operands (col = key, k = dims).
   u32x4 kf[KS], vf[DO_K ? KS : 1];
   {
@@ -365,7 +345,7 @@ __global__ __launch_bounds__(NTK, 1) void attn_dkdv_kernel(DkdvArgs a) {
         // chunks n .. n+TPBK-1 landed; the stages of chunks n-TPBK .. n-1
         // are free and receive chunks n+NST-TPBK ..
         const int issued = min(n_chunks, n + NST - TPBK);
-        wait_chunks(issued - min(n_chunks, n + TPBK));
+        wait_batches<NBW + 1, S::NST - 2 * TPBK>(issued - min(n_chunks, n + TPBK));
         __syncthreads();
 #pragma unroll
         for (int t = 0; t < TPBK; ++t)
@@ -479,6 +459,227 @@ __global__ __launch_bounds__(NTK, 1) void attn_dkdv_kernel(DkdvArgs a) {
     }
 }
 
+// ------------------------------------------------------- fused dK / dV
+// Workgroup = 8 wavefronts = 4 pairs; pair p owns keys k0 + 32p .. +32.
+// Per 32-row query chunk the pair splits the work: its P-wavefront (w < 4)
+// computes S = Q K^T, P and dV^T += dO^T P and hands P to its partner through
+// LDS (fp16: P lies in [0, 1]); the dS-wavefront (w >= 4) computes
+// dP = dO V^T, dS = P (dP - D) and dK^T += Q^T dS.  S is evaluated once per
+// pair (8*D MFMA work per pair instead of 10*D for separate dK and dV
+// kernels) and the Q / dO chunk tiles are staged once for both gradients.
+// Chunks go in groups of TPBF between barriers: in group g the
+// P-wavefronts work on group g, the dS-wavefronts on group g-1 (whose P is
+// complete), while group g+1 is copied in; stages hold three groups and the
+// P exchange two.
+constexpr int NPF = kDkdvWaves / 2;  // wavefront pairs per workgroup
+constexpr int TPBF = 2;              // chunks per group (barrier interval)
+constexpr int NSTF = 3 * TPBF;       // resident chunks
+constexpr int NXF = 2 * TPBF;        // P exchange slots
+static_assert(kDkdvFusedBN == 32 * NPF, "fused dkdv tiling");
+
+template <int D>
+struct FusedStage {
+  static constexpr int BQ = kDkdvBQ;
+  static constexpr int SUB = BQ * 4;            // chunks per sub-tile [BQ][32]
+  static constexpr int RB = BQ * (D / 8) / 64;  // 1 KB blocks of a tile
+  static constexpr int NB = 2 * RB;             // Q, dO
+  static constexpr int NBW = (NB + 2 * NPF - 1) / (2 * NPF);
+  static constexpr int OFF_O = RB * 64, OFF_LD = NB * 64, STAGE = OFF_LD + 16;
+  static constexpr int XSLOT = NPF * 128;       // per pair: 2 x 16 bytes x 64 lanes
+  static constexpr int OFF_X = NSTF * STAGE, JUNK = OFF_X + NXF * XSLOT, SMEM = JUNK + 64;
+  static SP_DEV int kind(int b) { return b < RB ? 0 : b < NB ? 1 : 2; }
+};
+
+template <int D, bool PWAVE>
+SP_DEV void fused_dkdv_body(const DkdvArgs& a, u32x4* smem, int w, int lane) {
+  using S = FusedStage<D>;
+  constexpr int BQ = S::BQ, KS = D / 16, DB = D / 32, SUB = S::SUB, NBW = S::NBW;
+  constexpr int STAGE = S::STAGE;
+  const int32_t* it = a.items + (int64_t)blockIdx.x * kItemInts;
+  const int k0 = it[0], k1 = it[1], qb = it[2], qe = it[3], delta = it[4], head = it[5],
+            kvh = it[6];
+  const int hh = lane >> 5, l32 = lane & 31;
+  const int pr = PWAVE ? w : w - NPF;  // pair index
+  const int wk0 = k0 + pr * 32;
+  const int key = wk0 + l32;
+  const bool key_ok = key < k1;
+  const int qc_first = qb & ~7;
+  const int n_chunks = (qe > qb) ? (qe - qc_first + BQ - 1) / BQ : 0;
+  const int n_groups = (n_chunks + TPBF - 1) / TPBF;
+  const int qc_last = qc_first + (n_chunks - 1) * BQ;
+  const int Tq1 = a.T_q - 1;
+  const int hstride = a.H * D;
+  const uint16_t* qh = a.q + (int64_t)head * D;
+  const uint16_t* oh = a.dout + (int64_t)head * D;
+  const float* lh = a.lse2 + (int64_t)head * a.T_q;
+  const float* dh = a.delta + (int64_t)head * a.T_q;
+  const int wave_qmin = wk0 >= k1 ? 0x7fffffff : a.causal ? wk0 - delta - BQ + 1 : -0x7fffffff;
+
+  // DMA: blocks w + 8j of each chunk's Q / dO tiles (kinds wave-uniform)
+  int off[NBW], row_of[NBW];
+#pragma unroll
+  for (int j = 0; j < NBW; ++j) {
+    const int b = w + 2 * NPF * j;
+    const int k = S::kind(b);
+    const int t = (k == 1 ? b - S::RB : k == 0 ? b : 0) * 64 + lane;
+    const int ts = t % SUB, r = ts / 4;
+    row_of[j] = r;
+    off[j] = r * hstride + (t / SUB) * 32 + blk_chunk(r, ts % 4) * 8;
+  }
+  auto issue = [&](int c) {
+    const int qc = qc_last - c * BQ;
+    u32x4* stg = smem + (c % NSTF) * STAGE;
+    const bool tail = qc + BQ > a.T_q;
+#pragma unroll
+    for (int j = 0; j < NBW; ++j) {
+      const int b = w + 2 * NPF * j;
+      const int k = S::kind(b);
+      int o = off[j];
+      if (tail) o += (min(qc + row_of[j], Tq1) - qc - row_of[j]) * hstride;
+      dma16((k == 1 ? oh : qh) + (int64_t)qc * hstride + o, k == 2 ? smem + S::JUNK : stg + b * 64);
+    }
+    const int rr = min(qc + (lane & (BQ - 1)), Tq1);
+    dma4((lane < BQ ? lh : dh) + rr, stg + S::OFF_LD);
+  };
+
+  // B operands: K rows (P-wavefront) or V rows (dS-wavefront) of this pair's keys
+  u32x4 bf[KS];
+  {
+    const int64_t koff = ((int64_t)(key_ok ? key : k0) * a.Hkv + kvh) * D + hh * 8;
+    const uint16_t* src = PWAVE ? a.k : a.v;
+#pragma unroll
+    for (int s = 0; s < KS; ++s) bf[s] = *(const u32x4*)(src + koff + s * 16);
+  }
+  f32x16 acc[DB];
+#pragma unroll
+  for (int d = 0; d < DB; ++d)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[d][r] = 0.f;
+  const float c2 = a.scale_log2;
+  const int qr = perm32(l32);
+  // plain A fragments: Q (S) or dO (dP); transposed ones: dO (dV) or Q (dK)
+  const int af0 = (PWAVE ? 0 : S::OFF_O) + qr * 4 + blk_chunk(qr, hh);
+  const int af1 = (PWAVE ? 0 : S::OFF_O) + qr * 4 + blk_chunk(qr, 2 + hh);
+  const int tr0 = (PWAVE ? S::OFF_O * 8 : 0) + blk_tr_off(lane);
+  const int tr1 = (PWAVE ? S::OFF_O * 8 : 0) + blk_tr_off2(lane);
+  const int xo = S::OFF_X + pr * 128 + lane;  // this lane's P exchange chunk (+64 second half)
+
+  auto chunk = [&](int c) {
+    const int qc = qc_last - c * BQ;
+    if (qc < wave_qmin) return;  // no row of the chunk sees this pair's keys
+    const u32x4* stg = smem + (c % NSTF) * STAGE;
+    const uint16_t* stg16 = (const uint16_t*)stg;
+    u32x4* xs = smem + (c % NXF) * S::XSLOT + xo;
+    f32x16 s;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) s[r] = 0.f;
+    __builtin_amdgcn_s_setprio(1);
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+      s = mfma32(stg[(ks >> 1) * SUB + ((ks & 1) ? af1 : af0)], bf[ks], s);
+    __builtin_amdgcn_s_setprio(0);
+    auto tr_frag = [&](int d, int ks) {
+      const int o = d * SUB * 8 + ks * 16 * 32;
+      const u32x2 lo = lds_tr16(stg16 + tr0 + o), hi = lds_tr16(stg16 + tr1 + o);
+      return u32x4{lo[0], lo[1], hi[0], hi[1]};
+    };
+    const f32x4* vLD = (const f32x4*)(stg + S::OFF_LD) + (PWAVE ? 0 : BQ / 4);
+    u32x4 pb[2];
+    if constexpr (PWAVE) {
+      // S -> masked -> P; P to the partner (fp16) and into dV (bf16)
+      const bool need_mask = (qc < qb) | (qc + BQ > qe) | (wk0 + 32 > k1) |
+                             (a.causal & (wk0 + 31 > qc + delta));
+      if (need_mask) {
+        int lo = qb - qc, hi = qe - qc;
+        if (a.causal) lo = max(lo, key - delta - qc);
+        if (!key_ok) hi = lo;
+        lo -= hh * 8;
+        hi -= hh * 8;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int br = (r >> 3) * 16 + (r & 7);
+          s[r] = (br >= lo && br < hi) ? s[r] : neg_inf();
+        }
+      }
+#pragma unroll
+      for (int half = 0; half < 2; ++half) {
+        const f32x4 La = vLD[half * 4 + hh * 2], Lb = vLD[half * 4 + hh * 2 + 1];
+        const float Lr[8] = {La[0], La[1], La[2], La[3], Lb[0], Lb[1], Lb[2], Lb[3]};
+        f32x8 p;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) p[i] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[half * 8 + i], c2, -Lr[i]));
+        pb[half] = __builtin_bit_cast(u32x4, __builtin_convertvector(p, bf16x8));
+        xs[half * 64] = __builtin_bit_cast(u32x4, __builtin_convertvector(p, f16x8));
+      }
+    } else {
+      // dP (in s) and the partner's P -> dS
+#pragma unroll
+      for (int half = 0; half < 2; ++half) {
+        const f32x4 Da = vLD[half * 4 + hh * 2], Db = vLD[half * 4 + hh * 2 + 1];
+        const float Dr[8] = {Da[0], Da[1], Da[2], Da[3], Db[0], Db[1], Db[2], Db[3]};
+        const f32x8 p = __builtin_convertvector(__builtin_bit_cast(f16x8, xs[half * 64]), f32x8);
+        f32x8 ds;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) ds[i] = p[i] * (s[half * 8 + i] - Dr[i]);
+        pb[half] = __builtin_bit_cast(u32x4, __builtin_convertvector(ds, bf16x8));
+      }
+    }
+    __builtin_amdgcn_s_setprio(1);
+#pragma unroll
+    for (int d = 0; d < DB; ++d) {
+      acc[d] = mfma32(tr_frag(d, 0), pb[0], acc[d]);
+      acc[d] = mfma32(tr_frag(d, 1), pb[1], acc[d]);
+    }
+    __builtin_amdgcn_s_setprio(0);
+  };
+
+  for (int t = 0; t < TPBF && t < n_chunks; ++t) issue(t);
+  for (int g = 0; g <= n_groups; ++g) {
+    // group g has landed; every wavefront is done with group g-2 (stages)
+    // and, for the P exchange, with the P of group g-2
+    wait_vmcnt<0>();
+    __syncthreads();
+#pragma unroll
+    for (int t = 0; t < TPBF; ++t)
+      if ((g + 1) * TPBF + t < n_chunks) issue((g + 1) * TPBF + t);
+    const int gw = PWAVE ? g : g - 1;
+    if (gw >= 0 && gw < n_groups) {
+#pragma unroll
+      for (int t = 0; t < TPBF; ++t)
+        if (gw * TPBF + t < n_chunks) chunk(gw * TPBF + t);
+    }
+  }
+
+  if (!key_ok) return;
+  const float sc = PWAVE ? 1.f : a.scale;
+#pragma unroll
+  for (int d = 0; d < DB; ++d)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int dim = d * 32 + j * 8 + hh * 4;
+      const float x0 = acc[d][j * 4] * sc, x1 = acc[d][j * 4 + 1] * sc;
+      const float x2 = acc[d][j * 4 + 2] * sc, x3 = acc[d][j * 4 + 3] * sc;
+      if (a.direct) {
+        const int64_t o = ((int64_t)key * a.Hkv + kvh) * D + dim;
+        *(u32x2*)((PWAVE ? a.dv : a.dk) + o) = pack_bf16x4(x0, x1, x2, x3);
+      } else {
+        const int64_t o = ((int64_t)head * a.T_k + key) * D + dim;
+        *(float4*)((PWAVE ? a.part_v : a.part_k) + o) = make_float4(x0, x1, x2, x3);
+      }
+    }
+}
+
+template <int D>
+__global__ __launch_bounds__(64 * 2 * NPF, 1) void attn_dkdv_fused_kernel(DkdvArgs a) {
+  __shared__ u32x4 smem[FusedStage<D>::SMEM];
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (w < NPF)
+    fused_dkdv_body<D, true>(a, smem, w, lane);
+  else
+    fused_dkdv_body<D, false>(a, smem, w, lane);
+}
+
 }  // namespace
 
 hipError_t launch_attn_dq(const DqArgs& a, int n_items, int D, hipStream_t st) {
@@ -489,8 +690,13 @@ hipError_t launch_attn_dq(const DqArgs& a, int n_items, int D, hipStream_t st) {
 
 hipError_t launch_attn_dkdv(const DkdvArgs& a, int n_items, int D, hipStream_t st) {
   if (n_items <= 0) return hipSuccess;
-  // dV and dK as two kernels (each fits two wavefronts per SIMD)
   const dim3 g(n_items), b(NTK);
+  if constexpr (kDkdvFused) {
+    // one kernel for both gradients (timed under the dK kernel id)
+    if (D == 128) return sp_launch(kKDk, attn_dkdv_fused_kernel<128>, g, b, st, a);
+    return sp_launch(kKDk, attn_dkdv_fused_kernel<64>, g, b, st, a);
+  }
+  // dV and dK as two kernels (each fits two wavefronts per SIMD)
   hipError_t e;
   if (D == 128) {
     if ((e = sp_launch(kKDv, attn_dkdv_kernel<128, 1>, g, b, st, a)) != hipSuccess) return e;

@@ -125,17 +125,6 @@ __global__ __launch_bounds__(NT, 1) void attn_fwd_kernel(FwdArgs a) {
       dma16(vbase + rowoff + o, stg + S::OFF_V + NW * j * 64);
     }
   };
-  // Wait until at most `pending` issued tiles are still in flight.
-  auto wait_tiles = [&](int pending) {
-    if constexpr (NST - 2 * TPB >= 2) {
-      if (pending >= 2) { wait_vmcnt<2 * NBW>(); return; }
-    }
-    if constexpr (NST - 2 * TPB >= 1) {
-      if (pending == 1) { wait_vmcnt<NBW>(); return; }
-    }
-    wait_vmcnt<0>();
-  };
-
   // Lane-constant LDS offsets of the fragments.  K fragment (g, ks): tile row
   // g*32 + perm32(l32), logical chunk 2ks + hh -> sub-tile ks/2 (immediate)
   // and one of two lane bases (ks even / odd).  V^T fragments: transposing
@@ -155,7 +144,7 @@ __global__ __launch_bounds__(NT, 1) void attn_fwd_kernel(FwdArgs a) {
         // tiles n .. n+TPB-1 landed; every wavefront is done with the stages
         // of tiles n-TPB .. n-1, which receive tiles n+NST-TPB ..
         const int issued = min(n_tiles, n + NST - TPB);
-        wait_tiles(issued - min(n_tiles, n + TPB));
+        wait_batches<NBW, NST - 2 * TPB>(issued - min(n_tiles, n + TPB));
         __syncthreads();
 #pragma unroll
         for (int t = 0; t < TPB; ++t)

@@ -131,5 +131,9 @@ static constexpr int kDkdvBQ = 32;
 static constexpr int kDkStages = 4;
 static constexpr int kDvStages = 4;
 static constexpr int kDkdvChunksPerSync = 2;
+// dK and dV in one kernel (wavefront pairs sharing S), 128 keys per item
+static constexpr bool kDkdvFused = true;
+static constexpr int kDkdvFusedBN = 128;
+static constexpr int kDkdvItemKeys = kDkdvFused ? kDkdvFusedBN : kDkdvBN;
 
 }  // namespace spk
