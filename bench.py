@@ -86,8 +86,8 @@ class KernelTimers:
         return out
 
 
-KNAMES = {1: "attn_fwd_kernel", 2: "attn_dq_kernel", 3: "attn_dk_kernel", 4: "pack_kernel",
-          5: "unpack_kernel", 6: "merge_kernel", 7: "attn_dv_kernel"}
+KNAMES = {1: "attn_fwd_kernel", 2: "attn_dq_kernel", 3: "attn_dkdv_kernel", 4: "pack_kernel",
+          5: "unpack_kernel", 6: "merge_kernel"}
 
 
 def lib_desc(sp, sh, pos_k=None):
@@ -175,8 +175,7 @@ class Step:
         H = nr * D
         self.flops_fwd = [4.0 * H * p for p in self.pairs]
         self.flops_dq = [6.0 * H * p for p in self.pairs]
-        self.flops_dk = [6.0 * H * p for p in self.pairs]   # S, dP, dK
-        self.flops_dv = [4.0 * H * p for p in self.pairs]   # S, dV
+        self.flops_dkdv = [8.0 * H * p for p in self.pairs]  # S, dV, dP, dK
         self.flops_metric = 14.0 * H * sum(self.pairs)
         self.flops_strict = 12.0 * H * sum(self.pairs)
         sh_ = sh
@@ -198,8 +197,7 @@ class Step:
             self.dq_acc.zero_()
             for c in range(n):
                 t.arm(sp.SP_KERNEL_ATTN_DQ, self.flops_dq[c])
-                t.arm(sp.SP_KERNEL_ATTN_DK, self.flops_dk[c])
-                t.arm(sp.SP_KERNEL_ATTN_DV, self.flops_dv[c])
+                t.arm(sp.SP_KERNEL_ATTN_DKDV, self.flops_dkdv[c])
                 sp.sp_attn_bwd(self.descs[c], self.q, self.k[c], self.v[c], self.o, self.lse_acc,
                                self.do, dq_acc=self.dq_acc, dk=self.dk[c], dv=self.dv[c],
                                workspace=self.ws_b)
@@ -219,8 +217,7 @@ class Step:
                                  dst=self.o_pre)
             sp.sp_ulysses_pack(self.do_pre, sh.sp, sh.H_loc, self.qmap, dst=self.send_do)
         t.arm(sp.SP_KERNEL_ATTN_DQ, self.flops_dq[0])
-        t.arm(sp.SP_KERNEL_ATTN_DK, self.flops_dk[0])
-        t.arm(sp.SP_KERNEL_ATTN_DV, self.flops_dv[0])
+        t.arm(sp.SP_KERNEL_ATTN_DKDV, self.flops_dkdv[0])
         sp.sp_attn_bwd(self.desc, self.q, self.k, self.v, self.o, self.lse, self.do, dq=self.dq,
                        dk=self.dk, dv=self.dv, workspace=self.ws_b)
         if self.ulysses:
@@ -307,18 +304,20 @@ def measure(sp, torch, name, steps, warmup, per_kernel=True, warmup_s=1.5):
 
 def measured_traffic(kernel, workload_name):
     """HBM bytes per launch of `kernel` from the committed rocprofv3 counter
-    summary (profiles/traffic_<kernel>_<workload>.json), or None when the
-    kernel's source changed since the counters were taken."""
+    summary (profiles/traffic_<kernel>_<workload>.json), or None when any of
+    the kernel's source files changed since the counters were taken."""
     import hashlib
     path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_{workload_name}.json")
     if not os.path.exists(path):
         return None
     with open(path) as f:
         rec = json.load(f)
-    src = os.path.join(ROOT, rec["source"])
-    with open(src, "rb") as f:
-        if hashlib.sha256(f.read()).hexdigest() != rec["source_sha256"]:
-            return None
+    h = hashlib.sha256()
+    for src in rec["sources"]:
+        with open(os.path.join(ROOT, src), "rb") as f:
+            h.update(f.read())
+    if h.hexdigest() != rec["sources_sha256"]:
+        return None
     return rec["hbm_bytes_per_launch"]
 
 

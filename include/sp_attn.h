@@ -250,11 +250,10 @@ sp_status sp_attn_schedule(const sp_attn_desc* desc, int32_t op, int32_t* items,
 enum {
   SP_KERNEL_ATTN_FWD = 1, /* forward / ring-step attention kernel        */
   SP_KERNEL_ATTN_DQ = 2,  /* backward dQ kernel (S, dP, dQ)              */
-  SP_KERNEL_ATTN_DK = 3,  /* backward dK kernel (S, dP, dK)              */
+  SP_KERNEL_ATTN_DKDV = 3,/* backward dK/dV kernel (S, P, dV, dP, dS, dK) */
   SP_KERNEL_PACK = 4,     /* Ulysses pack                                */
   SP_KERNEL_UNPACK = 5,   /* Ulysses unpack                              */
-  SP_KERNEL_LSE_MERGE = 6,/* standalone LSE merge                        */
-  SP_KERNEL_ATTN_DV = 7   /* backward dV kernel (S, dV)                  */
+  SP_KERNEL_LSE_MERGE = 6 /* standalone LSE merge                        */
 };
 sp_status sp_profile_events(int32_t kernel_id, void* start_event, void* stop_event);
 

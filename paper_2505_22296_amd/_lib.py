@@ -85,8 +85,8 @@ EXPORTED = ["sp_status_string", "sp_version", "sp_ulysses_pack", "sp_ulysses_unp
             "sp_attn_workspace_size", "sp_attn_fwd", "sp_attn_bwd", "sp_ring_step",
             "sp_lse_merge", "sp_f32_to_bf16", "sp_attn_schedule", "sp_profile_events"]
 
-SP_KERNEL_ATTN_FWD, SP_KERNEL_ATTN_DQ, SP_KERNEL_ATTN_DK = 1, 2, 3
-SP_KERNEL_PACK, SP_KERNEL_UNPACK, SP_KERNEL_LSE_MERGE, SP_KERNEL_ATTN_DV = 4, 5, 6, 7
+SP_KERNEL_ATTN_FWD, SP_KERNEL_ATTN_DQ, SP_KERNEL_ATTN_DKDV = 1, 2, 3
+SP_KERNEL_PACK, SP_KERNEL_UNPACK, SP_KERNEL_LSE_MERGE = 4, 5, 6
 
 
 def status_string(s: int) -> str:

@@ -220,7 +220,7 @@ void item_counts(const sp_attn_desc* d, const Problem& p, int op, size_t& a, siz
   if (op == SP_OP_BWD) {
     schedule_rows(d, p, spk::kDqBM, spk::kDqBN, true, tmp);
     a = tmp.size() / kItemInts;
-    schedule_keys(d, p, spk::kDkdvItemKeys, spk::kDkdvBQ, tmp);
+    schedule_keys(d, p, spk::kDkdvBN, spk::kDkdvBQ, tmp);
     b = tmp.size() / kItemInts;
   } else {
     schedule_rows(d, p, spk::kFwdBM, spk::kFwdBN, true, tmp);
@@ -359,7 +359,7 @@ sp_status sp_attn_schedule(const sp_attn_desc* desc, int32_t op, int32_t* items,
   if (op == SP_OP_FWD || op == SP_OP_RING_STEP)
     schedule_rows(desc, p, spk::kFwdBM, spk::kFwdBN, true, v);
   else if (op == SP_OP_BWD)
-    schedule_keys(desc, p, spk::kDkdvItemKeys, spk::kDkdvBQ, v);
+    schedule_keys(desc, p, spk::kDkdvBN, spk::kDkdvBQ, v);
   else
     return SP_ERR_INVALID_ARG;
   const int32_t n = (int32_t)(v.size() / kItemInts);
@@ -448,7 +448,7 @@ sp_status sp_attn_bwd(const sp_attn_desc* d, const void* q, const void* k, const
   if ((dq && !aligned16(dq)) || (dq_acc && !aligned16(dq_acc))) return SP_ERR_INVALID_ARG;
   std::vector<int32_t> it_dq, it_kv;
   schedule_rows(d, p, spk::kDqBM, spk::kDqBN, true, it_dq);
-  schedule_keys(d, p, spk::kDkdvItemKeys, spk::kDkdvBQ, it_kv);
+  schedule_keys(d, p, spk::kDkdvBN, spk::kDkdvBQ, it_kv);
   const size_t na = it_dq.size() / kItemInts, nb = it_kv.size() / kItemInts;
   Layout L = layout_for(d, p, SP_OP_BWD, na, nb);
   if ((s = check_ws(L, ws, ws_bytes)) != SP_OK) return s;

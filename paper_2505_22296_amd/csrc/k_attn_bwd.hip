@@ -10,17 +10,17 @@
 //     dS^T = P^T (dP^T - D)          (row statistics are per lane)
 //     dQ^T += K^T dS^T               (K^T by transposing LDS reads; dS^T C
 //                                     registers used directly as B)
-// dk/dv kernels (key-stationary): workgroup = 256 keys of one KV head and
-//   one query head, wavefront w owns 32 keys (K, V rows as B operands in
-//   registers); per 32-row query chunk, visited last to first (Q, dO staged
-//   in LDS):
-//     S = Q K^T, dP = dO V^T          (Q, dO rows loaded in perm32 order)
-//     dS = P (dP - D)
-//     dV^T += dO^T P, dK^T += Q^T dS (dO^T, Q^T by transposing LDS reads;
-//                                     P, dS C registers used directly as B)
-//   With one query head per KV head the results are written as bf16; under
-//   GQA each query head writes a float32 partial that a reduction kernel
-//   sums over the group in ascending head order.
+// dk/dv kernel (key-stationary): workgroup = 128 keys of one KV head and one
+//   query head, 4 wavefront pairs of 32 keys (K resp. V rows as B operands
+//   in registers); per 32-row query chunk, visited last to first (Q, dO
+//   staged in LDS), the pair's P-wavefront computes
+//     S = Q K^T, P, dV^T += dO^T P    (dO^T by transposing LDS reads)
+//   and hands P to the pair's dS-wavefront, which computes
+//     dP = dO V^T, dS = P (dP - D), dK^T += Q^T dS
+//   (Q, dO rows loaded in perm32 order, so P / dS C registers are used
+//   directly as B operands).  With one query head per KV head the results
+//   are written as bf16; under GQA each query head writes a float32 partial
+//   that a reduction kernel sums over the group in ascending head order.
 #include "dev_common.h"
 #include "launch.h"
 
@@ -219,254 +219,14 @@ __global__ __launch_bounds__(NTQ, 1) void attn_dq_kernel(DqArgs a) {
 }
 
 // ---------------------------------------------------------------- dK / dV
-// Workgroup = NWK wavefronts = 32*NWK keys of one KV head and one query head.
-// LDS stage (one 32-row query chunk): Q and dO tiles [32][D] in the blocked
-// layout of dev_common.h (Q^T and dO^T fragments are transposing reads of
-// them) and the chunk's LSE*log2(e) and D rows.  NST chunks resident,
-// barrier every TPBK chunks.
-constexpr int NWK = kDkdvWaves, NTK = 64 * NWK, TPBK = kDkdvChunksPerSync;
-static_assert(kDkdvBN == 32 * NWK, "dkdv tiling");
-
-template <int D, int MODE>
-struct DkdvStage {
-  static constexpr bool DO_V = MODE == 1, DO_K = MODE == 2;
-  static constexpr int BQ = kDkdvBQ;
-  static constexpr int SUB = BQ * 4;            // chunks per sub-tile [BQ][32]
-  static constexpr int RB = BQ * (D / 8) / 64;  // 1 KB blocks of a tile
-  static constexpr int NB = 2 * RB;             // Q, dO
-  static constexpr int NBW = (NB + NWK - 1) / NWK;  // blocks per wavefront (tail ones junk)
-  static constexpr int OFF_O = RB * 64, OFF_LD = NB * 64, STAGE = OFF_LD + 16;  // 16-byte chunks
-  static constexpr int NST = DO_K ? kDkStages : kDvStages;
-  static_assert(NST % TPBK == 0 && NST >= 2 * TPBK, "dkdv stages");
-  static constexpr int JUNK = NST * STAGE, SMEM = JUNK + 64;
-  // tile of block b: 0 Q, 1 dO, 2 none (junk)
-  static SP_DEV int kind(int b) { return b < RB ? 0 : b < NB ? 1 : 2; }
-};
-
-// MODE 1: dV (S, P, dV^T += dO^T P); MODE 2: dK (S, dP, dS, dK^T += Q^T dS).
-// The two kernels both recompute S but each fits two wavefronts per SIMD.
-template <int D, int MODE>
-__global__ __launch_bounds__(NTK, 1) void attn_dkdv_kernel(DkdvArgs a) {
-  using S = DkdvStage<D, MODE>;
-  constexpr bool DO_V = S::DO_V, DO_K = S::DO_K;
-  constexpr int BQ = S::BQ, KS = D / 16, DB = D / 32, SUB = S::SUB;
-  constexpr int NST = S::NST, STAGE = S::STAGE, NBW = S::NBW;
-  constexpr int OFF_O = S::OFF_O, OFF_LD = S::OFF_LD;
-
-  __shared__ u32x4 smem[S::SMEM];
-
-  const int32_t* it = a.items + (int64_t)blockIdx.x * kItemInts;
-  const int k0 = it[0], k1 = it[1], qb = it[2], qe = it[3], delta = it[4], head = it[5],
-            kvh = it[6];
-  const int tid = threadIdx.x;
-  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
-  const int lane = tid & 63, hh = lane >> 5, l32 = lane & 31;
-  const int wk0 = k0 + w * 32;        // first key of this wavefront
-  const int key = wk0 + l32;          // this lane's key (column of S)
-  const bool key_ok = key < k1;
-
-  const int qc_first = qb & ~7;
-  const int n_chunks = (qe > qb) ? (qe - qc_first + BQ - 1) / BQ : 0;
-  const int Tq1 = a.T_q - 1;
-  const int hstride = a.H * D;  // elements between consecutive rows
-  const uint16_t* qh = a.q + (int64_t)head * D;
-  const uint16_t* oh = a.dout + (int64_t)head * D;
-  const float* lh = a.lse2 + (int64_t)head * a.T_q;
-  const float* dh = a.delta + (int64_t)head * a.T_q;
-  // chunks starting at or below this row are invisible to all of this
-  // wavefront's keys (causal) -- their arithmetic is skipped
-  const int wave_qmin = wk0 >= k1 ? 0x7fffffff : a.causal ? wk0 - delta - BQ + 1 : -0x7fffffff;
-
-  // Per-lane, chunk-independent element offsets of this wavefront's DMA
-  // blocks w + NWK*j (block kinds are wave-uniform; Q and dO share shape and
-  // source row stride).
-  int off[NBW], row_of[NBW];
-#pragma unroll
-  for (int j = 0; j < NBW; ++j) {
-    const int b = w + NWK * j;
-    const int k = S::kind(b);
-    const int t = (k == 1 ? b - S::RB : k == 0 ? b : 0) * 64 + lane;
-    const int ts = t % SUB, r = ts / 4;
-    row_of[j] = r;
-    off[j] = r * hstride + (t / SUB) * 32 + blk_chunk(r, ts % 4) * 8;
-  }
-
-  // Chunks are visited from the segment end backwards: every item of a segment
-  // ends at the same row, so blocks running together stream the same rows at
-  // the same time and share them in L2.
-  const int qc_last = qc_first + (n_chunks - 1) * BQ;
-  auto issue = [&](int n) {
-    const int qc = qc_last - n * BQ;
-    u32x4* stg = smem + (n % NST) * STAGE;
-    const bool tail = qc + BQ > a.T_q;  // rows past T_q are clamped to the last row (masked)
-#pragma unroll
-    for (int j = 0; j < NBW; ++j) {
-      const int b = w + NWK * j;
-      const int k = S::kind(b);
-      int o = off[j];
-      if (tail) o += (min(qc + row_of[j], Tq1) - qc - row_of[j]) * hstride;
-      dma16((k == 1 ? oh : qh) + (int64_t)qc * hstride + o, k == 2 ? smem + S::JUNK : stg + b * 64);
-    }
-    // every wavefront copies the LSE / D rows (identical data): uniform DMA counts
-    const int rr = min(qc + (lane & (BQ - 1)), Tq1);
-    dma4((lane < BQ ? lh : dh) + rr, stg + OFF_LD);
-  };
-  // K (and for dK: V) rows as B operands (col = key, k = dims).
-  u32x4 kf[KS], vf[DO_K ? KS : 1];
-  {
-    const int64_t koff = ((int64_t)(key_ok ? key : k0) * a.Hkv + kvh) * D + hh * 8;
-#pragma unroll
-    for (int s = 0; s < KS; ++s) {
-      kf[s] = *(const u32x4*)(a.k + koff + s * 16);
-      if constexpr (DO_K) vf[s] = *(const u32x4*)(a.v + koff + s * 16);
-    }
-  }
-  f32x16 acc[DB];  // dK^T or dV^T: lane = key, registers = dims
-#pragma unroll
-  for (int d = 0; d < DB; ++d)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) acc[d][r] = 0.f;
-  const float c2 = a.scale_log2;
-  // lane-constant LDS offsets of the fragments (see the forward kernel); the
-  // accumulation's A operand is a transposing read of dO (dV) or Q (dK)
-  const int qr = perm32(l32);
-  const int qf0 = qr * 4 + blk_chunk(qr, hh), qf1 = qr * 4 + blk_chunk(qr, 2 + hh);
-  constexpr int OFF_T = DO_K ? 0 : OFF_O * 8;  // element offset of the transposed tile
-  const int tr0 = OFF_T + blk_tr_off(lane), tr1 = OFF_T + blk_tr_off2(lane);
-
-  for (int n = 0; n < NST - TPBK && n < n_chunks; ++n) issue(n);
-
-  for (int n0 = 0; n0 < n_chunks; n0 += NST) {
-#pragma unroll
-    for (int u = 0; u < NST; ++u) {
-      const int n = n0 + u;
-      if (n >= n_chunks) break;
-      if (u % TPBK == 0) {
-        // chunks n .. n+TPBK-1 landed; the stages of chunks n-TPBK .. n-1
-        // are free and receive chunks n+NST-TPBK ..
-        const int issued = min(n_chunks, n + NST - TPBK);
-        wait_batches<NBW + 1, S::NST - 2 * TPBK>(issued - min(n_chunks, n + TPBK));
-        __syncthreads();
-#pragma unroll
-        for (int t = 0; t < TPBK; ++t)
-          if (n + NST - TPBK + t < n_chunks) issue(n + NST - TPBK + t);
-      }
-      const int qc = qc_last - n * BQ;
-      if (qc < wave_qmin) continue;  // no row of the chunk sees this wavefront's keys
-      const u32x4* stg = smem + u * STAGE;
-
-      f32x16 s, dp;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        s[r] = 0.f;
-        dp[r] = 0.f;
-      }
-      __builtin_amdgcn_s_setprio(1);
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        const int fo = (ks >> 1) * SUB + ((ks & 1) ? qf1 : qf0);
-        s = mfma32(stg[fo], kf[ks], s);
-        if constexpr (DO_K) dp = mfma32(stg[OFF_O + fo], vf[ks], dp);
-      }
-      __builtin_amdgcn_s_setprio(0);
-      // A fragments of the accumulation: for dV read while the softmax runs;
-      // dK is at the register limit and reads them next to their MFMAs
-      const uint16_t* stg16 = (const uint16_t*)stg;
-      auto tr_frag = [&](int d, int ks) {
-        const int o = d * SUB * 8 + ks * 16 * 32;
-        const u32x2 lo = lds_tr16(stg16 + tr0 + o), hi = lds_tr16(stg16 + tr1 + o);
-        return u32x4{lo[0], lo[1], hi[0], hi[1]};
-      };
-      u32x4 fa[DO_V ? DB : 1][2];
-      if constexpr (DO_V) {
-#pragma unroll
-        for (int d = 0; d < DB; ++d) {
-          fa[d][0] = tr_frag(d, 0);
-          fa[d][1] = tr_frag(d, 1);
-        }
-      }
-      // the chunk needs masking if it straddles the item's row range, the key
-      // tile's end, or the causal diagonal of this wavefront's keys
-      const bool need_mask = (qc < qb) | (qc + BQ > qe) | (wk0 + 32 > k1) |
-                             (a.causal & (wk0 + 31 > qc + delta));
-      if (need_mask) {
-        // visible chunk rows for this lane's key: lo <= row-in-chunk < hi
-        int lo = qb - qc, hi = qe - qc;
-        if (a.causal) lo = max(lo, key - delta - qc);
-        if (!key_ok) hi = lo;
-        lo -= hh * 8;
-        hi -= hh * 8;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int br = (r >> 3) * 16 + (r & 7);  // chunk row minus hh*8
-          s[r] = (br >= lo && br < hi) ? s[r] : neg_inf();
-        }
-      }
-      const f32x4* vL = (const f32x4*)(stg + OFF_LD);
-      const f32x4* vD = vL + BQ / 4;
-      u32x4 pb[2];
-#pragma unroll
-      for (int half = 0; half < 2; ++half) {
-        const f32x4 La = vL[half * 4 + hh * 2], Lb = vL[half * 4 + hh * 2 + 1];
-        const float Lr[8] = {La[0], La[1], La[2], La[3], Lb[0], Lb[1], Lb[2], Lb[3]};
-        float Dr[8];
-        if constexpr (DO_K) {
-          const f32x4 Da = vD[half * 4 + hh * 2], Db = vD[half * 4 + hh * 2 + 1];
-          Dr[0] = Da[0]; Dr[1] = Da[1]; Dr[2] = Da[2]; Dr[3] = Da[3];
-          Dr[4] = Db[0]; Dr[5] = Db[1]; Dr[6] = Db[2]; Dr[7] = Db[3];
-        }
-        float x[8];
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          const int r = half * 8 + i;
-          const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[r], c2, -Lr[i]));
-          if constexpr (DO_K) x[i] = p * (dp[r] - Dr[i]);  // dS
-          else x[i] = p;                                    // P
-        }
-        pb[half] = pack_bf16x8(x[0], x[1], x[2], x[3], x[4], x[5], x[6], x[7]);
-      }
-      __builtin_amdgcn_s_setprio(1);
-#pragma unroll
-      for (int d = 0; d < DB; ++d) {
-        if constexpr (DO_V) {
-          acc[d] = mfma32(fa[d][0], pb[0], acc[d]);
-          acc[d] = mfma32(fa[d][1], pb[1], acc[d]);
-        } else {
-          acc[d] = mfma32(tr_frag(d, 0), pb[0], acc[d]);
-          acc[d] = mfma32(tr_frag(d, 1), pb[1], acc[d]);
-        }
-      }
-      __builtin_amdgcn_s_setprio(0);
-    }
-  }
-
-  if (!key_ok) return;
-  const float sc = DO_K ? a.scale : 1.f;
-#pragma unroll
-  for (int d = 0; d < DB; ++d)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int dim = d * 32 + j * 8 + hh * 4;
-      const float x0 = acc[d][j * 4] * sc, x1 = acc[d][j * 4 + 1] * sc;
-      const float x2 = acc[d][j * 4 + 2] * sc, x3 = acc[d][j * 4 + 3] * sc;
-      if (a.direct) {
-        const int64_t o = ((int64_t)key * a.Hkv + kvh) * D + dim;
-        *(u32x2*)((DO_K ? a.dk : a.dv) + o) = pack_bf16x4(x0, x1, x2, x3);
-      } else {
-        const int64_t o = ((int64_t)head * a.T_k + key) * D + dim;
-        *(float4*)((DO_K ? a.part_k : a.part_v) + o) = make_float4(x0, x1, x2, x3);
-      }
-    }
-}
-
-// ------------------------------------------------------- fused dK / dV
 // Workgroup = 8 wavefronts = 4 pairs; pair p owns keys k0 + 32p .. +32.
 // Per 32-row query chunk the pair splits the work: its P-wavefront (w < 4)
 // computes S = Q K^T, P and dV^T += dO^T P and hands P to its partner through
 // LDS (fp16: P lies in [0, 1]); the dS-wavefront (w >= 4) computes
 // dP = dO V^T, dS = P (dP - D) and dK^T += Q^T dS.  S is evaluated once per
 // pair (8*D MFMA work per pair instead of 10*D for separate dK and dV
-// kernels) and the Q / dO chunk tiles are staged once for both gradients.
+// kernels, which would each recompute S) and the Q / dO chunk tiles are
+// staged once for both gradients.
 // Chunks go in groups of TPBF between barriers: in group g the
 // P-wavefronts work on group g, the dS-wavefronts on group g-1 (whose P is
 // complete), while group g+1 is copied in; stages hold three groups and the
@@ -475,10 +235,10 @@ constexpr int NPF = kDkdvWaves / 2;  // wavefront pairs per workgroup
 constexpr int TPBF = 2;              // chunks per group (barrier interval)
 constexpr int NSTF = 3 * TPBF;       // resident chunks
 constexpr int NXF = 2 * TPBF;        // P exchange slots
-static_assert(kDkdvFusedBN == 32 * NPF, "fused dkdv tiling");
+static_assert(kDkdvBN == 32 * NPF, "dkdv tiling");
 
 template <int D>
-struct FusedStage {
+struct DkdvStage {
   static constexpr int BQ = kDkdvBQ;
   static constexpr int SUB = BQ * 4;            // chunks per sub-tile [BQ][32]
   static constexpr int RB = BQ * (D / 8) / 64;  // 1 KB blocks of a tile
@@ -491,8 +251,8 @@ struct FusedStage {
 };
 
 template <int D, bool PWAVE>
-SP_DEV void fused_dkdv_body(const DkdvArgs& a, u32x4* smem, int w, int lane) {
-  using S = FusedStage<D>;
+SP_DEV void dkdv_body(const DkdvArgs& a, u32x4* smem, int w, int lane) {
+  using S = DkdvStage<D>;
   constexpr int BQ = S::BQ, KS = D / 16, DB = D / 32, SUB = S::SUB, NBW = S::NBW;
   constexpr int STAGE = S::STAGE;
   const int32_t* it = a.items + (int64_t)blockIdx.x * kItemInts;
@@ -670,14 +430,14 @@ SP_DEV void fused_dkdv_body(const DkdvArgs& a, u32x4* smem, int w, int lane) {
 }
 
 template <int D>
-__global__ __launch_bounds__(64 * 2 * NPF, 1) void attn_dkdv_fused_kernel(DkdvArgs a) {
-  __shared__ u32x4 smem[FusedStage<D>::SMEM];
+__global__ __launch_bounds__(64 * 2 * NPF, 1) void attn_dkdv_kernel(DkdvArgs a) {
+  __shared__ u32x4 smem[DkdvStage<D>::SMEM];
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (w < NPF)
-    fused_dkdv_body<D, true>(a, smem, w, lane);
+    dkdv_body<D, true>(a, smem, w, lane);
   else
-    fused_dkdv_body<D, false>(a, smem, w, lane);
+    dkdv_body<D, false>(a, smem, w, lane);
 }
 
 }  // namespace
@@ -690,20 +450,9 @@ hipError_t launch_attn_dq(const DqArgs& a, int n_items, int D, hipStream_t st) {
 
 hipError_t launch_attn_dkdv(const DkdvArgs& a, int n_items, int D, hipStream_t st) {
   if (n_items <= 0) return hipSuccess;
-  const dim3 g(n_items), b(NTK);
-  if constexpr (kDkdvFused) {
-    // one kernel for both gradients (timed under the dK kernel id)
-    if (D == 128) return sp_launch(kKDk, attn_dkdv_fused_kernel<128>, g, b, st, a);
-    return sp_launch(kKDk, attn_dkdv_fused_kernel<64>, g, b, st, a);
-  }
-  // dV and dK as two kernels (each fits two wavefronts per SIMD)
-  hipError_t e;
-  if (D == 128) {
-    if ((e = sp_launch(kKDv, attn_dkdv_kernel<128, 1>, g, b, st, a)) != hipSuccess) return e;
-    return sp_launch(kKDk, attn_dkdv_kernel<128, 2>, g, b, st, a);
-  }
-  if ((e = sp_launch(kKDv, attn_dkdv_kernel<64, 1>, g, b, st, a)) != hipSuccess) return e;
-  return sp_launch(kKDk, attn_dkdv_kernel<64, 2>, g, b, st, a);
+  const dim3 g(n_items), b(64 * 2 * NPF);
+  if (D == 128) return sp_launch(kKDkdv, attn_dkdv_kernel<128>, g, b, st, a);
+  return sp_launch(kKDkdv, attn_dkdv_kernel<64>, g, b, st, a);
 }
 
 }  // namespace spk

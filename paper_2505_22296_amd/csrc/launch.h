@@ -8,7 +8,7 @@ namespace spk {
 
 // Kernel identifiers of the opt-in per-thread launch timer (values match the
 // SP_KERNEL_* constants of the public header).
-enum KernelId { kKFwd = 1, kKDq = 2, kKDk = 3, kKPack = 4, kKUnpack = 5, kKMerge = 6, kKDv = 7, kKCount = 8 };
+enum KernelId { kKFwd = 1, kKDq = 2, kKDkdv = 3, kKPack = 4, kKUnpack = 5, kKMerge = 6, kKCount = 7 };
 
 struct KernelTimer {
   hipEvent_t start = nullptr, stop = nullptr;
@@ -125,15 +125,8 @@ static constexpr int kDqBM = 32 * kDqWaves;
 static constexpr int kDqBN = 32;
 static constexpr int kDqStages = 4;
 static constexpr int kDqTilesPerSync = 2;
-static constexpr int kDkdvWaves = 8;                // wavefronts per dK / dV workgroup
-static constexpr int kDkdvBN = 32 * kDkdvWaves;
-static constexpr int kDkdvBQ = 32;
-static constexpr int kDkStages = 4;
-static constexpr int kDvStages = 4;
-static constexpr int kDkdvChunksPerSync = 2;
-// dK and dV in one kernel (wavefront pairs sharing S), 128 keys per item
-static constexpr bool kDkdvFused = true;
-static constexpr int kDkdvFusedBN = 128;
-static constexpr int kDkdvItemKeys = kDkdvFused ? kDkdvFusedBN : kDkdvBN;
+static constexpr int kDkdvWaves = 8;                // wavefronts per dK/dV workgroup (4 pairs)
+static constexpr int kDkdvBN = 16 * kDkdvWaves;     // keys per dK/dV item
+static constexpr int kDkdvBQ = 32;                  // query rows per chunk
 
 }  // namespace spk
