@@ -268,10 +268,15 @@ def measure(sp, torch, name, steps, warmup, per_kernel=True, warmup_s=1.5):
     sh = workload(name)
     timers = KernelTimers(sp, torch)
     st = Step(sp, torch, sh, timers)
-    # The event pool for the timed steps is created and exercised during the
-    # warmup: the first launches that record fresh timing events run slowly.
+    # Every timing event is created and recorded once before the timed
+    # region (fresh events record slowly), and nothing but one synchronize
+    # separates the last warmup step from the first timed one: the GPU
+    # clock drops within milliseconds of idling and takes ~20 ms to recover.
     timers.on = per_kernel
     timers.reserve(8 * (steps + warmup))
+    marks = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    for m in marks:
+        m.record()
     # W warmup steps, continued until ~1.5 s of GPU work so clocks settle
     t_w = time.perf_counter()
     n_w = 0
@@ -282,11 +287,7 @@ def measure(sp, torch, name, steps, warmup, per_kernel=True, warmup_s=1.5):
         n_w += 1
         if n_w % 4 == 0:
             torch.cuda.synchronize()
-    torch.cuda.synchronize()
     timers.used = []
-    marks = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
-    for m in marks:
-        m.record()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(steps):

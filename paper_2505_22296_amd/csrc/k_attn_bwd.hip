@@ -230,11 +230,12 @@ __global__ __launch_bounds__(NTQ, 1) void attn_dq_kernel(DqArgs a) {
 // Chunks go in groups of TPBF between barriers: in group g the
 // P-wavefronts work on group g, the dS-wavefronts on group g-1 (whose P is
 // complete), while group g+1 is copied in; stages hold three groups and the
-// P exchange two.
+// P exchange has one slot per stage, so the loop unrolled over three groups
+// addresses both with immediate offsets.
 constexpr int NPF = kDkdvWaves / 2;  // wavefront pairs per workgroup
 constexpr int TPBF = 2;              // chunks per group (barrier interval)
 constexpr int NSTF = 3 * TPBF;       // resident chunks
-constexpr int NXF = 2 * TPBF;        // P exchange slots
+constexpr int NXF = NSTF;            // P exchange slots (one per stage)
 static_assert(kDkdvBN == 32 * NPF, "dkdv tiling");
 
 template <int D>
@@ -324,12 +325,13 @@ SP_DEV void dkdv_body(const DkdvArgs& a, u32x4* smem, int w, int lane) {
   const int tr1 = (PWAVE ? S::OFF_O * 8 : 0) + blk_tr_off2(lane);
   const int xo = S::OFF_X + pr * 128 + lane;  // this lane's P exchange chunk (+64 second half)
 
-  auto chunk = [&](int c) {
+  // chunk c sits in stage (and exchange slot) `st` == c % NSTF
+  auto chunk = [&](int c, int st) {
     const int qc = qc_last - c * BQ;
     if (qc < wave_qmin) return;  // no row of the chunk sees this pair's keys
-    const u32x4* stg = smem + (c % NSTF) * STAGE;
+    const u32x4* stg = smem + st * STAGE;
     const uint16_t* stg16 = (const uint16_t*)stg;
-    u32x4* xs = smem + (c % NXF) * S::XSLOT + xo;
+    u32x4* xs = smem + st * S::XSLOT + xo;
     f32x16 s;
 #pragma unroll
     for (int r = 0; r < 16; ++r) s[r] = 0.f;
@@ -393,20 +395,27 @@ SP_DEV void dkdv_body(const DkdvArgs& a, u32x4* smem, int w, int lane) {
     __builtin_amdgcn_s_setprio(0);
   };
 
+  constexpr int NGS = NSTF / TPBF;  // groups per stage cycle
   for (int t = 0; t < TPBF && t < n_chunks; ++t) issue(t);
-  for (int g = 0; g <= n_groups; ++g) {
-    // group g has landed; every wavefront is done with group g-2 (stages)
-    // and, for the P exchange, with the P of group g-2
-    wait_vmcnt<0>();
-    __syncthreads();
+  for (int g0 = 0; g0 <= n_groups; g0 += NGS) {
 #pragma unroll
-    for (int t = 0; t < TPBF; ++t)
-      if ((g + 1) * TPBF + t < n_chunks) issue((g + 1) * TPBF + t);
-    const int gw = PWAVE ? g : g - 1;
-    if (gw >= 0 && gw < n_groups) {
+    for (int u = 0; u < NGS; ++u) {
+      const int g = g0 + u;
+      if (g > n_groups) break;
+      // group g has landed; every wavefront is done with group g-2 (its
+      // stages and exchange slots receive group g+1)
+      wait_vmcnt<0>();
+      __syncthreads();
 #pragma unroll
       for (int t = 0; t < TPBF; ++t)
-        if (gw * TPBF + t < n_chunks) chunk(gw * TPBF + t);
+        if ((g + 1) * TPBF + t < n_chunks) issue((g + 1) * TPBF + t);
+      const int gw = PWAVE ? g : g - 1;
+      if (gw >= 0 && gw < n_groups) {
+#pragma unroll
+        for (int t = 0; t < TPBF; ++t)
+          if (gw * TPBF + t < n_chunks)
+            chunk(gw * TPBF + t, (TPBF * (PWAVE ? u : u + NGS - 1) + t) % NSTF);
+      }
     }
   }
 
