@@ -146,12 +146,15 @@ __global__ __launch_bounds__(NT, 1) void attn_fwd_kernel(FwdArgs a) {
         const int issued = min(n_tiles, n + NST - TPB);
         wait_batches<NBW, NST - 2 * TPB>(issued - min(n_tiles, n + TPB));
         __syncthreads();
-#pragma unroll
-        for (int t = 0; t < TPB; ++t)
-          if (n + NST - TPB + t < n_tiles) issue(n + NST - TPB + t);
       }
+      // tile n + NST - TPB goes to a stage freed at the last barrier; its
+      // copy is issued after this tile's first MFMAs (spreads the DMA burst)
+      const bool pf = n + NST - TPB < n_tiles;
       const int kt = kt_first + n * BN;
-      if (kt >= wave_kmax) continue;  // wholly past this wavefront's rows
+      if (kt >= wave_kmax) {  // wholly past this wavefront's rows
+        if (pf) issue(n + NST - TPB);
+        continue;
+      }
       const u32x4* stg = smem + u * STAGE;
 
       // ---- S^T = K Q^T for the two 32-key halves of the tile
@@ -167,6 +170,7 @@ __global__ __launch_bounds__(NT, 1) void attn_fwd_kernel(FwdArgs a) {
         for (int ks = 0; ks < KS; ++ks)
           s[g] = mfma32(stg[(ks >> 1) * SUB + g * 128 + ((ks & 1) ? kf1 : kf0)], qf[ks], s[g]);
       __builtin_amdgcn_s_setprio(0);
+      if (pf) issue(n + NST - TPB);
 
       // ---- mask (only on edge / diagonal tiles)
       const bool need_mask = (kt < k0) | (kt + BN > k1) | (a.causal & (kt + BN - 1 > q0 + w * 32 + delta));
