@@ -334,6 +334,73 @@ def copy_calibration(torch, nbytes=1 << 30):
     del a, b
 
 
+def bandwidth(sp, torch, reps=24):
+    """GB/s of the bandwidth kernels at the workloads' shapes: the Ulysses
+    pack/unpack of the 7B-like (c1) and long (c4) shards and the fp32 LSE
+    merge of the ring shard (c3).  Buffer sets rotate (>= 4 sets, > 1 GB in
+    total) so that the 256 MB last-level cache cannot serve repeats; each
+    call is timed with HIP events, the median is reported."""
+    out = []
+    HBM_PEAK = 8000.0  # GB/s
+
+    def run(label, nbytes, sets, call):
+        n = max(4, -(-(1 << 30) // max(nbytes, 1)) + 1)
+        bufs = [sets() for _ in range(n)]
+        for i in range(5):
+            call(bufs[i % n])
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(reps)]
+        torch.cuda.synchronize()
+        for i, (a, b) in enumerate(ev):
+            a.record()
+            call(bufs[i % n])
+            b.record()
+        torch.cuda.synchronize()
+        ts = sorted(a.elapsed_time(b) for a, b in ev)
+        med = ts[len(ts) // 2]
+        gbs = nbytes / (med * 1e-3) / 1e9
+        out.append({"bandwidth_kernel": label, "bytes": int(nbytes), "buffer_sets": n,
+                    "ms_median": round(med, 4), "ms_min": round(ts[0], 4),
+                    "GB_per_s": round(gbs, 1), "frac_of_hbm_peak": round(gbs / HBM_PEAK, 4)})
+        del bufs
+
+    for name in ("ulysses_7b_L32768_q28kv4_sp8_r6_d128", "ulysses_long_L131072_4x32768_q40kv8_sp16_r13_d128"):
+        sh = workload(name)
+        Tl, hs, spn, Hl, D = sh.T_q // sh.sp, sh.hs, sh.sp, sh.H_loc, sh.D
+        hmap = ulysses_q_head_map(hs, spn)
+        el = 2 * D
+        rd, wr = Tl * hs * el, Tl * spn * Hl * el
+
+        def mk_pack(Tl=Tl, hs=hs, spn=spn, Hl=Hl, D=D):
+            src = torch.empty((Tl, hs, D), dtype=torch.bfloat16, device="cuda").normal_()
+            return src, torch.empty((spn, Tl, Hl, D), dtype=torch.bfloat16, device="cuda")
+
+        run(f"pack {name} [{Tl},{hs},{D}] -> [{spn},{Tl},{Hl},{D}]", rd + wr, mk_pack,
+            lambda b, spn=spn, Hl=Hl, hmap=hmap: sp.sp_ulysses_pack(b[0], spn, Hl, hmap, dst=b[1]))
+
+        def mk_unpack(Tl=Tl, hs=hs, spn=spn, Hl=Hl, D=D):
+            src = torch.empty((spn, Tl, Hl, D), dtype=torch.bfloat16, device="cuda").normal_()
+            return src, torch.empty((Tl, hs, D), dtype=torch.bfloat16, device="cuda")
+
+        run(f"unpack {name} [{spn},{Tl},{Hl},{D}] -> [{Tl},{hs},{D}]", 2 * rd, mk_unpack,
+            lambda b, hs=hs, hmap=hmap: sp.sp_ulysses_unpack(b[0], hmap, hs, dst=b[1]))
+
+    sh = workload("ring_L131072_8chunks_r4_q28kv4_d128")
+    T, H, D = sh.chunk, sh.H_loc, sh.D
+    mb = T * H * (D * 4 * 2 + D * 4 + 12)
+
+    def mk_merge():
+        o = torch.empty((T, H, D), dtype=torch.float32, device="cuda").normal_()
+        lse = torch.empty((H, T), dtype=torch.float32, device="cuda").normal_()
+        op = torch.empty((T, H, D), dtype=torch.float32, device="cuda").normal_()
+        lp = torch.empty((H, T), dtype=torch.float32, device="cuda").normal_()
+        return o, lse, op, lp
+
+    run(f"lse_merge ring_L131072_8chunks_r4_q28kv4_d128 fp32 partial [{T},{H},{D}]", mb, mk_merge,
+        lambda b: sp.sp_lse_merge(b[0], b[1], b[2], b[3]))
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -347,6 +414,8 @@ def main():
                     help="keep warming up until this much time has passed")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run one 1 GiB device copy first (counter scaling)")
+    ap.add_argument("--bandwidth", action="store_true",
+                    help="only measure the pack / unpack / LSE-merge kernels (one JSON line each)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path "
@@ -357,6 +426,10 @@ def main():
     sp.load()
     if args.copy_calibration:
         copy_calibration(torch)
+    if args.bandwidth:
+        for rec in bandwidth(sp, torch):
+            print(json.dumps(rec), flush=True)
+        return
     names = WORKLOADS if args.all else [args.workload]
     for name in names:
         sh, st, ms, ks, per_step = measure(sp, torch, name, args.steps, args.warmup,
