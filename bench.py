@@ -34,7 +34,8 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 from workloads import (allowed_pairs, ring_chunk_positions, shard_inputs, randn_bf16_bits,  # noqa: E402
-                       ulysses_kv_head_map, ulysses_q_head_map, workload, WORKLOADS)
+                       ulysses_kv_head_map, ulysses_q_head_map, workload, WORKLOADS,
+                       zigzag_inputs, zigzag_step_positions)
 
 METRIC = "attn fwd+bwd TFLOP/s (real heads) per SP-rank shard; % of bf16 MFMA peak"
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA, published
@@ -97,7 +98,7 @@ def lib_desc(sp, sh, pos_k=None):
                    Hkv_loc=sh.Hkv_loc, kv_head_offset=sh.kv_head_offset,
                    cu_seqlens_q=sh.cu_q, cu_seqlens_k=sh.cu_k, position_ids_q=sh.pos_q,
                    position_ids_k=sh.pos_k if pos_k is None else pos_k, causal=sh.causal,
-                   softmax_scale=sh.scale)
+                   softmax_scale=sh.scale, single_sequence=sh.single_sequence)
 
 
 def to_dev(torch, bits):
@@ -113,7 +114,20 @@ class Step:
         D = sh.D
         self.ring = sh.ring_chunks > 0
         nr = sh.n_real_loc
-        if self.ring:
+        if self.ring and sh.zigzag_sp:
+            # zigzag ring: the rank's two chunks against the two chunks of each step
+            self.descs = [lib_desc(sp, sh, zigzag_step_positions(sh, s))
+                          for s in range(sh.ring_chunks)]
+            self.pairs = [allowed_pairs(sh.cu_q, sh.cu_k, sh.pos_q, zigzag_step_positions(sh, s),
+                                        single_sequence=True) for s in range(sh.ring_chunks)]
+            q, do = zigzag_inputs(sh)
+            self.q, self.do = to_dev(torch, q), to_dev(torch, do)
+            self.k, self.v = [], []
+            for s in range(sh.ring_chunks):
+                k, v = zigzag_inputs(sh, s)
+                self.k.append(to_dev(torch, k))
+                self.v.append(to_dev(torch, v))
+        elif self.ring:
             self.descs = [lib_desc(sp, sh, ring_chunk_positions(sh, c)) for c in range(sh.ring_chunks)]
             self.pairs = [allowed_pairs(sh.cu_q, sh.cu_k, sh.pos_q, ring_chunk_positions(sh, c))
                           for c in range(sh.ring_chunks)]
@@ -124,6 +138,7 @@ class Step:
                 _, k, v, _ = shard_inputs(sh, chunk=c)
                 self.k.append(to_dev(torch, k))
                 self.v.append(to_dev(torch, v))
+        if self.ring:
             self.o_acc = torch.empty((sh.T_q, sh.H_loc, D), dtype=torch.float32, device=dev)
             self.lse_acc = torch.empty((sh.H_loc, sh.T_q), dtype=torch.float32, device=dev)
             self.o = torch.empty((sh.T_q, sh.H_loc, D), dtype=torch.bfloat16, device=dev)
@@ -131,10 +146,10 @@ class Step:
             self.dq = torch.empty((sh.T_q, sh.H_loc, D), dtype=torch.bfloat16, device=dev)
             self.dk = [torch.empty_like(x) for x in self.k]
             self.dv = [torch.empty_like(x) for x in self.v]
-            self.ws_f = torch.empty(sp.sp_attn_workspace_size(self.descs[0], sp.SP_OP_RING_STEP),
-                                    dtype=torch.uint8, device=dev)
-            self.ws_b = torch.empty(sp.sp_attn_workspace_size(self.descs[0], sp.SP_OP_BWD),
-                                    dtype=torch.uint8, device=dev)
+            self.ws_f = torch.empty(max(sp.sp_attn_workspace_size(d, sp.SP_OP_RING_STEP)
+                                        for d in self.descs), dtype=torch.uint8, device=dev)
+            self.ws_b = torch.empty(max(sp.sp_attn_workspace_size(d, sp.SP_OP_BWD)
+                                        for d in self.descs), dtype=torch.uint8, device=dev)
         else:
             self.desc = lib_desc(sp, sh)
             self.pairs = [allowed_pairs(sh.cu_q, sh.cu_k, sh.pos_q, sh.pos_k)]

@@ -88,6 +88,20 @@ enum { SP_OP_FWD = 0, SP_OP_BWD = 1, SP_OP_RING_STEP = 2 };
  * offsets here (Q chunk r at r*C.., KV chunk c at c*C..).  NULL means
  * positions 0,1,.. restarting at every segment.
  */
+/*
+ * SP_DESC_SINGLE_SEQUENCE: the num_seqs segments on each side are PIECES of
+ * one sequence rather than separate sequences -- e.g. the zigzag split of
+ * Ring-Attention (Section 3.2), where a rank holds chunks r and 2*sp-1-r of
+ * the sequence and each ring step brings two KV chunks.  Every query row may
+ * see every key; with causal = 1, key j is visible from row i iff
+ * position_ids_k[j] <= position_ids_q[i].  Both position arrays are then
+ * required, and over the rows [0, cu_seqlens_q[num_seqs]) (keys
+ * [0, cu_seqlens_k[num_seqs])) they must increase strictly -- pieces in
+ * ascending position order, each a +1 ramp.  Rows / keys past the last
+ * piece are padding as usual.
+ */
+#define SP_DESC_SINGLE_SEQUENCE 1
+
 typedef struct sp_attn_desc {
   int32_t T_q;              /* query tokens at this rank (rows of q, o, dq)         */
   int32_t T_k;              /* key tokens (rows of k, v, dk, dv)                     */
@@ -102,7 +116,7 @@ typedef struct sp_attn_desc {
   int32_t num_seqs;         /* segments (>= 0)                                       */
   int32_t causal;           /* 1 = causal by position inside a segment, 0 = full     */
   float softmax_scale;      /* multiplies q.k (callers pass 1/sqrt(D))               */
-  int32_t reserved;         /* must be 0                                             */
+  int32_t flags;            /* 0 or SP_DESC_SINGLE_SEQUENCE                          */
   const int32_t* cu_seqlens_q;   /* HOST, num_seqs + 1                               */
   const int32_t* cu_seqlens_k;   /* HOST, num_seqs + 1                               */
   const int32_t* position_ids_q; /* HOST, T_q, or NULL                               */

@@ -19,6 +19,7 @@ LIB_PATH = os.path.join(HERE, "libspattn.so")
 
 SP_OK, SP_ERR_INVALID_ARG, SP_ERR_UNSUPPORTED, SP_ERR_WORKSPACE, SP_ERR_HIP = range(5)
 SP_OP_FWD, SP_OP_BWD, SP_OP_RING_STEP = 0, 1, 2
+SP_DESC_SINGLE_SEQUENCE = 1
 SCHED_ITEM_INTS = 8
 
 _i32p = ctypes.POINTER(ctypes.c_int32)
@@ -32,7 +33,7 @@ class SpAttnDesc(ctypes.Structure):
         ("gqa_group", ctypes.c_int32), ("Hkv_loc", ctypes.c_int32),
         ("kv_head_offset", ctypes.c_int32), ("num_seqs", ctypes.c_int32),
         ("causal", ctypes.c_int32), ("softmax_scale", ctypes.c_float),
-        ("reserved", ctypes.c_int32),
+        ("flags", ctypes.c_int32),
         ("cu_seqlens_q", _i32p), ("cu_seqlens_k", _i32p),
         ("position_ids_q", _i32p), ("position_ids_k", _i32p),
     ]
@@ -104,7 +105,7 @@ class Desc:
     def __init__(self, *, T_q, T_k, head_dim, H_loc, head_offset, num_real_heads,
                  num_padded_heads, gqa_group, Hkv_loc, kv_head_offset, cu_seqlens_q,
                  cu_seqlens_k, position_ids_q=None, position_ids_k=None, causal=True,
-                 softmax_scale=None):
+                 softmax_scale=None, single_sequence=False):
         self._keep = []
 
         def arr(x):
@@ -121,7 +122,8 @@ class Desc:
             gqa_group=gqa_group, Hkv_loc=Hkv_loc, kv_head_offset=kv_head_offset,
             num_seqs=max(0, len(cq) - 1), causal=1 if causal else 0,
             softmax_scale=(1.0 / math.sqrt(head_dim)) if softmax_scale is None else softmax_scale,
-            reserved=0, cu_seqlens_q=arr(cu_seqlens_q), cu_seqlens_k=arr(cu_seqlens_k),
+            flags=SP_DESC_SINGLE_SEQUENCE if single_sequence else 0,
+            cu_seqlens_q=arr(cu_seqlens_q), cu_seqlens_k=arr(cu_seqlens_k),
             position_ids_q=arr(position_ids_q), position_ids_k=arr(position_ids_k))
 
     @property

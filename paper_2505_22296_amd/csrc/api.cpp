@@ -33,7 +33,12 @@ struct Seg {
 struct Problem {
   int D = 0;
   int n_real = 0;  // real local query heads: slots [0, n_real)
-  std::vector<Seg> segs;
+  // Row-side and key-side runs: rows [qa, qb) x keys [ka, kb) with key j
+  // visible from row i iff j <= i + delta (causal).  For separate sequences
+  // both lists are the segments; for one sequence in pieces they are the
+  // maximal row (key) ranges over which the visible key (row) range grows
+  // by 0 or 1 per row (key).
+  std::vector<Seg> segs, segs_k;
   int q_pad = 0, k_pad = 0;  // first padding row / key
   std::vector<int> kv_of;    // per real local head
   std::vector<int> kv_lo, kv_hi;  // per local KV head: real heads [lo, hi) reading it
@@ -41,9 +46,63 @@ struct Problem {
 };
 
 
+// One sequence in pieces (SP_DESC_SINGLE_SEQUENCE): rows [0, Qn) and keys
+// [0, Kn) have strictly increasing positions, so the keys visible from row i
+// are a prefix [0, n(i)) and the rows that see key j a suffix [m(j), Qn).
+// n and m are split into maximal runs of constant step 0 or 1; each run is a
+// Seg whose linear rule j <= i + delta reproduces the prefix / suffix.
+sp_status single_sequence_runs(const sp_attn_desc* d, Problem& p) {
+  const int n = d->num_seqs;
+  if (n < 1 || !d->position_ids_q || !d->position_ids_k) return SP_ERR_INVALID_ARG;
+  const int Qn = d->cu_seqlens_q[n], Kn = d->cu_seqlens_k[n];
+  const int32_t* pq = d->position_ids_q;
+  const int32_t* pk = d->position_ids_k;
+  for (int i = 1; i < Qn; ++i)
+    if (pq[i] <= pq[i - 1]) return SP_ERR_INVALID_ARG;
+  for (int j = 1; j < Kn; ++j)
+    if (pk[j] <= pk[j - 1]) return SP_ERR_INVALID_ARG;
+  std::vector<int> cnt(Qn), first(Kn);
+  for (int i = 0, j = 0; i < Qn; ++i) {  // n(i) = #keys with pos_k <= pos_q[i]
+    if (d->causal)
+      while (j < Kn && pk[j] <= pq[i]) ++j;
+    cnt[i] = d->causal ? j : Kn;
+  }
+  for (int j = 0, i = 0; j < Kn; ++j) {  // m(j) = first row with pos_q >= pos_k[j]
+    if (d->causal)
+      while (i < Qn && pq[i] < pk[j]) ++i;
+    first[j] = d->causal ? i : 0;
+  }
+  p.segs.clear();
+  for (int i0 = 0; i0 < Qn;) {
+    const int step = (i0 + 1 < Qn) ? cnt[i0 + 1] - cnt[i0] : 0;
+    int i1 = i0 + 1;
+    if (step == 0 || step == 1)
+      while (i1 < Qn && cnt[i1] - cnt[i1 - 1] == step) ++i1;
+    // step 1: keys [0, cnt[i]) = j <= i + cnt[i0] - 1 - i0; step 0 (or a
+    // single row): keys [0, cnt[i0]), every one of them visible
+    const int delta = (i1 - i0 > 1 && step == 1) ? cnt[i0] - 1 - i0 : cnt[i0];
+    p.segs.push_back(Seg{i0, i1, 0, cnt[i1 - 1], delta});
+    i0 = i1;
+  }
+  p.segs_k.clear();
+  for (int j0 = 0; j0 < Kn;) {
+    const int step = (j0 + 1 < Kn) ? first[j0 + 1] - first[j0] : 0;
+    int j1 = j0 + 1;
+    if (step == 0 || step == 1)
+      while (j1 < Kn && first[j1] - first[j1 - 1] == step) ++j1;
+    // step 1: rows [first[j], Qn) = j <= i + j0 - first[j0]; step 0 (or a
+    // single key): rows [first[j0], Qn), visible from every key of the run
+    const int delta = (j1 - j0 > 1 && step == 1) ? j0 - first[j0] : (j1 - 1) - first[j0];
+    p.segs_k.push_back(Seg{first[j0], Qn, j0, j1, delta});
+    j0 = j1;
+  }
+  return SP_OK;
+}
+
 sp_status validate(const sp_attn_desc* d, Problem& p) {
   if (!d) return SP_ERR_INVALID_ARG;
-  if (d->reserved != 0) return SP_ERR_INVALID_ARG;
+  if (d->flags & ~SP_DESC_SINGLE_SEQUENCE) return SP_ERR_INVALID_ARG;
+  const bool single = (d->flags & SP_DESC_SINGLE_SEQUENCE) != 0;
   if (d->T_q < 0 || d->T_k < 0 || d->T_q >= kMaxTokens || d->T_k >= kMaxTokens)
     return SP_ERR_INVALID_ARG;
   if (d->head_dim != 64 && d->head_dim != 128) return SP_ERR_UNSUPPORTED;
@@ -118,6 +177,8 @@ sp_status validate(const sp_attn_desc* d, Problem& p) {
       p.segs.push_back(g);
     }
   }
+  p.segs_k = p.segs;
+  if (single) return single_sequence_runs(d, p);
   return SP_OK;
 }
 
@@ -164,7 +225,7 @@ void schedule_keys(const sp_attn_desc* d, const Problem& p, int BNK, int BQ,
                    std::vector<int32_t>& out) {
   std::vector<Item> items;
   for (int y = 0; y < p.n_real; ++y) {
-    for (const Seg& g : p.segs) {
+    for (const Seg& g : p.segs_k) {
       for (int a = g.ka; a < g.kb; a += BNK) {
         const int b = std::min(a + BNK, g.kb);
         int q0 = g.qa;

@@ -27,7 +27,11 @@ def header_functions():
 
 
 def oracle_kw(sh: Shard, pos_q=None, pos_k=None, causal=None):
-    return dict(cu_q=sh.cu_q, cu_k=sh.cu_k,
+    # pieces of one sequence are one segment for the oracle (its mask then
+    # depends on positions alone)
+    cu_q = np.array([0, sh.cu_q[-1]]) if sh.single_sequence else sh.cu_q
+    cu_k = np.array([0, sh.cu_k[-1]]) if sh.single_sequence else sh.cu_k
+    return dict(cu_q=cu_q, cu_k=cu_k,
                 pos_q=sh.pos_q if pos_q is None else pos_q,
                 pos_k=sh.pos_k if pos_k is None else pos_k,
                 H_loc=sh.H_loc, head_offset=sh.head_offset, num_real_heads=sh.num_real_heads,
@@ -43,7 +47,8 @@ def lib_desc(sh: Shard, pos_q=None, pos_k=None, causal=None, T_k=None):
                 Hkv_loc=sh.Hkv_loc, kv_head_offset=sh.kv_head_offset, cu_seqlens_q=sh.cu_q,
                 cu_seqlens_k=sh.cu_k, position_ids_q=sh.pos_q if pos_q is None else pos_q,
                 position_ids_k=sh.pos_k if pos_k is None else pos_k,
-                causal=sh.causal if causal is None else causal, softmax_scale=sh.scale)
+                causal=sh.causal if causal is None else causal, softmax_scale=sh.scale,
+                single_sequence=sh.single_sequence)
 
 
 def to_dev(bits: np.ndarray):
@@ -79,7 +84,8 @@ def assert_close(gpu, ref, what, max_abs=MAX_ABS, rel_l2=REL_L2):
 
 
 def make_shard(name, T_q, T_k, D, H_loc, head_offset, num_real, num_padded, gqa, Hkv_loc,
-               kv_off, seg_q, seg_k=None, pos_q=None, pos_k=None, causal=True, seed_base=0):
+               kv_off, seg_q, seg_k=None, pos_q=None, pos_k=None, causal=True, seed_base=0,
+               single_sequence=False):
     """Explicit small problem (segments given as lengths; positions default to
     0.. per segment)."""
     cu_q = np.concatenate([[0], np.cumsum(seg_q)]).astype(np.int32)
@@ -96,4 +102,4 @@ def make_shard(name, T_q, T_k, D, H_loc, head_offset, num_real, num_padded, gqa,
                  Hkv_loc=Hkv_loc, kv_head_offset=kv_off, cu_q=cu_q, cu_k=cu_k,
                  pos_q=ramp(cu_q, T_q) if pos_q is None else np.asarray(pos_q, np.int32),
                  pos_k=ramp(cu_k, T_k) if pos_k is None else np.asarray(pos_k, np.int32),
-                 causal=causal, seed_base=seed_base)
+                 causal=causal, seed_base=seed_base, single_sequence=single_sequence)

@@ -252,6 +252,40 @@ def pin_ring_fold(A, S):
     assert np.allclose(np.concatenate(dvs), dvm, atol=1e-12)
 
 
+def pin_zigzag_fold(A, S):
+    """Zigzag ring (Section 3.2): the sequence cut into 2*sp chunks, rank r
+    holding chunks r and 2*sp-1-r.  For every rank, folding its sp ring steps
+    (each bringing the two chunks of rank (r - s) mod sp, positions jumping
+    between the pieces) equals monolithic causal attention of its rows over
+    the whole sequence; per-step dK/dV summed over all ranks and steps equal
+    the monolithic dK/dV of every key."""
+    rng = np.random.default_rng(12)
+    sp, C, H, Hkv, D = 3, 6, 4, 2, 5
+    L = 2 * sp * C
+    q_full, k_full, v_full, do_full = (_rand(rng, L, H, D), _rand(rng, L, Hkv, D),
+                                       _rand(rng, L, Hkv, D), _rand(rng, L, H, D))
+    common = dict(H_loc=H, head_offset=0, num_real_heads=H, gqa_group=2, kv_head_offset=0, scale=0.41)
+    full = dict(cu_q=np.array([0, L]), cu_k=np.array([0, L]), pos_q=np.arange(L), pos_k=np.arange(L),
+                **common)
+    Om, Lm = A.attn_forward(q_full, k_full, v_full, **full)
+    dqm, dkm, dvm = A.attn_backward(q_full, k_full, v_full, do_full, **full)
+    dk_sum, dv_sum = np.zeros_like(k_full), np.zeros_like(v_full)
+    for r in range(sp):
+        rows = np.r_[r * C + np.arange(C), (2 * sp - 1 - r) * C + np.arange(C)]
+        steps = [(r - s) % sp for s in range(sp)]
+        keys = [np.r_[j * C + np.arange(C), (2 * sp - 1 - j) * C + np.arange(C)] for j in steps]
+        chunks = [(k_full[kk], v_full[kk]) for kk in keys]
+        o, lse = S.ring_forward(q_full[rows], chunks, q_pos=rows, kv_pos=keys, **common)
+        assert np.allclose(o, Om[rows], atol=1e-12) and np.allclose(lse, Lm[:, rows], atol=1e-12)
+        dq, dks, dvs = S.ring_backward(q_full[rows], chunks, do_full[rows], o, lse, q_pos=rows,
+                                       kv_pos=keys, **common)
+        assert np.allclose(dq, dqm[rows], atol=1e-12)
+        for kk, a, b in zip(keys, dks, dvs):
+            dk_sum[kk] += a
+            dv_sum[kk] += b
+    assert np.allclose(dk_sum, dkm, atol=1e-12) and np.allclose(dv_sum, dvm, atol=1e-12)
+
+
 def pin_merge_identity(S):
     """(0, -inf) is the merge identity; the merge is commutative; two
     all-masked partials give (0, -inf) without NaN."""
@@ -317,4 +351,4 @@ def pin_pack_unpack(S):
 ATTN_PINS = [pin_single_visible_key, pin_zero_query_uniform, pin_torch_sdpa,
              pin_finite_differences, pin_gradient_sums, pin_packed_equals_separate]
 SP_PINS = [pin_merge_identity, pin_pack_unpack]
-BOTH_PINS = [pin_ring_fold, pin_ulysses_equals_no_sp]
+BOTH_PINS = [pin_ring_fold, pin_zigzag_fold, pin_ulysses_equals_no_sp]

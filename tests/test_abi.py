@@ -8,7 +8,7 @@ import pytest
 
 import paper_2505_22296_amd as sp
 from oracle import attention as A
-from tests.helpers import header_functions, lib_desc, make_shard
+from tests.helpers import header_functions, lib_desc, make_shard, oracle_kw
 from workloads import workload, WORKLOADS
 
 
@@ -36,6 +36,12 @@ def _ws_status(d, op=sp.SP_OP_FWD):
     return sp.load().sp_attn_workspace_size(d.ref, op, ctypes.byref(n)), n.value
 
 
+def test_unknown_descriptor_flags_rejected():
+    d = _good()
+    d.c.flags = 2
+    assert _ws_status(d)[0] == sp.SP_ERR_INVALID_ARG
+
+
 @pytest.mark.parametrize("over,expect", [
     (dict(), sp.SP_OK),
     (dict(head_dim=96), sp.SP_ERR_UNSUPPORTED),
@@ -51,6 +57,14 @@ def _ws_status(d, op=sp.SP_OP_FWD):
     (dict(position_ids_q=np.r_[np.arange(100), np.arange(156) * 2]), sp.SP_ERR_INVALID_ARG),
     (dict(position_ids_q=np.r_[np.arange(100) + 7, np.arange(156)]), sp.SP_OK),
     (dict(T_q=-1), sp.SP_ERR_INVALID_ARG),
+    # pieces of one sequence: positions required and strictly increasing
+    (dict(single_sequence=True, position_ids_q=np.arange(256), position_ids_k=np.arange(256)),
+     sp.SP_OK),
+    (dict(single_sequence=True), sp.SP_ERR_INVALID_ARG),
+    (dict(single_sequence=True, position_ids_q=np.r_[np.arange(100) + 500, np.arange(156)],
+          position_ids_k=np.arange(256)), sp.SP_ERR_INVALID_ARG),
+    (dict(single_sequence=True, position_ids_q=np.r_[np.arange(100), np.arange(156) + 300],
+          position_ids_k=np.r_[np.arange(100) + 50, np.arange(156) + 1000]), sp.SP_OK),
 ])
 def test_descriptor_validation(over, expect):
     st, n = _ws_status(_good(**over))
@@ -137,6 +151,21 @@ CASES = [
                causal=False),
     make_shard("future_keys", 64, 64, 64, 1, 0, 1, 1, 1, 1, 0, [64], [64],
                pos_q=np.arange(64), pos_k=500 + np.arange(64)),
+    # pieces of one sequence: a zigzag rank (chunks 1 and 6 of 8, C = 40)
+    # against each of its four ring steps, uneven pieces with gaps, and the
+    # non-causal case
+    *[make_shard(f"zigzag_r1_step{st}", 80, 80, 128, 2, 0, 2, 2, 1, 2, 0, [40, 40], [40, 40],
+                 pos_q=np.r_[40 + np.arange(40), 240 + np.arange(40)],
+                 pos_k=np.r_[40 * a + np.arange(40), 40 * (7 - a) + np.arange(40)],
+                 single_sequence=True)
+      for st, a in enumerate([1, 0, 3, 2])],
+    make_shard("pieces_uneven", 70, 90, 64, 1, 0, 1, 1, 1, 1, 0, [10, 45, 15], [25, 5, 60],
+               pos_q=np.r_[5 + np.arange(10), 40 + np.arange(45), 200 + np.arange(15)],
+               pos_k=np.r_[np.arange(25), 60 + np.arange(5), 100 + np.arange(60)],
+               single_sequence=True),
+    make_shard("pieces_noncausal", 50, 60, 64, 1, 0, 1, 1, 1, 1, 0, [20, 30], [30, 30],
+               pos_q=np.r_[np.arange(20), 100 + np.arange(30)], pos_k=50 + np.arange(60),
+               causal=False, single_sequence=True),
 ]
 
 
@@ -146,7 +175,8 @@ def test_schedule_covers_exactly_the_mask(sh):
     once by the forward schedule and once by the dK/dV schedule, and no
     disallowed pair is; dummy heads never appear (bit-exact integer check)."""
     d = lib_desc(sh)
-    seg_q, seg_k = A.segment_ids(sh.cu_q, sh.T_q), A.segment_ids(sh.cu_k, sh.T_k)
+    kw = oracle_kw(sh)
+    seg_q, seg_k = A.segment_ids(kw["cu_q"], sh.T_q), A.segment_ids(kw["cu_k"], sh.T_k)
     mask = A.allowed_mask(np.arange(sh.T_q), seg_q, seg_k, sh.pos_q, sh.pos_k, sh.causal)
     real = [h for h in range(sh.H_loc) if sh.head_offset + h < sh.num_real_heads]
     for op, kind in ((sp.SP_OP_FWD, "rows"), (sp.SP_OP_BWD, "keys")):

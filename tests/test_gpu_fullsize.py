@@ -13,7 +13,8 @@ import pytest
 import oracle
 from tests.helpers import (LSE_MAX_ABS, assert_close, bits_from_dev, from_dev, lib_desc, oracle_kw,
                            to_dev)
-from workloads import ring_chunk_positions, shard_inputs, workload, WORKLOADS
+from workloads import (ring_chunk_positions, shard_inputs, workload, WORKLOADS, zigzag_inputs,
+                       zigzag_step_positions)
 
 pytestmark = [pytest.mark.gpu, pytest.mark.timeout(300)]
 
@@ -66,7 +67,7 @@ def _grad_sums(sh, dk, dv, do, nr):
             assert np.abs(got - want).max() <= 1e-2 * max(1.0, np.abs(want).max()), ("sum dV", s, kv)
 
 
-@pytest.mark.parametrize("name", [w for w in WORKLOADS if not w.startswith("ring")])
+@pytest.mark.parametrize("name", [w for w in WORKLOADS if not w.startswith(("ring", "zigzag"))])
 def test_fullsize_shard(sp, name):
     import torch
     sh = workload(name)
@@ -155,6 +156,68 @@ def test_fullsize_ring_rank(sp):
     assert_close(from_dev(dks[-1][kl]), RdK, "ring dK keys")
     assert_close(from_dev(dvs[-1][kl]), RdV, "ring dV keys")
     # whole-array identities over all chunks
+    dk_all = np.concatenate([from_dev(x) for x in dks])
+    dv_all = np.concatenate([from_dev(x) for x in dvs])
+    for kv in range(sh.Hkv_loc):
+        heads = [h for h in range(H) if sh.kv_of(h) == kv]
+        assert np.abs(dk_all[:, kv].sum(axis=0)).max() <= 2e-2 * np.sqrt((dk_all[:, kv] ** 2).sum())
+        want = dof[:, heads].sum(axis=(0, 1))
+        assert np.abs(dv_all[:, kv].sum(axis=0) - want).max() <= 1e-2 * max(1.0, np.abs(want).max())
+
+
+def test_fullsize_zigzag_rank(sp):
+    """Zigzag ring rank 4 of 8 (Section 3.2; chunks 4 and 11 of 16, 8192
+    tokens each, 28 query / 4 KV heads): 8 ring steps over pieces of one
+    sequence with the fused merge, then per-step backward into an fp32 dQ
+    accumulator.  Oracle: monolithic attention over the keys of all steps
+    (positions decide visibility), on sampled rows and keys; whole-array
+    gradient identities over all steps."""
+    import torch
+    sh = [workload(w) for w in WORKLOADS if w.startswith("zigzag")][0]
+    n, T, H, D = sh.ring_chunks, sh.T_q, sh.H_loc, sh.D
+    q, do = zigzag_inputs(sh)
+    kvs = [zigzag_inputs(sh, s) for s in range(n)]
+    pks = [zigzag_step_positions(sh, s) for s in range(n)]
+    Q, dO = to_dev(q), to_dev(do)
+    Ks, Vs = [to_dev(k) for k, _ in kvs], [to_dev(v) for _, v in kvs]
+    o_acc = torch.empty((T, H, D), dtype=torch.float32, device="cuda")
+    lse = torch.empty((H, T), dtype=torch.float32, device="cuda")
+    o = torch.empty((T, H, D), dtype=torch.bfloat16, device="cuda")
+    descs = [lib_desc(sh, pos_k=pks[s]) for s in range(n)]
+    for s in range(n):
+        sp.sp_ring_step(descs[s], Q, Ks[s], Vs[s], o_acc, lse, init=(s == 0),
+                        o_out=o if s == n - 1 else None)
+    dq_acc = torch.zeros((T, H, D), dtype=torch.float32, device="cuda")
+    dks, dvs = [], []
+    for s in range(n):
+        _, gk, gv = sp.sp_attn_bwd(descs[s], Q, Ks[s], Vs[s], o, lse, dO, dq_acc=dq_acc)
+        dks.append(gk)
+        dvs.append(gv)
+    torch.cuda.synchronize()
+    kcat = oracle.bf16_bits_to_f64(np.concatenate([k for k, _ in kvs]))
+    vcat = oracle.bf16_bits_to_f64(np.concatenate([v for _, v in kvs]))
+    pcat = np.concatenate(pks)
+    qf, dof = oracle.bf16_bits_to_f64(q), oracle.bf16_bits_to_f64(do)
+    kw = dict(cu_q=np.array([0, T]), cu_k=np.array([0, n * T]), pos_q=sh.pos_q, pos_k=pcat,
+              H_loc=H, head_offset=0, num_real_heads=H, gqa_group=sh.gqa_group,
+              kv_head_offset=0, scale=sh.scale, causal=True)
+    C = sh.chunk
+    rows = np.array(sorted({0, 1, C - 1, C, C + 1, T - 1} |
+                           set(np.random.default_rng(2).integers(0, T, 10).tolist())))
+    RO, RL = oracle.attn_forward(qf, kcat, vcat, rows=rows, **kw)
+    ridx = torch.from_numpy(rows).cuda()
+    assert_close(from_dev(o[ridx]), RO, "zigzag O rows")
+    assert np.abs(lse[:, ridx].cpu().numpy() - RL).max() <= LSE_MAX_ABS
+    RdQ, _, _ = oracle.attn_dq_rows(qf, kcat, vcat, dof, rows[::2], **kw)
+    assert_close(dq_acc[torch.from_numpy(rows[::2]).cuda()].cpu().numpy().astype(np.float64), RdQ,
+                 "zigzag dQ rows")
+    # keys at the end of the rank's own second chunk (step 0): only the last
+    # rows see them, so the oracle evaluates few rows
+    loc = np.array([2 * C - 1, 2 * C - 3, 2 * C - 40])
+    RdK, RdV = oracle.attn_dkdv_keys(qf, kcat, vcat, dof, loc, **kw)
+    kl = torch.from_numpy(loc).cuda()
+    assert_close(from_dev(dks[0][kl]), RdK, "zigzag dK keys")
+    assert_close(from_dev(dvs[0][kl]), RdV, "zigzag dV keys")
     dk_all = np.concatenate([from_dev(x) for x in dks])
     dv_all = np.concatenate([from_dev(x) for x in dvs])
     for kv in range(sh.Hkv_loc):

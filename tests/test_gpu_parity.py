@@ -98,6 +98,11 @@ CASES = [
     ("noncausal_varlen_d64", 300, 280, 64, 3, 0, 3, 3, 3, 1, 0, [100, 200], [180, 100],
      dict(causal=False)),
     ("gqa2_partial_d128", 257, 257, 128, 4, 0, 4, 4, 2, 2, 0, [129, 128], None, {}),
+    # pieces of one sequence (SP_DESC_SINGLE_SEQUENCE), uneven, with gaps
+    ("pieces_uneven_d128", 300, 330, 128, 2, 0, 2, 2, 1, 2, 0, [40, 200, 60], [100, 30, 200],
+     dict(pos_q=np.r_[10 + np.arange(40), 150 + np.arange(200), 600 + np.arange(60)],
+          pos_k=np.r_[np.arange(100), 140 + np.arange(30), 400 + np.arange(200)],
+          single_sequence=True)),
 ]
 
 
@@ -242,3 +247,52 @@ def test_ring_rank_fwd_bwd(sp):
     for c in range(r + 1):
         assert_close(dks[c], RdKs[c], f"ring dK chunk {c}")
         assert_close(dvs[c], RdVs[c], f"ring dV chunk {c}")
+
+
+@pytest.mark.parametrize("D,Hkv", [(128, 2), (64, 4)])
+def test_zigzag_rank_fwd_bwd(sp, D, Hkv):
+    """Zigzag ring (Section 3.2) with sp = 3 and 2*sp chunks of C tokens:
+    rank 1 holds chunks 1 and 4 and meets, step by step, the chunks of ranks
+    1, 0, 2 -- every step is one sp_ring_step / sp_attn_bwd over pieces of one
+    sequence (SP_DESC_SINGLE_SEQUENCE) whose positions jump between pieces.
+    Oracle: ring fold and per-step backward over the same pieces."""
+    import torch
+    spn, C, r, H = 3, 72, 1, 4
+    base = make_shard("zigzag", 2 * C, 2 * C, D, H, 0, H, H, H // Hkv, Hkv, 0, [C, C], [C, C],
+                      single_sequence=True)
+    pos_q = np.r_[r * C + np.arange(C), (2 * spn - 1 - r) * C + np.arange(C)]
+    q = randn_bf16_bits((2 * C, H, D), 61)
+    do = randn_bf16_bits((2 * C, H, D), 62)
+    steps = [(r - s) % spn for s in range(spn)]
+    kvpos = [np.r_[j * C + np.arange(C), (2 * spn - 1 - j) * C + np.arange(C)] for j in steps]
+    ks = [randn_bf16_bits((2 * C, Hkv, D), 70 + s) for s in range(spn)]
+    vs = [randn_bf16_bits((2 * C, Hkv, D), 80 + s) for s in range(spn)]
+    dq = to_dev(q)
+    o_acc = torch.empty((2 * C, H, D), dtype=torch.float32, device="cuda")
+    lse_acc = torch.empty((H, 2 * C), dtype=torch.float32, device="cuda")
+    o_bf = torch.empty((2 * C, H, D), dtype=torch.bfloat16, device="cuda")
+    for s in range(spn):
+        d = lib_desc(base, pos_q=pos_q, pos_k=kvpos[s])
+        sp.sp_ring_step(d, dq, to_dev(ks[s]), to_dev(vs[s]), o_acc, lse_acc, init=(s == 0),
+                        o_out=o_bf if s == spn - 1 else None)
+    common = dict(H_loc=H, head_offset=0, num_real_heads=H, gqa_group=H // Hkv, kv_head_offset=0,
+                  scale=base.scale)
+    chunks = [(_dec(ks[s]), _dec(vs[s])) for s in range(spn)]
+    RO, RL = oracle.ring_forward(_dec(q), chunks, q_pos=pos_q, kv_pos=kvpos, **common)
+    assert_close(o_acc.cpu().numpy().astype(np.float64), RO, "zigzag O acc")
+    assert_close(from_dev(o_bf), RO, "zigzag O bf16")
+    assert np.abs(lse_acc.cpu().numpy() - RL).max() <= LSE_MAX_ABS
+    dq_acc = torch.zeros((2 * C, H, D), dtype=torch.float32, device="cuda")
+    dks, dvs = [], []
+    for s in range(spn):
+        d = lib_desc(base, pos_q=pos_q, pos_k=kvpos[s])
+        _, gk, gv = sp.sp_attn_bwd(d, dq, to_dev(ks[s]), to_dev(vs[s]), o_bf, lse_acc, to_dev(do),
+                                   dq_acc=dq_acc)
+        dks.append(from_dev(gk))
+        dvs.append(from_dev(gv))
+    RdQ, RdKs, RdVs = oracle.ring_backward(_dec(q), chunks, _dec(do), RO, RL, q_pos=pos_q,
+                                           kv_pos=kvpos, **common)
+    assert_close(dq_acc.cpu().numpy().astype(np.float64), RdQ, "zigzag dQ")
+    for s in range(spn):
+        assert_close(dks[s], RdKs[s], f"zigzag dK step {s}")
+        assert_close(dvs[s], RdVs[s], f"zigzag dV step {s}")

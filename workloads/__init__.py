@@ -127,6 +127,12 @@ class Shard:
     # Ring bookkeeping: number of KV chunks this rank loops over (0 = not ring).
     ring_chunks: int = 0
     chunk: int = 0
+    # Zigzag ring (Section 3.2): the sequence is cut into 2*zigzag_sp chunks,
+    # rank r holds chunks r and 2*zigzag_sp-1-r, and ring step s brings the
+    # two chunks of rank (r - s) mod zigzag_sp.  Q and each step's KV are
+    # pieces of one sequence (single_sequence).
+    zigzag_sp: int = 0
+    single_sequence: bool = False
 
     @property
     def scale(self) -> float:
@@ -208,6 +214,53 @@ def _ring(name, L, n_chunks, rank, D, hq, hkv, seed_base) -> Shard:
                  ring_chunks=rank + 1, chunk=C, rank=rank, sp=1)
 
 
+def _zigzag(name, L, sp, rank, D, hq, hkv, seed_base) -> Shard:
+    C = L // (2 * sp)
+    cu = np.array([0, C, 2 * C], dtype=np.int32)
+    a, b = zigzag_chunks(rank, sp)
+    pos_q = np.concatenate([a * C + np.arange(C), b * C + np.arange(C)]).astype(np.int32)
+    return Shard(name=name, T_q=2 * C, T_k=2 * C, D=D, H_loc=hq, head_offset=0,
+                 num_real_heads=hq, num_padded_heads=hq, gqa_group=hq // hkv,
+                 Hkv_loc=hkv, kv_head_offset=0, cu_q=cu, cu_k=cu.copy(), pos_q=pos_q,
+                 pos_k=pos_q.copy(), causal=True, seed_base=seed_base, hs=hq, hkv=hkv,
+                 ring_chunks=sp, chunk=C, rank=rank, sp=1, zigzag_sp=sp, single_sequence=True)
+
+
+def zigzag_chunks(rank: int, sp: int):
+    """The two sequence chunks (of 2*sp) a zigzag rank holds, in position order."""
+    return rank, 2 * sp - 1 - rank
+
+
+def zigzag_step_chunks(sh: Shard, s: int):
+    """Sequence chunks of the KV that zigzag ring step s brings to the rank."""
+    return zigzag_chunks((sh.rank - s) % sh.zigzag_sp, sh.zigzag_sp)
+
+
+def zigzag_step_positions(sh: Shard, s: int) -> np.ndarray:
+    C = sh.chunk
+    a, b = zigzag_step_chunks(sh, s)
+    return np.concatenate([a * C + np.arange(C), b * C + np.arange(C)]).astype(np.int32)
+
+
+def zigzag_inputs(sh: Shard, s: int = None):
+    """bf16 bits of a zigzag shard: (q, do) for the rank's two chunks when s
+    is None, else (k, v) of ring step s.  Every sequence chunk has its own
+    seeds, so a chunk's data is the same wherever it appears."""
+    C, sb = sh.chunk, sh.seed_base
+
+    def piece(c, off, H):
+        return randn_bf16_bits((C, H, sh.D), sb + off + 16 * (c + 1))
+    if s is None:
+        chunks = zigzag_chunks(sh.rank, sh.zigzag_sp)
+        q = np.concatenate([piece(c, 0, sh.H_loc) for c in chunks])
+        do = np.concatenate([piece(c, 3, sh.H_loc) for c in chunks])
+        return q, do
+    chunks = zigzag_step_chunks(sh, s)
+    k = np.concatenate([piece(c, 1, sh.Hkv_loc) for c in chunks])
+    v = np.concatenate([piece(c, 2, sh.Hkv_loc) for c in chunks])
+    return k, v
+
+
 def ring_chunk_positions(sh: Shard, c: int) -> np.ndarray:
     """Positions of KV chunk c under the contiguous ring split."""
     return _ramp_positions(sh.cu_k, sh.T_k, c * sh.chunk)
@@ -225,6 +278,8 @@ def workload(name: str) -> Shard:
         return _ring(name, 131072, 8, 4, 128, 28, 4, 300)
     if name == "ulysses_long_L131072_4x32768_q40kv8_sp16_r13_d128":
         return _ulysses(name, 131072, 128, 40, 8, 16, 13, [32768] * 4, 400)
+    if name == "zigzag_ring_L131072_sp8_r4_q28kv4_d128":
+        return _zigzag(name, 131072, 8, 4, 128, 28, 4, 500)
     raise KeyError(name)
 
 
@@ -234,6 +289,7 @@ WORKLOADS = [
     "packed_varlen_T65536_q4kv1_d128",
     "ring_L131072_8chunks_r4_q28kv4_d128",
     "ulysses_long_L131072_4x32768_q40kv8_sp16_r13_d128",
+    "zigzag_ring_L131072_sp8_r4_q28kv4_d128",
 ]
 
 
@@ -260,10 +316,18 @@ def shard_inputs(sh: Shard, peaky: float = 1.0, chunk: Optional[int] = None):
     return q, k, v, do
 
 
-def allowed_pairs(cu_q, cu_k, pos_q, pos_k, causal: bool = True) -> int:
+def allowed_pairs(cu_q, cu_k, pos_q, pos_k, causal: bool = True,
+                  single_sequence: bool = False) -> int:
     """Number of (query, key) pairs the mask allows, per head: same segment
-    index and, when causal, pos_k <= pos_q.  Positions must be +1 ramps inside
-    each segment, so each segment's count has a closed form."""
+    index (any valid row / key for pieces of one sequence) and, when causal,
+    pos_k <= pos_q.  Positions must be +1 ramps inside each segment (and
+    increase strictly over all pieces of one sequence)."""
+    if single_sequence:
+        nq, nk = int(cu_q[-1]), int(cu_k[-1])
+        if not causal:
+            return nq * nk
+        return int(np.searchsorted(np.asarray(pos_k[:nk], np.int64),
+                                   np.asarray(pos_q[:nq], np.int64), side="right").sum())
     total = 0
     for s in range(len(cu_q) - 1):
         qa, qb = int(cu_q[s]), int(cu_q[s + 1])
