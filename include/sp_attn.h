@@ -255,10 +255,10 @@ sp_status sp_attn_schedule(const sp_attn_desc* desc, int32_t op, int32_t* items,
 /*
  * Opt-in kernel timer (measurement support, per calling thread).  After
  * sp_profile_events(id, start, stop) with hipEvent_t handles created by the
- * caller, every launch of kernel `id` made by THIS thread records `start` when
- * the kernel begins and `stop` when it ends (hipExtLaunchKernelGGL), on the
- * stream of the call.  If a call launches that kernel more than once, the
- * events describe the last launch.  Pass NULL events to disarm.  This is the
+ * caller, every launch of kernel `id` made by THIS thread records `start` on
+ * the stream of the call immediately before the kernel is launched and `stop`
+ * immediately after it (hipEventRecord).  If a call launches that kernel more
+ * than once, the events describe the last launch.  Pass NULL events to disarm.  This is the
  * only state the library keeps (thread-local, no allocation).
  */
 enum {

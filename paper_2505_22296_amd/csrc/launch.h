@@ -1,6 +1,5 @@
 // Internal interface between the host-side ABI code and the gfx950 kernels.
 #pragma once
-#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -17,16 +16,22 @@ struct KernelTimer {
 KernelTimer& timer_for(int kernel_id);
 
 // Launch `kernel`; when the calling thread armed events for `id`, record them
-// at the kernel's start and end (hipExtLaunchKernelGGL).
+// on the same stream immediately before and after the launch.  (Plain event
+// records: passing events to hipExtLaunchKernelGGL was measured to stall the
+// running kernels by ~5 ms per dispatch for ~0.2 s after new events are first
+// used that way.)
 template <typename F, typename... Args>
 inline hipError_t sp_launch(int id, F kernel, dim3 grid, dim3 block, hipStream_t st,
                             Args... args) {
   KernelTimer& t = timer_for(id);
-  if (t.start || t.stop)
-    hipExtLaunchKernelGGL(kernel, grid, block, 0, st, t.start, t.stop, 0, args...);
-  else
-    hipLaunchKernelGGL(kernel, grid, block, 0, st, args...);
-  return hipGetLastError();
+  if (t.start) {
+    hipError_t e = hipEventRecord(t.start, st);
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(kernel, grid, block, 0, st, args...);
+  hipError_t e = hipGetLastError();
+  if (e == hipSuccess && t.stop) e = hipEventRecord(t.stop, st);
+  return e;
 }
 
 // Maximum head-map entries a pack/unpack carries by value in its arguments.
