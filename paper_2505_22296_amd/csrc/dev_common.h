@@ -111,20 +111,42 @@ SP_DEV int blk_tr_off2(int lane) {
   return row * 32 + blk_chunk(row, col >> 3) * 8 + (col & 7);
 }
 
-SP_DEV float wave_max_xor32(float x) { return fmaxf(x, __shfl_xor(x, 32)); }
-SP_DEV float wave_sum_xor32(float x) { return x + __shfl_xor(x, 32); }
+// Combine a value with the one of lane l^32 through v_permlane32_swap_b32
+// (a VALU op; a shuffle would go through LDS with ds_bpermute).  Called with
+// the same register as both operands, the swap returns {x[l & 31], x[l | 32]}
+// in some order on every lane, so max / sum of the two is the xor-32 result.
+SP_DEV float wave_max_xor32(float x) {
+  const uint32_t u = __float_as_uint(x);
+  const auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+SP_DEV float wave_sum_xor32(float x) {
+  const uint32_t u = __float_as_uint(x);
+  const auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
 
-// Direct global -> LDS copy of 16 bytes per lane (gfx950 global_load_lds_dwordx4).
-// `lds_block` must be wave-uniform: lane i's 16 bytes land at lds_block + 16 i.
-// Completion is tracked by vmcnt only; callers wait with wait_vmcnt<N>() and a
-// barrier before other wavefronts read the data.
+// Direct global -> LDS copy of 16 (4) bytes per lane (gfx950
+// global_load_lds_dwordx4 / _dword).  `lds_block` must be wave-uniform: lane
+// i's bytes land at lds_block + 16 i (4 i).  Completion is tracked by vmcnt
+// only; callers wait with wait_vmcnt<N>() and a barrier before other
+// wavefronts read the data, and never copy into a stage that is being read.
+// The copies are issued from inline assembly on purpose: the compiler treats
+// an LDS DMA it can see as a pending write to all of LDS and inserts
+// s_waitcnt vmcnt(0) before every later LDS read and barrier, which drains
+// the multi-stage prefetch on every tile.  Hidden from it, the only vmcnt
+// waits are the explicit ones of the staging protocol.
+SP_DEV uint32_t lds_addr(const void* lds_block) {
+  return __builtin_amdgcn_readfirstlane(
+      (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const void*)lds_block);
+}
 SP_DEV void dma16(const void* gsrc, void* lds_block) {
-  __builtin_amdgcn_global_load_lds(gsrc, (__attribute__((address_space(3))) void*)lds_block, 16,
-                                   0, 0);
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
+               :: "v"(gsrc), "s"(lds_addr(lds_block)) : "memory", "m0");
 }
 SP_DEV void dma4(const void* gsrc, void* lds_block) {
-  __builtin_amdgcn_global_load_lds(gsrc, (__attribute__((address_space(3))) void*)lds_block, 4,
-                                   0, 0);
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dword %0, off"
+               :: "v"(gsrc), "s"(lds_addr(lds_block)) : "memory", "m0");
 }
 // s_waitcnt vmcnt(N) leaving expcnt / lgkmcnt unconstrained (gfx9 encoding).
 template <int N>

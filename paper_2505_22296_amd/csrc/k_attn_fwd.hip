@@ -157,7 +157,16 @@ __global__ __launch_bounds__(NT, 1) void attn_fwd_kernel(FwdArgs a) {
       }
       const u32x4* stg = smem + u * STAGE;
 
-      // ---- S^T = K Q^T for the two 32-key halves of the tile
+      // ---- S^T = K Q^T for the two 32-key halves of the tile.  All K
+      // fragments are read before the first MFMA, so the LDS latency is
+      // paid once per tile instead of once per MFMA.
+      u32x4 kfr[2 * KS];
+#pragma unroll
+      for (int g = 0; g < 2; ++g)
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
+          kfr[g * KS + ks] = stg[(ks >> 1) * SUB + g * 128 + ((ks & 1) ? kf1 : kf0)];
+      __builtin_amdgcn_sched_barrier(0);
       f32x16 s[2];
 #pragma unroll
       for (int g = 0; g < 2; ++g)
@@ -165,11 +174,22 @@ __global__ __launch_bounds__(NT, 1) void attn_fwd_kernel(FwdArgs a) {
         for (int r = 0; r < 16; ++r) s[g][r] = 0.f;
       __builtin_amdgcn_s_setprio(1);
 #pragma unroll
-      for (int g = 0; g < 2; ++g)
+      for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks)
-          s[g] = mfma32(stg[(ks >> 1) * SUB + g * 128 + ((ks & 1) ? kf1 : kf0)], qf[ks], s[g]);
+        for (int g = 0; g < 2; ++g) s[g] = mfma32(kfr[g * KS + ks], qf[ks], s[g]);
       __builtin_amdgcn_s_setprio(0);
+      // V^T fragments of this tile, read while the softmax runs
+      const uint16_t* stg16 = (const uint16_t*)stg;
+      u32x4 vfr[DB * 4];
+#pragma unroll
+      for (int d = 0; d < DB; ++d)
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks) {
+          const int o = d * SUB * 8 + ks * 16 * 32;
+          const u32x2 lo = lds_tr16(stg16 + vt0 + o), hi = lds_tr16(stg16 + vt1 + o);
+          vfr[d * 4 + ks] = u32x4{lo[0], lo[1], hi[0], hi[1]};
+        }
+      __builtin_amdgcn_sched_barrier(0);
       if (pf) issue(n + NST - TPB);
 
       // ---- mask (only on edge / diagonal tiles)
@@ -225,15 +245,10 @@ __global__ __launch_bounds__(NT, 1) void attn_fwd_kernel(FwdArgs a) {
 
       // ---- O^T += V^T P^T
       __builtin_amdgcn_s_setprio(1);
-      const uint16_t* stg16 = (const uint16_t*)stg;
 #pragma unroll
-      for (int d = 0; d < DB; ++d)
+      for (int ks = 0; ks < 4; ++ks)
 #pragma unroll
-        for (int ks = 0; ks < 4; ++ks) {
-          const int o = d * SUB * 8 + ks * 16 * 32;
-          const u32x2 lo = lds_tr16(stg16 + vt0 + o), hi = lds_tr16(stg16 + vt1 + o);
-          oacc[d] = mfma32(u32x4{lo[0], lo[1], hi[0], hi[1]}, pb[ks], oacc[d]);
-        }
+        for (int d = 0; d < DB; ++d) oacc[d] = mfma32(vfr[d * 4 + ks], pb[ks], oacc[d]);
       __builtin_amdgcn_s_setprio(0);
     }
   }
