@@ -8,11 +8,18 @@ TEST INFRASTRUCTURE ONLY.  Nothing on the product path may import this.
   * ulysses_pack / ulysses_unpack: the send/receive layouts around the
     Ulysses all-to-all (Section 4: [bs, L/sp, hs, d] <-> [bs, L, hs/sp, d]),
     written as index maps over a head map (-1 = zero dummy head).
+  * ulysses_unpack_add: the backward of the GQA K/V pack.  The pack
+    replicates a KV head to every rank whose real query heads read it, so on
+    the way back the gradients the ranks return for one KV head are summed
+    (the adjoint of the replication).  A bfloat16 variant fixes the order and
+    precision the library uses: float32 sum in ascending slot order, one
+    rounding to bfloat16.
   * all_to_all: the collective itself, simulated as an index permutation.
   * lse_merge / ring_forward: Ring-Attention (Section 2.1, Table 1): the
     rank's Q chunk is run against each KV chunk and the partial results are
     combined through log-sum-exp.
-  * ulysses_simulate: every rank of a DHU layer, end to end.
+  * ulysses_simulate / ulysses_simulate_backward: every rank of a DHU
+    layer, end to end, forward and backward.
 """
 from __future__ import annotations
 
@@ -66,6 +73,45 @@ def ulysses_unpack(src: np.ndarray, head_map, H_dst: int) -> np.ndarray:
                 seen[g] += 1
     assert np.all(seen == 1), "unpack map must name every destination head once"
     return dst
+
+
+def ulysses_unpack_add(src: np.ndarray, head_map, H_dst: int) -> np.ndarray:
+    """Adjoint of ulysses_pack: dst[t, g, :] = sum of src[j, t, h, :] over the
+    slots j*H + h whose map entry is g, in ascending slot order; -1 slots are
+    dropped; a head named by no slot is zero.  src: [sp, T_loc, H, D] (float
+    values) -> dst: [T_loc, H_dst, D]."""
+    sp, T_loc, H_src_loc, D = src.shape
+    dst = np.zeros((T_loc, H_dst, D), dtype=np.float64)
+    for j in range(sp):
+        for h in range(H_src_loc):
+            g = int(head_map[j * H_src_loc + h])
+            if g >= 0:
+                dst[:, g, :] += src[j, :, h, :]
+    return dst
+
+
+def f32_to_bf16_bits(x) -> np.ndarray:
+    """float32 -> bfloat16 bit patterns, round to nearest, ties to even
+    (finite inputs): add 0x7fff plus the lowest kept bit, drop 16 bits."""
+    b = np.asarray(x, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    b = (b + 0x7FFF + ((b >> 16) & 1)) >> 16
+    return b.astype(np.uint16)
+
+
+def ulysses_unpack_add_bf16(src_bits: np.ndarray, head_map, H_dst: int) -> np.ndarray:
+    """ulysses_unpack_add on bfloat16 bit patterns as the library defines it:
+    each input decoded to float32 (exact), the sum formed in float32 one term
+    at a time in ascending slot order (rank j, then slot h), rounded once to
+    bfloat16 (nearest-even).  Returns uint16 bits [T_loc, H_dst, D]."""
+    sp, T_loc, H_src_loc, D = src_bits.shape
+    vals = (np.asarray(src_bits, dtype=np.uint16).astype(np.uint32) << 16).view(np.float32)
+    acc = np.zeros((T_loc, H_dst, D), dtype=np.float32)
+    for j in range(sp):
+        for h in range(H_src_loc):
+            g = int(head_map[j * H_src_loc + h])
+            if g >= 0:
+                acc[:, g, :] = acc[:, g, :] + vals[j, :, h, :]
+    return f32_to_bf16_bits(acc)
 
 
 def all_to_all(send):
@@ -125,6 +171,62 @@ def ring_backward(q, kv_chunks, do, o, lse, *, q_pos, kv_pos, H_loc, head_offset
     return dq, dks, dvs
 
 
+def _dhu_layout(hs, hs_new, hkv, sp, gqa_group):
+    """Head maps of one DHU layer, given the padded head count hs_new that
+    Listing 1's pad produced: Q map, K/V map, K/V slots per rank and each
+    rank's first KV head.  MHA pads K/V like Q; under GQA only Q is padded
+    and rank j receives the contiguous KV heads its real Q heads read."""
+    assert hs_new % sp == 0 and hs_new >= hs
+    hloc = hs_new // sp
+    qmap = np.array([h if h < hs else -1 for h in range(hs_new)])
+    if hkv == hs:
+        return qmap, qmap, hloc, [j * hloc for j in range(sp)], hloc, hs_new
+    rng = []
+    for j in range(sp):
+        real = [h for h in range(j * hloc, (j + 1) * hloc) if h < hs]
+        rng.append((real[0] // gqa_group, real[-1] // gqa_group + 1) if real else (0, 0))
+    kvw = max(1, max(b - a for a, b in rng))
+    kmap = np.full(sp * kvw, -1)
+    for j, (a, b) in enumerate(rng):
+        kmap[j * kvw: j * kvw + b - a] = np.arange(a, b)
+    return qmap, kmap, kvw, [a for a, _ in rng], hloc, hs_new
+
+
+def _dhu_scatter(q_full, k_full, v_full, sp, gqa_group, extra=()):
+    """Pad, split sequentially, pack and exchange: per rank the full-sequence
+    tensors over its heads ([L, H_loc, D] each), plus the layout."""
+    L, hs, D = q_full.shape
+    hkv = k_full.shape[1]
+    assert L % sp == 0
+    Tl = L // sp
+    qp = pad_heads(q_full[None], sp)[0]
+    qmap, kmap, kvw, kv_off, hloc, hs_new = _dhu_layout(hs, qp.shape[1], hkv, sp, gqa_group)
+    mha = hkv == hs
+    kp, vp = ((pad_heads(k_full[None], sp)[0], pad_heads(v_full[None], sp)[0]) if mha
+              else (k_full, v_full))
+    kv_pack_map = np.arange(hs_new) if mha else kmap
+
+    def exchange(x, width, m):
+        sends = [ulysses_pack(x[r * Tl:(r + 1) * Tl], sp, width, m) for r in range(sp)]
+        recv = all_to_all(sends)
+        # sequential split: source chunks in rank order are the whole sequence
+        return [np.concatenate(recv[j], axis=0) for j in range(sp)]
+
+    qs = exchange(qp, hloc, np.arange(hs_new))
+    ks = exchange(kp, kvw, kv_pack_map)
+    vs = exchange(vp, kvw, kv_pack_map)
+    xs = [exchange(pad_heads(x[None], sp)[0], hloc, np.arange(hs_new)) for x in extra]
+    return qs, ks, vs, xs, (qmap, kmap, kvw, kv_off, hloc, hs_new, Tl, mha)
+
+
+def _dhu_gather(per_rank, sp, Tl, hloc, hs_new, hs):
+    """Reverse exchange of [L, H_loc, D] per-rank results, unpack, unpad."""
+    back = all_to_all([list(np.split(per_rank[j], sp, axis=0)) for j in range(sp)])
+    return np.concatenate([
+        unpad_heads(ulysses_unpack(np.stack(back[r]), np.arange(hs_new), hs_new)[None], hs)[0]
+        for r in range(sp)], axis=0)
+
+
 def ulysses_simulate(q_full, k_full, v_full, sp, *, scale, cu, pos, gqa_group=1):
     """Every rank of one Dummy-Head Ulysses attention layer (batch 1).
 
@@ -136,46 +238,49 @@ def ulysses_simulate(q_full, k_full, v_full, sp, *, scale, cu, pos, gqa_group=1)
     [L, hs, D].  For GQA only Q is padded and rank j receives the KV heads
     its real Q heads read.  Returns (O [L, hs, D], per-rank LSE)."""
     L, hs, D = q_full.shape
-    hkv = k_full.shape[1]
-    assert L % sp == 0
-    Tl = L // sp
-    qp = pad_heads(q_full[None], sp)[0]
-    hs_new = qp.shape[1]
-    hloc = hs_new // sp
-    qmap = np.array([h if h < hs else -1 for h in range(hs_new)])
-    if hkv == hs:
-        kp, vp = pad_heads(k_full[None], sp)[0], pad_heads(v_full[None], sp)[0]
-        kmap, kvw = qmap, hloc
-        kv_off = [j * hloc for j in range(sp)]
-    else:
-        kp, vp = k_full, v_full
-        rng = []
-        for j in range(sp):
-            real = [h for h in range(j * hloc, (j + 1) * hloc) if h < hs]
-            rng.append((real[0] // gqa_group, real[-1] // gqa_group + 1) if real else (0, 0))
-        kvw = max(1, max(b - a for a, b in rng))
-        kmap = np.full(sp * kvw, -1)
-        for j, (a, b) in enumerate(rng):
-            kmap[j * kvw: j * kvw + b - a] = np.arange(a, b)
-        kv_off = [a for a, _ in rng]
-    # send side: each rank packs its token slice
-    sends_q = [ulysses_pack(qp[r * Tl:(r + 1) * Tl], sp, hloc, np.arange(hs_new)) for r in range(sp)]
-    sends_k = [ulysses_pack(kp[r * Tl:(r + 1) * Tl], sp, kvw, kmap if hkv != hs else np.arange(hs_new)) for r in range(sp)]
-    sends_v = [ulysses_pack(vp[r * Tl:(r + 1) * Tl], sp, kvw, kmap if hkv != hs else np.arange(hs_new)) for r in range(sp)]
-    rq, rk, rv = all_to_all(sends_q), all_to_all(sends_k), all_to_all(sends_v)
+    qs, ks, vs, _, lay = _dhu_scatter(q_full, k_full, v_full, sp, gqa_group)
+    qmap, kmap, kvw, kv_off, hloc, hs_new, Tl, mha = lay
     outs, lses = [], []
     for j in range(sp):
-        # sequential split: concatenating source chunks in rank order is [L, H, D]
-        qj = np.concatenate(rq[j], axis=0)
-        kj = np.concatenate(rk[j], axis=0)
-        vj = np.concatenate(rv[j], axis=0)
-        oj, lj = attn_forward(qj, kj, vj, cu_q=cu, cu_k=cu, pos_q=pos, pos_k=pos,
+        oj, lj = attn_forward(qs[j], ks[j], vs[j], cu_q=cu, cu_k=cu, pos_q=pos, pos_k=pos,
                               H_loc=hloc, head_offset=j * hloc, num_real_heads=hs,
                               gqa_group=gqa_group, kv_head_offset=kv_off[j], scale=scale)
-        outs.append(np.stack(np.split(oj, sp, axis=0)))  # [sp, Tl, hloc, D]
+        outs.append(oj)
         lses.append(lj)
-    back = all_to_all([[outs[j][r] for r in range(sp)] for j in range(sp)])
-    o = np.concatenate([
-        unpad_heads(ulysses_unpack(np.stack(back[r]), np.arange(hs_new), hs_new)[None], hs)[0]
-        for r in range(sp)], axis=0)
-    return o, lses
+    return _dhu_gather(outs, sp, Tl, hloc, hs_new, hs), lses
+
+
+def ulysses_simulate_backward(q_full, k_full, v_full, do_full, sp, *, scale, cu, pos,
+                              gqa_group=1):
+    """Gradients of one DHU layer over every rank (batch 1), for the loss
+    sum(dO * O).  dO reaches each rank through the same pad + all-to-all as Q
+    (its dummy heads are zero); each rank differentiates its own heads; dQ
+    goes back through the reverse all-to-all and unpad (the backward of the
+    pad drops the dummy heads).  K/V: for MHA the same as dQ; under GQA the
+    reverse all-to-all returns each rank's dK/dV of the KV heads it received
+    and ulysses_unpack_add sums the copies of a KV head that several ranks
+    held.  Returns dQ [L, hs, D], dK and dV [L, hkv, D]."""
+    L, hs, D = q_full.shape
+    hkv = k_full.shape[1]
+    qs, ks, vs, (dos,), lay = _dhu_scatter(q_full, k_full, v_full, sp, gqa_group, (do_full,))
+    qmap, kmap, kvw, kv_off, hloc, hs_new, Tl, mha = lay
+    dqs, dks, dvs = [], [], []
+    for j in range(sp):
+        a, b, c = attn_backward(qs[j], ks[j], vs[j], dos[j], cu_q=cu, cu_k=cu, pos_q=pos,
+                                pos_k=pos, H_loc=hloc, head_offset=j * hloc,
+                                num_real_heads=hs, gqa_group=gqa_group,
+                                kv_head_offset=kv_off[j], scale=scale)
+        dqs.append(a)
+        dks.append(b)
+        dvs.append(c)
+    dq = _dhu_gather(dqs, sp, Tl, hloc, hs_new, hs)
+    if mha:
+        return dq, _dhu_gather(dks, sp, Tl, hloc, hs_new, hs), _dhu_gather(dvs, sp, Tl, hloc,
+                                                                            hs_new, hs)
+
+    def kv_back(per_rank):
+        back = all_to_all([list(np.split(per_rank[j], sp, axis=0)) for j in range(sp)])
+        return np.concatenate([ulysses_unpack_add(np.stack(back[r]), kmap, hkv)
+                               for r in range(sp)], axis=0)
+
+    return dq, kv_back(dks), kv_back(dvs)

@@ -22,7 +22,7 @@ from __future__ import annotations
 import numpy as np
 import torch
 
-from workloads import padded_heads
+from workloads import padded_heads, ulysses_kv_head_map, ulysses_q_head_map
 
 
 def _kw(T, H, Hkv, cu=None, pos_q=None, pos_k=None, head_offset=0, num_real=None,
@@ -348,7 +348,72 @@ def pin_pack_unpack(S):
         assert back.dtype == bits.dtype and np.array_equal(back, bits)
 
 
+def pin_unpack_add_adjoint(S):
+    """The summing unpack is the adjoint of the pack (the pack replicates a
+    head into every slot that names it): <pack(x), y> = <x, unpack_add(y)>
+    for the GQA K/V maps and the MHA map with dummies; with a one-to-one map
+    it is the plain unpack."""
+    rng = np.random.default_rng(12)
+    cases = [(28, 4, 8), (40, 8, 16), (7, 1, 4), (6, 2, 4), (7, 7, 2)]
+    for hs, hkv, sp in cases:
+        hm = ulysses_kv_head_map(hs, hkv, sp) if hkv != hs else ulysses_q_head_map(hs, sp)
+        H = len(hm) // sp
+        T, D = 5, 3
+        x = _rand(rng, T, hkv, D)
+        y = _rand(rng, sp, T, H, D)
+        lhs = float(np.sum(S.ulysses_pack(x, sp, H, hm) * y))
+        rhs = float(np.sum(x * S.ulysses_unpack_add(y, hm, hkv)))
+        assert abs(lhs - rhs) <= 1e-12 * (1.0 + abs(lhs)), (hs, hkv, sp, lhs, rhs)
+    hm = ulysses_q_head_map(7, 2)
+    y = _rand(rng, 2, 4, 4, 3)
+    assert np.array_equal(S.ulysses_unpack_add(y, hm, 7), S.ulysses_unpack(y, hm, 7))
+
+
+def pin_unpack_add_bf16(S):
+    """bfloat16 summing unpack: float32 sum of the copies, one rounding to
+    bfloat16, nearest-even.  Closed-form cases (bit patterns): 1 + 2^-9 -> 1
+    (under half an ulp), 1 + 2^-8 -> 1 (tie, even), 1 + 2^-8 + 2^-8 -> 1 + 2^-7
+    (exact), (1 + 2^-7) + 2^-8 -> 1 + 2^-6 (tie, odd rounds up); random data
+    within half an ulp (plus float32 error) of the float64 sum."""
+    one, e9, e8, one7 = 0x3F80, 0x3B00, 0x3B80, 0x3F81
+    src = np.array([[one, one, one, one7], [e9, e8, e8, e8], [0, 0, e8, 0]],
+                   dtype=np.uint16).reshape(3, 1, 1, 4)
+    got = S.ulysses_unpack_add_bf16(src, np.array([0, 0, 0]), 1)
+    assert got.dtype == np.uint16
+    assert got.reshape(-1).tolist() == [0x3F80, 0x3F80, 0x3F81, 0x3F82], got
+    rng = np.random.default_rng(13)
+    hm = ulysses_kv_head_map(28, 4, 8)
+    bits = rng.integers(0x3C00, 0x4100, size=(8, 6, len(hm) // 8, 4)).astype(np.uint16)
+    bits |= (rng.integers(0, 2, size=bits.shape) << 15).astype(np.uint16)  # random signs
+    got = (S.ulysses_unpack_add_bf16(bits, hm, 4).astype(np.uint32) << 16).view(np.float32)
+    vals = (bits.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    ref = S.ulysses_unpack_add(vals, hm, 4)
+    assert np.all(np.abs(got - ref) <= np.abs(ref) * 2.0 ** -8 + 1e-6)
+
+
+def pin_ulysses_backward_equals_no_sp(A, S):
+    """DHU backward over all ranks (dO through the same pad + all-to-all, dQ
+    back through the reverse all-to-all and unpad, replicated GQA K/V
+    gradients summed by the unpack) equals the backward without SP."""
+    rng = np.random.default_rng(14)
+    for L, hs, hkv, sp, D in ((16, 7, 7, 2, 4), (24, 7, 1, 4, 3), (16, 6, 2, 4, 4),
+                              (16, 28, 4, 8, 2)):
+        q, k, v = _rand(rng, L, hs, D), _rand(rng, L, hkv, D), _rand(rng, L, hkv, D)
+        do = _rand(rng, L, hs, D)
+        cu = np.array([0, L // 2 + 1, L])
+        pos = np.concatenate([np.arange(L // 2 + 1), np.arange(L - L // 2 - 1)])
+        g = hs // hkv
+        dq, dk, dv = S.ulysses_simulate_backward(q, k, v, do, sp, scale=0.5, cu=cu, pos=pos,
+                                                 gqa_group=g)
+        rq, rk, rv = A.attn_backward(q, k, v, do, cu_q=cu, cu_k=cu, pos_q=pos, pos_k=pos,
+                                     H_loc=hs, head_offset=0, num_real_heads=hs, gqa_group=g,
+                                     kv_head_offset=0, scale=0.5)
+        for a, b in ((dq, rq), (dk, rk), (dv, rv)):
+            assert a.shape == b.shape and np.allclose(a, b, atol=1e-12), (L, hs, hkv, sp)
+
+
 ATTN_PINS = [pin_single_visible_key, pin_zero_query_uniform, pin_torch_sdpa,
              pin_finite_differences, pin_gradient_sums, pin_packed_equals_separate]
-SP_PINS = [pin_merge_identity, pin_pack_unpack]
-BOTH_PINS = [pin_ring_fold, pin_zigzag_fold, pin_ulysses_equals_no_sp]
+SP_PINS = [pin_merge_identity, pin_pack_unpack, pin_unpack_add_adjoint, pin_unpack_add_bf16]
+BOTH_PINS = [pin_ring_fold, pin_zigzag_fold, pin_ulysses_equals_no_sp,
+             pin_ulysses_backward_equals_no_sp]

@@ -96,6 +96,10 @@ MUTANTS = [
      "pad = np.zeros(x.shape[:2] + (sp - rem + 1,) + x.shape[3:], dtype=x.dtype)"),
     ("sp", "dst[j, :, h, :] = src[:, g, :]", "dst[j, :, h, :] = src[:, (g + 1) % src.shape[1], :]"),
     ("sp", "return np.concatenate([x, pad], axis=2)", "return np.concatenate([pad, x], axis=2)"),
+    ("sp", "dst[:, g, :] += src[j, :, h, :]", "dst[:, g, :] = src[j, :, h, :]"),
+    ("sp", "acc[:, g, :] = acc[:, g, :] + vals[j, :, h, :]", "acc[:, g, :] = vals[j, :, h, :]"),
+    ("sp", "b = (b + 0x7FFF + ((b >> 16) & 1)) >> 16", "b = (b + 0x8000) >> 16"),
+    ("sp", "dst[:, g, :] += src[j, :, h, :]", "dst[:, g, :] += src[j, :, h, :] / max(1, sp - 1)"),
 ]
 
 
