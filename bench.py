@@ -8,7 +8,9 @@ bf16 dense MFMA peak (2.5 PFLOP/s).
 A step is one pass of the rank's hot path over one batch of synthetic input
 already resident in HBM:
   Ulysses shard: pack Q, K, V (dummy-head zero fill) -> attention forward ->
-      unpack O -> pack dO -> attention backward -> unpack dQ (MHA: dK, dV too)
+      unpack O -> pack dO -> attention backward -> unpack dQ (MHA: dK, dV too;
+      GQA: summing unpack of the dK, dV copies received from the ranks that
+      share each KV head)
   packed varlen shard: attention forward -> backward
   ring rank r: r+1 fused ring steps (LSE merge in the epilogue, bf16 O on the
       last) -> per-chunk backward into an fp32 dQ accumulator -> dQ to bf16
@@ -88,7 +90,7 @@ class KernelTimers:
 
 
 KNAMES = {1: "attn_fwd_kernel", 2: "attn_dq_kernel", 3: "attn_dkdv_kernel", 4: "pack_kernel",
-          5: "unpack_kernel", 6: "merge_kernel"}
+          5: "unpack_kernel", 6: "merge_kernel", 7: "unpack_add_kernel"}
 
 
 def lib_desc(sp, sh, pos_k=None):
@@ -184,9 +186,14 @@ class Step:
                 self.send_v = torch.empty_like(self.send_k)
                 self.o_pre = torch.empty((Tl, sh.hs, D), dtype=torch.bfloat16, device=dev)
                 self.dq_pre = torch.empty_like(self.o_pre)
-                if self.mha:
-                    self.dk_pre = torch.empty((Tl, sh.hkv, D), dtype=torch.bfloat16, device=dev)
-                    self.dv_pre = torch.empty_like(self.dk_pre)
+                self.dk_pre = torch.empty((Tl, sh.hkv, D), dtype=torch.bfloat16, device=dev)
+                self.dv_pre = torch.empty_like(self.dk_pre)
+                if not self.mha:
+                    # reverse all-to-all receive buffers of dK / dV: chunk j is
+                    # what rank j returns for the KV heads it was sent (the
+                    # other ranks' gradients are synthetic here: one GPU)
+                    self.recv_dk = to_dev(torch, randn_bf16_bits((sh.sp, Tl, self.kw, D), sb + 4))
+                    self.recv_dv = to_dev(torch, randn_bf16_bits((sh.sp, Tl, self.kw, D), sb + 5))
         H = nr * D
         self.flops_fwd = [4.0 * H * p for p in self.pairs]
         self.flops_dq = [6.0 * H * p for p in self.pairs]
@@ -243,6 +250,10 @@ class Step:
                                      sh.hkv, dst=self.dk_pre)
                 sp.sp_ulysses_unpack(self.dv.view(sh.sp, self.Tl, sh.H_loc, sh.D), self.qmap,
                                      sh.hkv, dst=self.dv_pre)
+            else:
+                t.arm(sp.SP_KERNEL_UNPACK_ADD, 0.0)
+                sp.sp_ulysses_unpack_add(self.recv_dk, self.kmap, sh.hkv, dst=self.dk_pre)
+                sp.sp_ulysses_unpack_add(self.recv_dv, self.kmap, sh.hkv, dst=self.dv_pre)
 
 
 def cpu_baseline(sh, budget_s=15.0):
@@ -351,7 +362,8 @@ def copy_calibration(torch, nbytes=1 << 30):
 
 def bandwidth(sp, torch, reps=24):
     """GB/s of the bandwidth kernels at the workloads' shapes: the Ulysses
-    pack/unpack of the 7B-like (c1) and long (c4) shards and the fp32 LSE
+    pack/unpack and the summing K/V-gradient unpack of the 7B-like (c1) and
+    long (c4) shards and the fp32 LSE
     merge of the ring shard (c3).  Buffer sets rotate (>= 4 sets, > 1 GB in
     total) so that the 256 MB last-level cache cannot serve repeats; each
     call is timed with HIP events, the median is reported."""
@@ -399,6 +411,19 @@ def bandwidth(sp, torch, reps=24):
 
         run(f"unpack {name} [{spn},{Tl},{Hl},{D}] -> [{Tl},{hs},{D}]", 2 * rd, mk_unpack,
             lambda b, hs=hs, hmap=hmap: sp.sp_ulysses_unpack(b[0], hmap, hs, dst=b[1]))
+
+        # summing unpack of the dK (or dV) copies the ranks return (GQA)
+        kmap = ulysses_kv_head_map(hs, sh.hkv, spn)
+        kw_ = len(kmap) // spn
+        ua_bytes = (int(np.sum(kmap >= 0)) * Tl + Tl * sh.hkv) * el  # named slots read
+
+        def mk_unpack_add(Tl=Tl, spn=spn, kw_=kw_, D=D, hkv=sh.hkv):
+            src = torch.empty((spn, Tl, kw_, D), dtype=torch.bfloat16, device="cuda").normal_()
+            return src, torch.empty((Tl, hkv, D), dtype=torch.bfloat16, device="cuda")
+
+        run(f"unpack_add {name} [{spn},{Tl},{kw_},{D}] -> [{Tl},{sh.hkv},{D}]", ua_bytes,
+            mk_unpack_add, lambda b, kmap=kmap, hkv=sh.hkv: sp.sp_ulysses_unpack_add(
+                b[0], kmap, hkv, dst=b[1]))
 
     sh = workload("ring_L131072_8chunks_r4_q28kv4_d128")
     T, H, D = sh.chunk, sh.H_loc, sh.D

@@ -163,6 +163,29 @@ sp_status sp_ulysses_unpack(const void* src, int32_t T_loc, int32_t H_src_loc, i
                             int32_t sp, const int32_t* head_map, int32_t H_dst, void* dst,
                             void* stream);
 
+/*
+ * Summing unpack of GQA K/V gradients after the reverse all-to-all (the
+ * backward of the K/V pack, Section 4.1 / Listing 1 with GQA: the pack sends
+ * one KV head to every rank whose real query heads read it, so the gradients
+ * those ranks return for it are added):
+ *
+ *   dst[t, g, :] = sum over slots s = j*H_src_loc + h with head_map[s] == g,
+ *                  in ascending s (source rank j, then slot h), of src[j, t, h, :]
+ *
+ * src: [sp, T_loc, H_src_loc, D] bf16 (the receive buffer: chunk j came from
+ * rank j); dst: [T_loc, H_dst, D] bf16; head_map: HOST, the same map the
+ * forward pack used (-1 slots are dropped).  Each sum is formed in float32,
+ * one slot at a time in that order, and rounded once to bf16 (nearest-even),
+ * so the result is deterministic bit for bit.  A head named by no slot is
+ * written as +0.  Limits: sp*H_src_loc <= 512, H_dst <= 256
+ * (SP_ERR_UNSUPPORTED); map entries outside [-1, H_dst) are
+ * SP_ERR_INVALID_ARG.  T_loc == 0 is a no-op.  Reads sp*T_loc*H_src_loc*D*2
+ * bytes and writes T_loc*H_dst*D*2.
+ */
+sp_status sp_ulysses_unpack_add(const void* src, int32_t T_loc, int32_t H_src_loc,
+                                int32_t head_dim, int32_t sp, const int32_t* head_map,
+                                int32_t H_dst, void* dst, void* stream);
+
 /* Workspace bytes needed by `op` (SP_OP_FWD, SP_OP_BWD, SP_OP_RING_STEP) for
  * this problem.  Validates the descriptor. */
 sp_status sp_attn_workspace_size(const sp_attn_desc* desc, int32_t op, size_t* bytes);
@@ -267,7 +290,8 @@ enum {
   SP_KERNEL_ATTN_DKDV = 3,/* backward dK/dV kernel (S, P, dV, dP, dS, dK) */
   SP_KERNEL_PACK = 4,     /* Ulysses pack                                */
   SP_KERNEL_UNPACK = 5,   /* Ulysses unpack                              */
-  SP_KERNEL_LSE_MERGE = 6 /* standalone LSE merge                        */
+  SP_KERNEL_LSE_MERGE = 6,/* standalone LSE merge                        */
+  SP_KERNEL_UNPACK_ADD = 7/* summing unpack of GQA K/V gradients         */
 };
 sp_status sp_profile_events(int32_t kernel_id, void* start_event, void* stop_event);
 

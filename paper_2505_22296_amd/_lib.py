@@ -65,6 +65,7 @@ def load() -> ctypes.CDLL:
         "sp_version": (i32, []),
         "sp_ulysses_pack": (i32, [vp, i32, i32, i32, i32, i32, _i32p, vp, vp]),
         "sp_ulysses_unpack": (i32, [vp, i32, i32, i32, i32, _i32p, i32, vp, vp]),
+        "sp_ulysses_unpack_add": (i32, [vp, i32, i32, i32, i32, _i32p, i32, vp, vp]),
         "sp_attn_workspace_size": (i32, [D, i32, ctypes.POINTER(sz)]),
         "sp_attn_fwd": (i32, [D, vp, vp, vp, vp, vp, vp, sz, vp]),
         "sp_attn_bwd": (i32, [D, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
@@ -83,11 +84,12 @@ def load() -> ctypes.CDLL:
 
 
 EXPORTED = ["sp_status_string", "sp_version", "sp_ulysses_pack", "sp_ulysses_unpack",
+            "sp_ulysses_unpack_add",
             "sp_attn_workspace_size", "sp_attn_fwd", "sp_attn_bwd", "sp_ring_step",
             "sp_lse_merge", "sp_f32_to_bf16", "sp_attn_schedule", "sp_profile_events"]
 
 SP_KERNEL_ATTN_FWD, SP_KERNEL_ATTN_DQ, SP_KERNEL_ATTN_DKDV = 1, 2, 3
-SP_KERNEL_PACK, SP_KERNEL_UNPACK, SP_KERNEL_LSE_MERGE = 4, 5, 6
+SP_KERNEL_PACK, SP_KERNEL_UNPACK, SP_KERNEL_LSE_MERGE, SP_KERNEL_UNPACK_ADD = 4, 5, 6, 7
 
 
 def status_string(s: int) -> str:
@@ -187,6 +189,20 @@ def sp_ulysses_unpack(src, head_map: Sequence[int], H_dst: int, dst=None, stream
     m = np.ascontiguousarray(np.asarray(head_map, dtype=np.int32))
     _check(load().sp_ulysses_unpack(_ptr(src), T, Hs, D, sp, m.ctypes.data_as(_i32p), H_dst,
                                     _ptr(dst), _stream(stream)), "sp_ulysses_unpack")
+    return dst
+
+
+def sp_ulysses_unpack_add(src, head_map: Sequence[int], H_dst: int, dst=None, stream=None):
+    """src [sp, T_loc, H_src_loc, D] bf16 -> dst [T_loc, H_dst, D] bf16: the
+    copies of a head that several slots name are summed (float32, ascending
+    slot order, one rounding to bf16)."""
+    import torch
+    sp, T, Hs, D = src.shape
+    if dst is None:
+        dst = torch.empty((T, H_dst, D), dtype=src.dtype, device=src.device)
+    m = np.ascontiguousarray(np.asarray(head_map, dtype=np.int32))
+    _check(load().sp_ulysses_unpack_add(_ptr(src), T, Hs, D, sp, m.ctypes.data_as(_i32p), H_dst,
+                                        _ptr(dst), _stream(stream)), "sp_ulysses_unpack_add")
     return dst
 
 

@@ -398,6 +398,35 @@ sp_status sp_ulysses_unpack(const void* src, int32_t T_loc, int32_t H_src_loc, i
   return SP_OK;
 }
 
+sp_status sp_ulysses_unpack_add(const void* src, int32_t T_loc, int32_t H_src_loc,
+                                int32_t head_dim, int32_t sp, const int32_t* head_map,
+                                int32_t H_dst, void* dst, void* stream) {
+  if (T_loc < 0 || H_src_loc < 1 || head_dim < 8 || head_dim % 8 != 0 || sp < 1 || H_dst < 1 ||
+      !head_map)
+    return SP_ERR_INVALID_ARG;
+  if ((int64_t)sp * H_src_loc > spk::kMaxMap || H_dst > spk::kMaxAddDst) return SP_ERR_UNSUPPORTED;
+  spk::PackAddArgs a;
+  a.sp = sp; a.T = T_loc; a.Hs = H_src_loc; a.Hd = H_dst; a.nch = head_dim / 8;
+  // counting sort of the slots by destination head keeps each head's slots
+  // in ascending order
+  std::vector<int> cnt(H_dst + 1, 0);
+  const int n_slots = sp * H_src_loc;
+  for (int i = 0; i < n_slots; ++i) {
+    const int g = head_map[i];
+    if (g < -1 || g >= H_dst) return SP_ERR_INVALID_ARG;
+    if (g >= 0) ++cnt[g + 1];
+  }
+  for (int g = 0; g < H_dst; ++g) cnt[g + 1] += cnt[g];
+  for (int g = 0; g <= H_dst; ++g) a.start[g] = (int16_t)cnt[g];
+  std::vector<int> fill(cnt.begin(), cnt.end() - 1);
+  for (int i = 0; i < n_slots; ++i)
+    if (head_map[i] >= 0) a.slot[fill[head_map[i]]++] = (int16_t)i;
+  if (T_loc == 0) return SP_OK;
+  if (!src || !dst || !aligned16(src) || !aligned16(dst)) return SP_ERR_INVALID_ARG;
+  SP_HIP(spk::launch_unpack_add(src, dst, a, (hipStream_t)stream));
+  return SP_OK;
+}
+
 sp_status sp_attn_workspace_size(const sp_attn_desc* desc, int32_t op, size_t* bytes) {
   if (!bytes) return SP_ERR_INVALID_ARG;
   if (op != SP_OP_FWD && op != SP_OP_BWD && op != SP_OP_RING_STEP) return SP_ERR_INVALID_ARG;

@@ -1,6 +1,7 @@
 // HBM-bound kernels of the SP attention library (gfx950):
 //   * Ulysses pack / unpack with dummy-head zero fill (Listing 1 pad/unpad
-//     around the all-to-all layout of Section 4),
+//     around the all-to-all layout of Section 4), and the summing unpack of
+//     GQA K/V gradients replicated to several ranks,
 //   * the log-sum-exp merge of two partial attention results (ring combine,
 //     Section 2.1),
 //   * fills, bf16 casts, the backward's row dot D_i = dO_i . O_i, and the
@@ -57,11 +58,59 @@ __global__ __launch_bounds__(kBlock) void unpack_kernel(const u32x4* __restrict_
   }
 }
 
+// dst[t, g, c] = sum over the slots s = j*Hs + h listed for g (ascending) of
+// src[j, t, h, c]: eight bf16 per 16-byte chunk, summed in float32 one slot
+// at a time, rounded once to bf16 (nearest-even); no slot gives +0.
+__global__ __launch_bounds__(kBlock) void unpack_add_kernel(const u32x4* __restrict__ src,
+                                                            u32x4* __restrict__ dst,
+                                                            PackAddArgs a) {
+  const int64_t n = (int64_t)a.T * a.Hd * a.nch;
+  for (int64_t e = (int64_t)blockIdx.x * kBlock + threadIdx.x; e < n;
+       e += (int64_t)gridDim.x * kBlock) {
+    const int c = (int)(e % a.nch);
+    const int64_t r = e / a.nch;
+    const int g = (int)(r % a.Hd);
+    const int t = (int)(r / a.Hd);
+    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    auto load = [&](int i) {
+      const int s = a.slot[i];
+      const int j = s / a.Hs, h = s % a.Hs;
+      return src[(((int64_t)j * a.T + t) * a.Hs + h) * a.nch + c];
+    };
+    auto add = [&](const u32x4& v) {
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        acc[2 * k] += __uint_as_float(v[k] << 16);
+        acc[2 * k + 1] += __uint_as_float(v[k] & 0xffff0000u);
+      }
+    };
+    // the first four copies are loaded together (a KV head rarely has more),
+    // then added in slot order
+    const int i0 = a.start[g], i1 = a.start[g + 1];
+    u32x4 v[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+      if (i0 + k < i1) v[k] = load(i0 + k);
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+      if (i0 + k < i1) add(v[k]);
+    for (int i = i0 + 4; i < i1; ++i) add(load(i));
+    dst[e] = pack_bf16x8(acc[0], acc[1], acc[2], acc[3], acc[4], acc[5], acc[6], acc[7]);
+  }
+}
+
 hipError_t launch_pack(const void* src, void* dst, const PackArgs& a, hipStream_t st) {
   int64_t n = (int64_t)a.sp * a.T * a.Hd * a.nch;
   if (n == 0) return hipSuccess;
   return sp_launch(kKPack, pack_kernel, dim3(grid_for(n)), dim3(kBlock), st, (const u32x4*)src,
                    (u32x4*)dst, a);
+}
+
+hipError_t launch_unpack_add(const void* src, void* dst, const PackAddArgs& a, hipStream_t st) {
+  int64_t n = (int64_t)a.T * a.Hd * a.nch;
+  if (n == 0) return hipSuccess;
+  return sp_launch(kKUnpackAdd, unpack_add_kernel, dim3(grid_for(n)), dim3(kBlock), st,
+                   (const u32x4*)src, (u32x4*)dst, a);
 }
 
 hipError_t launch_unpack(const void* src, void* dst, const PackArgs& a, hipStream_t st) {

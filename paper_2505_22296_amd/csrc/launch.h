@@ -7,7 +7,10 @@ namespace spk {
 
 // Kernel identifiers of the opt-in per-thread launch timer (values match the
 // SP_KERNEL_* constants of the public header).
-enum KernelId { kKFwd = 1, kKDq = 2, kKDkdv = 3, kKPack = 4, kKUnpack = 5, kKMerge = 6, kKCount = 7 };
+enum KernelId {
+  kKFwd = 1, kKDq = 2, kKDkdv = 3, kKPack = 4, kKUnpack = 5, kKMerge = 6, kKUnpackAdd = 7,
+  kKCount = 8
+};
 
 struct KernelTimer {
   hipEvent_t start = nullptr, stop = nullptr;
@@ -42,6 +45,16 @@ static constexpr int kMaxKv = 64;
 struct PackArgs {
   int sp, T, Hs, Hd, nch;  // nch = 16-byte chunks per head row (D / 8)
   int map[kMaxMap];        // pack: slot -> source head; unpack: dest head -> j*Hs + h
+};
+
+// Summing unpack: destination head g sums source slots slot[start[g]] ..
+// slot[start[g+1]-1] (each j*Hs + h, ascending).  int16 keeps the arguments
+// small (slots < kMaxMap, heads <= kMaxAddDst).
+static constexpr int kMaxAddDst = 256;
+struct PackAddArgs {
+  int sp, T, Hs, Hd, nch;
+  int16_t start[kMaxAddDst + 1];
+  int16_t slot[kMaxMap];
 };
 
 struct ReduceArgs {
@@ -104,6 +117,7 @@ struct DkdvArgs {
 
 hipError_t launch_pack(const void* src, void* dst, const PackArgs& a, hipStream_t st);
 hipError_t launch_unpack(const void* src, void* dst, const PackArgs& a, hipStream_t st);
+hipError_t launch_unpack_add(const void* src, void* dst, const PackAddArgs& a, hipStream_t st);
 hipError_t launch_merge(float* o_acc, float* lse_acc, const void* o_part, bool part_bf16,
                         const float* lse_part, int T, int H, int D, void* o_out, hipStream_t st);
 hipError_t launch_zero_heads_bf16(void* x, int T, int H, int D, int h0, int h1, hipStream_t st);

@@ -119,6 +119,19 @@ def test_pack_unpack_validation():
     assert lib.sp_ulysses_unpack(fake, 8, 2, 64, 2, p, 3, fake, None) == sp.SP_ERR_INVALID_ARG
     a, p = m(0, 1, 2, -1)
     assert lib.sp_ulysses_unpack(fake, 0, 2, 64, 2, p, 3, fake, None) == sp.SP_OK
+    # summing unpack: repeated destinations are fine, out-of-range ones are not
+    a, p = m(0, 0, 1, -1)
+    assert lib.sp_ulysses_unpack_add(fake, 0, 2, 64, 2, p, 2, fake, None) == sp.SP_OK
+    a, p = m(0, 0, 2, -1)
+    assert lib.sp_ulysses_unpack_add(fake, 8, 2, 64, 2, p, 2, fake, None) == sp.SP_ERR_INVALID_ARG
+    a, p = m(0, 0, 1, -2)
+    assert lib.sp_ulysses_unpack_add(fake, 8, 2, 64, 2, p, 2, fake, None) == sp.SP_ERR_INVALID_ARG
+    a, p = m(0, 0, 1, -1)
+    assert lib.sp_ulysses_unpack_add(fake + 2, 8, 2, 64, 2, p, 2, fake, None) == sp.SP_ERR_INVALID_ARG
+    assert lib.sp_ulysses_unpack_add(fake, 8, 2, 60, 2, p, 2, fake, None) == sp.SP_ERR_INVALID_ARG
+    assert lib.sp_ulysses_unpack_add(fake, 8, 2, 64, 2, p, 257, fake, None) == sp.SP_ERR_UNSUPPORTED
+    big, pb = m(*([0] * 514))
+    assert lib.sp_ulysses_unpack_add(fake, 8, 257, 64, 2, pb, 2, fake, None) == sp.SP_ERR_UNSUPPORTED
 
 
 # ------------------------------------------------------------- scheduler

@@ -55,6 +55,32 @@ def test_pack_gqa_kv_map_bit_exact(sp):
     assert np.array_equal(got, oracle.ulysses_pack(bits, 8, w, hm))
 
 
+@pytest.mark.parametrize("T,hs,hkv,sp_size,D", [(4096, 28, 4, 8, 128), (1000, 40, 8, 16, 128),
+                                                (333, 7, 1, 4, 64), (3, 6, 2, 4, 128),
+                                                (77, 7, 7, 2, 64)])
+def test_unpack_add_bit_exact(sp, T, hs, hkv, sp_size, D):
+    """Summing unpack of replicated K/V gradients: bit-exact against the
+    oracle's float32 ordered sum + one RNE rounding (GQA maps, where KV heads
+    appear in up to three slots, and the one-copy MHA map)."""
+    print(f"unpack_add T={T} hs={hs} hkv={hkv} sp={sp_size} D={D}", flush=True)
+    hm = (ulysses_kv_head_map(hs, hkv, sp_size) if hkv != hs else ulysses_q_head_map(hs, sp_size))
+    w = len(hm) // sp_size
+    rng = np.random.default_rng(T + hs + D)
+    bits = randn_bf16_bits((sp_size, T, w, D), seed=T + 7 * hs)
+    got = bits_from_dev(sp.sp_ulysses_unpack_add(to_dev(bits), hm, hkv))
+    ref = oracle.ulysses_unpack_add_bf16(bits, hm, hkv)
+    assert got.shape == ref.shape and np.array_equal(got, ref)
+    if hkv == hs:  # one copy per head: the plain unpack
+        assert np.array_equal(got, oracle.ulysses_unpack(bits, hm, hkv))
+    # a head no slot names comes out +0; cancelling copies give +0 too
+    hm2 = np.array([0, -1, 0, 2], dtype=np.int32)
+    b2 = rng.integers(0x0080, 0x7F00, size=(2, T, 2, D)).astype(np.uint16)  # normal
+    b2[1, :, 0] = b2[0, :, 0] ^ 0x8000  # x + (-x)
+    got2 = bits_from_dev(sp.sp_ulysses_unpack_add(to_dev(b2), hm2, 3))
+    assert np.array_equal(got2, oracle.ulysses_unpack_add_bf16(b2, hm2, 3))
+    assert np.all(got2[:, 1] == 0) and np.all(got2[:, 0] == 0)
+
+
 # ------------------------------------------------------------------ merge
 @pytest.mark.parametrize("part_bf16", [False, True])
 def test_lse_merge(sp, part_bf16):
