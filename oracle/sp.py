@@ -20,6 +20,8 @@ TEST INFRASTRUCTURE ONLY.  Nothing on the product path may import this.
     combined through log-sum-exp.
   * ulysses_simulate / ulysses_simulate_backward: every rank of a DHU
     layer, end to end, forward and backward.
+  * usp_simulate: USP (the paper's 2-D comparison method, Table 1): Ulysses
+    inside groups of sp_hp ranks, zigzag Ring-Attention across sp_cp groups.
 """
 from __future__ import annotations
 
@@ -284,3 +286,67 @@ def ulysses_simulate_backward(q_full, k_full, v_full, do_full, sp, *, scale, cu,
                                for r in range(sp)], axis=0)
 
     return dq, kv_back(dks), kv_back(dvs)
+
+
+def usp_simulate(q_full, k_full, v_full, do_full, sp_hp, sp_cp, *, scale, gqa_group=1):
+    """Every rank of a USP attention layer (batch 1, one causal sequence).
+
+    Ranks form sp_cp ring groups of sp_hp Ulysses ranks.  The sequence is cut
+    into 2*sp_cp chunks; ring rank r holds chunks r and 2*sp_cp-1-r (zigzag),
+    split sequentially over its sp_hp Ulysses ranks.  Inside a ring group the
+    DHU all-to-all gives Ulysses rank j the group's whole share over heads
+    j*H_loc..; across groups, rank (r, j) runs the zigzag ring over the
+    shares of ranks (r - s mod sp_cp, j), s = 0..sp_cp-1, merging partials
+    by log-sum-exp; the backward uses the merged O / LSE, and each step's dK,
+    dV are summed at the rank that owns those keys before the reverse
+    all-to-all (summing unpack under GQA).  Returns O, dQ [L, hs, D], dK, dV
+    [L, hkv, D] and the per-rank results {(r, j): dict(q_pos, o, lse, dq,
+    kv_pos, dk, dv)} (dk / dv per ring step)."""
+    L, hs, D = q_full.shape
+    hkv = k_full.shape[1]
+    n_ch = 2 * sp_cp
+    assert L % n_ch == 0
+    C = L // n_ch
+    share = [np.concatenate([r * C + np.arange(C), (n_ch - 1 - r) * C + np.arange(C)])
+             for r in range(sp_cp)]
+    groups = [_dhu_scatter(q_full[share[r]], k_full[share[r]], v_full[share[r]], sp_hp, gqa_group,
+                           (do_full[share[r]],)) for r in range(sp_cp)]
+    qmap, kmap, kvw, kv_off, hloc, hs_new, Tl, mha = groups[0][4]
+    per_rank = {}
+    o_g = [[None] * sp_hp for _ in range(sp_cp)]
+    dq_g = [[None] * sp_hp for _ in range(sp_cp)]
+    dk_g = [[np.zeros_like(groups[r][1][j]) for j in range(sp_hp)] for r in range(sp_cp)]
+    dv_g = [[np.zeros_like(groups[r][2][j]) for j in range(sp_hp)] for r in range(sp_cp)]
+    for r in range(sp_cp):
+        for j in range(sp_hp):
+            steps = [(r - s) % sp_cp for s in range(sp_cp)]
+            chunks = [(groups[r2][1][j], groups[r2][2][j]) for r2 in steps]
+            kv_pos = [share[r2] for r2 in steps]
+            kw = dict(q_pos=share[r], kv_pos=kv_pos, H_loc=hloc, head_offset=j * hloc,
+                      num_real_heads=hs, gqa_group=gqa_group, kv_head_offset=kv_off[j],
+                      scale=scale)
+            q, do = groups[r][0][j], groups[r][3][0][j]
+            o, lse = ring_forward(q, chunks, **kw)
+            dq, dks, dvs = ring_backward(q, chunks, do, o, lse, **kw)
+            for r2, a, b in zip(steps, dks, dvs):
+                dk_g[r2][j] += a
+                dv_g[r2][j] += b
+            o_g[r][j], dq_g[r][j] = o, dq
+            per_rank[(r, j)] = dict(q_pos=share[r], o=o, lse=lse, dq=dq, kv_pos=kv_pos,
+                                    dk=dks, dv=dvs)
+
+    def kv_back(per_j):
+        if mha:
+            return _dhu_gather(per_j, sp_hp, Tl, hloc, hs_new, hs)
+        back = all_to_all([list(np.split(per_j[j], sp_hp, axis=0)) for j in range(sp_hp)])
+        return np.concatenate([ulysses_unpack_add(np.stack(back[i]), kmap, hkv)
+                               for i in range(sp_hp)], axis=0)
+
+    O, dQ = np.zeros_like(q_full), np.zeros_like(q_full)
+    dK, dV = np.zeros_like(k_full), np.zeros_like(v_full)
+    for r in range(sp_cp):
+        O[share[r]] = _dhu_gather(o_g[r], sp_hp, Tl, hloc, hs_new, hs)
+        dQ[share[r]] = _dhu_gather(dq_g[r], sp_hp, Tl, hloc, hs_new, hs)
+        dK[share[r]] = kv_back(dk_g[r])
+        dV[share[r]] = kv_back(dv_g[r])
+    return O, dQ, dK, dV, per_rank

@@ -412,8 +412,29 @@ def pin_ulysses_backward_equals_no_sp(A, S):
             assert a.shape == b.shape and np.allclose(a, b, atol=1e-12), (L, hs, hkv, sp)
 
 
+def pin_usp_equals_no_sp(A, S):
+    """USP over every rank of an sp_hp x sp_cp mesh (Ulysses inside ring
+    groups, zigzag ring across them, Table 1) equals attention without SP,
+    forward and backward: MHA with dummy heads, GQA with replicated KV heads
+    and a one-KV-head-per-rank GQA layout."""
+    rng = np.random.default_rng(15)
+    for L, hs, hkv, hp, cp, D in ((24, 7, 7, 2, 2, 3), (36, 6, 2, 2, 3, 4), (32, 8, 4, 4, 2, 2)):
+        q, k, v = _rand(rng, L, hs, D), _rand(rng, L, hkv, D), _rand(rng, L, hkv, D)
+        do = _rand(rng, L, hs, D)
+        g = hs // hkv
+        O, dQ, dK, dV, per = S.usp_simulate(q, k, v, do, hp, cp, scale=0.45, gqa_group=g)
+        full = dict(cu_q=np.array([0, L]), cu_k=np.array([0, L]), pos_q=np.arange(L),
+                    pos_k=np.arange(L), H_loc=hs, head_offset=0, num_real_heads=hs,
+                    gqa_group=g, kv_head_offset=0, scale=0.45)
+        Om, _ = A.attn_forward(q, k, v, **full)
+        rq, rk, rv = A.attn_backward(q, k, v, do, **full)
+        for a, b in ((O, Om), (dQ, rq), (dK, rk), (dV, rv)):
+            assert np.allclose(a, b, atol=1e-12), (L, hs, hkv, hp, cp)
+        assert len(per) == hp * cp
+
+
 ATTN_PINS = [pin_single_visible_key, pin_zero_query_uniform, pin_torch_sdpa,
              pin_finite_differences, pin_gradient_sums, pin_packed_equals_separate]
 SP_PINS = [pin_merge_identity, pin_pack_unpack, pin_unpack_add_adjoint, pin_unpack_add_bf16]
 BOTH_PINS = [pin_ring_fold, pin_zigzag_fold, pin_ulysses_equals_no_sp,
-             pin_ulysses_backward_equals_no_sp]
+             pin_ulysses_backward_equals_no_sp, pin_usp_equals_no_sp]

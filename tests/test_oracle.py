@@ -100,6 +100,9 @@ MUTANTS = [
     ("sp", "acc[:, g, :] = acc[:, g, :] + vals[j, :, h, :]", "acc[:, g, :] = vals[j, :, h, :]"),
     ("sp", "b = (b + 0x7FFF + ((b >> 16) & 1)) >> 16", "b = (b + 0x8000) >> 16"),
     ("sp", "dst[:, g, :] += src[j, :, h, :]", "dst[:, g, :] += src[j, :, h, :] / max(1, sp - 1)"),
+    ("sp", "                dk_g[r2][j] += a", "                dk_g[r2][j] = a"),
+    ("sp", "share = [np.concatenate([r * C + np.arange(C), (n_ch - 1 - r) * C + np.arange(C)])",
+     "share = [np.concatenate([r * C + np.arange(C), (n_ch - 2 - r) % n_ch * C + np.arange(C)])"),
 ]
 
 
