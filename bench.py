@@ -14,6 +14,9 @@ already resident in HBM:
   packed varlen shard: attention forward -> backward
   ring rank r: r+1 fused ring steps (LSE merge in the epilogue, bf16 O on the
       last) -> per-chunk backward into an fp32 dQ accumulator -> dQ to bf16
+  USP rank (Ulysses inside a zigzag-ring group): the Ulysses pack of Q, K, V
+      and dO and unpack of O, dQ (summing unpack of dK, dV) around the zigzag
+      ring steps and their backward
 The all-to-all itself is not run (one GPU).
 
 Output: ONE JSON line on stdout (driver contract), with a `roofline` object
@@ -152,6 +155,7 @@ class Step:
                                         for d in self.descs), dtype=torch.uint8, device=dev)
             self.ws_b = torch.empty(max(sp.sp_attn_workspace_size(d, sp.SP_OP_BWD)
                                         for d in self.descs), dtype=torch.uint8, device=dev)
+            self._ulysses_setup(sh)  # USP: Ulysses exchange inside the ring group
         else:
             self.desc = lib_desc(sp, sh)
             self.pairs = [allowed_pairs(sh.cu_q, sh.cu_k, sh.pos_q, sh.pos_k)]
@@ -166,34 +170,7 @@ class Step:
                                     dtype=torch.uint8, device=dev)
             self.ws_b = torch.empty(sp.sp_attn_workspace_size(self.desc, sp.SP_OP_BWD),
                                     dtype=torch.uint8, device=dev)
-            self.ulysses = sh.sp > 1
-            if self.ulysses:
-                Tl = sh.T_q // sh.sp
-                self.Tl = Tl
-                sb = sh.seed_base + 50
-                # the rank's pre-all-to-all token slice of every head
-                self.q_pre = to_dev(torch, randn_bf16_bits((Tl, sh.hs, D), sb))
-                self.do_pre = to_dev(torch, randn_bf16_bits((Tl, sh.hs, D), sb + 1))
-                self.k_pre = to_dev(torch, randn_bf16_bits((Tl, sh.hkv, D), sb + 2))
-                self.v_pre = to_dev(torch, randn_bf16_bits((Tl, sh.hkv, D), sb + 3))
-                self.qmap = ulysses_q_head_map(sh.hs, sh.sp)
-                self.mha = sh.hkv == sh.hs
-                self.kmap = self.qmap if self.mha else ulysses_kv_head_map(sh.hs, sh.hkv, sh.sp)
-                self.kw = len(self.kmap) // sh.sp
-                self.send_q = torch.empty((sh.sp, Tl, sh.H_loc, D), dtype=torch.bfloat16, device=dev)
-                self.send_do = torch.empty_like(self.send_q)
-                self.send_k = torch.empty((sh.sp, Tl, self.kw, D), dtype=torch.bfloat16, device=dev)
-                self.send_v = torch.empty_like(self.send_k)
-                self.o_pre = torch.empty((Tl, sh.hs, D), dtype=torch.bfloat16, device=dev)
-                self.dq_pre = torch.empty_like(self.o_pre)
-                self.dk_pre = torch.empty((Tl, sh.hkv, D), dtype=torch.bfloat16, device=dev)
-                self.dv_pre = torch.empty_like(self.dk_pre)
-                if not self.mha:
-                    # reverse all-to-all receive buffers of dK / dV: chunk j is
-                    # what rank j returns for the KV heads it was sent (the
-                    # other ranks' gradients are synthetic here: one GPU)
-                    self.recv_dk = to_dev(torch, randn_bf16_bits((sh.sp, Tl, self.kw, D), sb + 4))
-                    self.recv_dv = to_dev(torch, randn_bf16_bits((sh.sp, Tl, self.kw, D), sb + 5))
+            self._ulysses_setup(sh)
         H = nr * D
         self.flops_fwd = [4.0 * H * p for p in self.pairs]
         self.flops_dq = [6.0 * H * p for p in self.pairs]
@@ -202,13 +179,53 @@ class Step:
         self.flops_strict = 12.0 * H * sum(self.pairs)
         sh_ = sh
         self.pack_bytes = 0
-        if not self.ring and self.ulysses:
+        if self.ulysses:
             el = 2 * sh_.D
             Tl = self.Tl
             self.pack_bytes = Tl * sh_.hs * el + sh_.sp * Tl * sh_.H_loc * el
 
+
+    def _ulysses_setup(self, sh):
+        """Buffers of the Ulysses exchange around attention: the rank's
+        pre-all-to-all token slices, head maps, send buffers, and the
+        reverse-side outputs."""
+        torch, dev, D = self.torch, "cuda", sh.D
+        self.ulysses = sh.sp > 1
+        if self.ulysses:
+            Tl = sh.T_q // sh.sp
+            self.Tl = Tl
+            sb = sh.seed_base + 50
+            # the rank's pre-all-to-all token slice of every head
+            self.q_pre = to_dev(torch, randn_bf16_bits((Tl, sh.hs, D), sb))
+            self.do_pre = to_dev(torch, randn_bf16_bits((Tl, sh.hs, D), sb + 1))
+            self.k_pre = to_dev(torch, randn_bf16_bits((Tl, sh.hkv, D), sb + 2))
+            self.v_pre = to_dev(torch, randn_bf16_bits((Tl, sh.hkv, D), sb + 3))
+            self.qmap = ulysses_q_head_map(sh.hs, sh.sp)
+            self.mha = sh.hkv == sh.hs
+            self.kmap = self.qmap if self.mha else ulysses_kv_head_map(sh.hs, sh.hkv, sh.sp)
+            self.kw = len(self.kmap) // sh.sp
+            self.send_q = torch.empty((sh.sp, Tl, sh.H_loc, D), dtype=torch.bfloat16, device=dev)
+            self.send_do = torch.empty_like(self.send_q)
+            self.send_k = torch.empty((sh.sp, Tl, self.kw, D), dtype=torch.bfloat16, device=dev)
+            self.send_v = torch.empty_like(self.send_k)
+            self.o_pre = torch.empty((Tl, sh.hs, D), dtype=torch.bfloat16, device=dev)
+            self.dq_pre = torch.empty_like(self.o_pre)
+            self.dk_pre = torch.empty((Tl, sh.hkv, D), dtype=torch.bfloat16, device=dev)
+            self.dv_pre = torch.empty_like(self.dk_pre)
+            if not self.mha:
+                # reverse all-to-all receive buffers of dK / dV: chunk j is
+                # what rank j returns for the KV heads it was sent (the
+                # other ranks' gradients are synthetic here: one GPU)
+                self.recv_dk = to_dev(torch, randn_bf16_bits((sh.sp, Tl, self.kw, D), sb + 4))
+                self.recv_dv = to_dev(torch, randn_bf16_bits((sh.sp, Tl, self.kw, D), sb + 5))
+
     def run(self):
-        sp, t = self.sp, self.t
+        sp, t, sh = self.sp, self.t, self.sh
+        if self.ulysses:
+            t.arm(sp.SP_KERNEL_PACK, 0.0)
+            sp.sp_ulysses_pack(self.q_pre, sh.sp, sh.H_loc, self.qmap, dst=self.send_q)
+            sp.sp_ulysses_pack(self.k_pre, sh.sp, self.kw, self.kmap, dst=self.send_k)
+            sp.sp_ulysses_pack(self.v_pre, sh.sp, self.kw, self.kmap, dst=self.send_v)
         if self.ring:
             n = len(self.descs)
             for c in range(n):
@@ -216,6 +233,16 @@ class Step:
                 sp.sp_ring_step(self.descs[c], self.q, self.k[c], self.v[c], self.o_acc,
                                 self.lse_acc, init=(c == 0), o_out=self.o if c == n - 1 else None,
                                 workspace=self.ws_f)
+        else:
+            t.arm(sp.SP_KERNEL_ATTN_FWD, self.flops_fwd[0])
+            sp.sp_attn_fwd(self.desc, self.q, self.k, self.v, self.o, self.lse,
+                           workspace=self.ws_f)
+        if self.ulysses:
+            t.arm(sp.SP_KERNEL_UNPACK, 0.0)
+            sp.sp_ulysses_unpack(self.o.view(sh.sp, self.Tl, sh.H_loc, sh.D), self.qmap, sh.hs,
+                                 dst=self.o_pre)
+            sp.sp_ulysses_pack(self.do_pre, sh.sp, sh.H_loc, self.qmap, dst=self.send_do)
+        if self.ring:
             self.dq_acc.zero_()
             for c in range(n):
                 t.arm(sp.SP_KERNEL_ATTN_DQ, self.flops_dq[c])
@@ -224,33 +251,20 @@ class Step:
                                self.do, dq_acc=self.dq_acc, dk=self.dk[c], dv=self.dv[c],
                                workspace=self.ws_b)
             sp.sp_f32_to_bf16(self.dq_acc, self.dq)
-            return
-        sh = self.sh
-        if self.ulysses:
-            t.arm(sp.SP_KERNEL_PACK, 0.0)
-            sp.sp_ulysses_pack(self.q_pre, sh.sp, sh.H_loc, self.qmap, dst=self.send_q)
-            sp.sp_ulysses_pack(self.k_pre, sh.sp, self.kw, self.kmap, dst=self.send_k)
-            sp.sp_ulysses_pack(self.v_pre, sh.sp, self.kw, self.kmap, dst=self.send_v)
-        t.arm(sp.SP_KERNEL_ATTN_FWD, self.flops_fwd[0])
-        sp.sp_attn_fwd(self.desc, self.q, self.k, self.v, self.o, self.lse, workspace=self.ws_f)
-        if self.ulysses:
-            t.arm(sp.SP_KERNEL_UNPACK, 0.0)
-            sp.sp_ulysses_unpack(self.o.view(sh.sp, self.Tl, sh.H_loc, sh.D), self.qmap, sh.hs,
-                                 dst=self.o_pre)
-            sp.sp_ulysses_pack(self.do_pre, sh.sp, sh.H_loc, self.qmap, dst=self.send_do)
-        t.arm(sp.SP_KERNEL_ATTN_DQ, self.flops_dq[0])
-        t.arm(sp.SP_KERNEL_ATTN_DKDV, self.flops_dkdv[0])
-        sp.sp_attn_bwd(self.desc, self.q, self.k, self.v, self.o, self.lse, self.do, dq=self.dq,
-                       dk=self.dk, dv=self.dv, workspace=self.ws_b)
+        else:
+            t.arm(sp.SP_KERNEL_ATTN_DQ, self.flops_dq[0])
+            t.arm(sp.SP_KERNEL_ATTN_DKDV, self.flops_dkdv[0])
+            sp.sp_attn_bwd(self.desc, self.q, self.k, self.v, self.o, self.lse, self.do,
+                           dq=self.dq, dk=self.dk, dv=self.dv, workspace=self.ws_b)
         if self.ulysses:
             sp.sp_ulysses_unpack(self.dq.view(sh.sp, self.Tl, sh.H_loc, sh.D), self.qmap, sh.hs,
                                  dst=self.dq_pre)
-            if self.mha:
+            if self.mha and not self.ring:
                 sp.sp_ulysses_unpack(self.dk.view(sh.sp, self.Tl, sh.H_loc, sh.D), self.qmap,
                                      sh.hkv, dst=self.dk_pre)
                 sp.sp_ulysses_unpack(self.dv.view(sh.sp, self.Tl, sh.H_loc, sh.D), self.qmap,
                                      sh.hkv, dst=self.dv_pre)
-            else:
+            elif not self.mha:
                 t.arm(sp.SP_KERNEL_UNPACK_ADD, 0.0)
                 sp.sp_ulysses_unpack_add(self.recv_dk, self.kmap, sh.hkv, dst=self.dk_pre)
                 sp.sp_ulysses_unpack_add(self.recv_dv, self.kmap, sh.hkv, dst=self.dv_pre)
@@ -507,11 +521,11 @@ def main():
                        "H_loc": sh.H_loc, "H_real": sh.n_real_loc, "Hkv_loc": sh.Hkv_loc,
                        "segments": int(len(sh.cu_q) - 1), "ring_chunks": sh.ring_chunks,
                        "sp": sh.sp, "rank": sh.rank, "pairs_per_head": int(sum(st.pairs)),
-                       "flops_per_step": st.flops_metric},
+                       "flops_per_step": st.flops_metric,
+                       **({"ulysses_rank": sh.hp_rank} if sh.zigzag_sp and sh.sp > 1 else {})},
             "pct_of_bf16_peak": round(100.0 * value / PEAK_BF16_TFLOPS, 2),
             "strict_12D_tflops": round(st.flops_strict / (ms * 1e-3) / 1e12, 2),
-            # per-step GPU times (events between steps): the spread shows the
-            # occasional slow dispatches seen on the box; `value` uses the mean
+            # per-step GPU times (events between steps); `value` uses the mean
             "ms_per_step_median": round(per_step[len(per_step) // 2], 4),
             "ms_per_step_min": round(per_step[0], 4),
             "tflops_at_median_step": round(st.flops_metric / (per_step[len(per_step) // 2] * 1e-3) / 1e12, 2),

@@ -67,7 +67,7 @@ def _grad_sums(sh, dk, dv, do, nr):
             assert np.abs(got - want).max() <= 1e-2 * max(1.0, np.abs(want).max()), ("sum dV", s, kv)
 
 
-@pytest.mark.parametrize("name", [w for w in WORKLOADS if not w.startswith(("ring", "zigzag"))])
+@pytest.mark.parametrize("name", [w for w in WORKLOADS if not w.startswith(("ring", "zigzag", "usp"))])
 def test_fullsize_shard(sp, name):
     import torch
     sh = workload(name)
@@ -165,15 +165,19 @@ def test_fullsize_ring_rank(sp):
         assert np.abs(dv_all[:, kv].sum(axis=0) - want).max() <= 1e-2 * max(1.0, np.abs(want).max())
 
 
-def test_fullsize_zigzag_rank(sp):
+@pytest.mark.parametrize("name", [w for w in WORKLOADS if w.startswith(("zigzag", "usp"))])
+def test_fullsize_zigzag_rank(sp, name):
     """Zigzag ring rank 4 of 8 (Section 3.2; chunks 4 and 11 of 16, 8192
-    tokens each, 28 query / 4 KV heads): 8 ring steps over pieces of one
-    sequence with the fused merge, then per-step backward into an fp32 dQ
-    accumulator.  Oracle: monolithic attention over the keys of all steps
-    (positions decide visibility), on sampled rows and keys; whole-array
-    gradient identities over all steps."""
+    tokens each, 28 query / 4 KV heads), and the USP rank (ring rank 1 of 2,
+    Ulysses rank 2 of 4: chunks 1 and 2 of 4, 32768 tokens each, query heads
+    14-20 on KV head 2): ring steps over pieces of one sequence with the
+    fused merge, then per-step backward into an fp32 dQ accumulator.
+    Oracle: monolithic attention over the keys of all steps (positions decide
+    visibility), on sampled rows and keys; whole-array gradient identities
+    over all steps."""
     import torch
-    sh = [workload(w) for w in WORKLOADS if w.startswith("zigzag")][0]
+    sh = workload(name)
+    print(f"full-size {name}: T={sh.T_q} H_loc={sh.H_loc} steps={sh.ring_chunks}", flush=True)
     n, T, H, D = sh.ring_chunks, sh.T_q, sh.H_loc, sh.D
     q, do = zigzag_inputs(sh)
     kvs = [zigzag_inputs(sh, s) for s in range(n)]
@@ -199,8 +203,9 @@ def test_fullsize_zigzag_rank(sp):
     pcat = np.concatenate(pks)
     qf, dof = oracle.bf16_bits_to_f64(q), oracle.bf16_bits_to_f64(do)
     kw = dict(cu_q=np.array([0, T]), cu_k=np.array([0, n * T]), pos_q=sh.pos_q, pos_k=pcat,
-              H_loc=H, head_offset=0, num_real_heads=H, gqa_group=sh.gqa_group,
-              kv_head_offset=0, scale=sh.scale, causal=True)
+              H_loc=H, head_offset=sh.head_offset, num_real_heads=sh.num_real_heads,
+              gqa_group=sh.gqa_group, kv_head_offset=sh.kv_head_offset, scale=sh.scale,
+              causal=True)
     C = sh.chunk
     rows = np.array(sorted({0, 1, C - 1, C, C + 1, T - 1} |
                            set(np.random.default_rng(2).integers(0, T, 10).tolist())))

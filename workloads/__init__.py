@@ -23,7 +23,7 @@ import numpy as np
 __all__ = [
     "Shard", "WORKLOADS", "workload", "padded_heads", "bf16_bits_from_f32",
     "randn_bf16_bits", "varlen_lengths", "shard_inputs", "allowed_pairs",
-    "ulysses_q_head_map", "ulysses_kv_head_map",
+    "ulysses_q_head_map", "ulysses_kv_head_map", "usp_shard",
 ]
 
 
@@ -133,6 +133,9 @@ class Shard:
     # pieces of one sequence (single_sequence).
     zigzag_sp: int = 0
     single_sequence: bool = False
+    # USP (Ulysses inside zigzag-ring groups): the Ulysses rank inside the
+    # ring group (sp = Ulysses size, rank = ring rank, zigzag_sp = ring size).
+    hp_rank: int = 0
 
     @property
     def scale(self) -> float:
@@ -226,6 +229,35 @@ def _zigzag(name, L, sp, rank, D, hq, hkv, seed_base) -> Shard:
                  ring_chunks=sp, chunk=C, rank=rank, sp=1, zigzag_sp=sp, single_sequence=True)
 
 
+def usp_shard(name, L, hp, cp, r_cp, j_hp, D, hs, hkv, seed_base) -> Shard:
+    """USP rank (ring rank r_cp of cp, Ulysses rank j_hp of hp): after the
+    Ulysses all-to-all inside its ring group it holds the group's zigzag
+    share (chunks r_cp and 2*cp-1-r_cp of 2*cp) over the heads Ulysses rank
+    j_hp receives, and runs the zigzag ring over the shares of the other
+    ring groups' rank j_hp."""
+    C = L // (2 * cp)
+    hs_new = padded_heads(hs, hp)
+    hloc = hs_new // hp
+    off = j_hp * hloc
+    g = hs // hkv
+    real = [h for h in range(off, off + hloc) if h < hs]
+    if hkv == hs:
+        kvloc, kvoff = hloc, off
+    elif real:
+        kvoff = real[0] // g
+        kvloc = real[-1] // g + 1 - kvoff
+    else:
+        kvoff, kvloc = 0, 1
+    cu = np.array([0, C, 2 * C], dtype=np.int32)
+    a, b = zigzag_chunks(r_cp, cp)
+    pos_q = np.concatenate([a * C + np.arange(C), b * C + np.arange(C)]).astype(np.int32)
+    return Shard(name=name, T_q=2 * C, T_k=2 * C, D=D, H_loc=hloc, head_offset=off,
+                 num_real_heads=hs, num_padded_heads=hs_new, gqa_group=g, Hkv_loc=kvloc,
+                 kv_head_offset=kvoff, cu_q=cu, cu_k=cu.copy(), pos_q=pos_q, pos_k=pos_q.copy(),
+                 causal=True, seed_base=seed_base, hs=hs, hkv=hkv, ring_chunks=cp, chunk=C,
+                 rank=r_cp, sp=hp, zigzag_sp=cp, single_sequence=True, hp_rank=j_hp)
+
+
 def zigzag_chunks(rank: int, sp: int):
     """The two sequence chunks (of 2*sp) a zigzag rank holds, in position order."""
     return rank, 2 * sp - 1 - rank
@@ -254,6 +286,8 @@ def zigzag_inputs(sh: Shard, s: int = None):
         chunks = zigzag_chunks(sh.rank, sh.zigzag_sp)
         q = np.concatenate([piece(c, 0, sh.H_loc) for c in chunks])
         do = np.concatenate([piece(c, 3, sh.H_loc) for c in chunks])
+        q[:, sh.n_real_loc:] = 0   # dummy slots arrive zero from the pack
+        do[:, sh.n_real_loc:] = 0
         return q, do
     chunks = zigzag_step_chunks(sh, s)
     k = np.concatenate([piece(c, 1, sh.Hkv_loc) for c in chunks])
@@ -280,6 +314,8 @@ def workload(name: str) -> Shard:
         return _ulysses(name, 131072, 128, 40, 8, 16, 13, [32768] * 4, 400)
     if name == "zigzag_ring_L131072_sp8_r4_q28kv4_d128":
         return _zigzag(name, 131072, 8, 4, 128, 28, 4, 500)
+    if name == "usp_L131072_hp4_cp2_r1_j2_q28kv4_d128":
+        return usp_shard(name, 131072, 4, 2, 1, 2, 128, 28, 4, 600)
     raise KeyError(name)
 
 
@@ -290,6 +326,7 @@ WORKLOADS = [
     "ring_L131072_8chunks_r4_q28kv4_d128",
     "ulysses_long_L131072_4x32768_q40kv8_sp16_r13_d128",
     "zigzag_ring_L131072_sp8_r4_q28kv4_d128",
+    "usp_L131072_hp4_cp2_r1_j2_q28kv4_d128",
 ]
 
 
