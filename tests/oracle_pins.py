@@ -19,6 +19,9 @@ Sources of truth used here:
 """
 from __future__ import annotations
 
+import json
+import os
+
 import numpy as np
 import torch
 
@@ -433,8 +436,128 @@ def pin_usp_equals_no_sp(A, S):
         assert len(per) == hp * cp
 
 
+# ------------------------------------------------------------------ loss
+def pin_token_logprobs_torch(Lo):
+    """Token log-probabilities against torch's float64 cross entropy (minus
+    it), with ignored labels; closed forms: a constant row gives
+    lse = c + log V and logp = -log V."""
+    rng = np.random.default_rng(16)
+    T, V = 9, 37
+    x = rng.standard_normal((T, V)) * 3
+    lab = rng.integers(0, V, T)
+    lab[[2, 5]] = -100
+    logp, lse = Lo.token_logprobs(x, lab)
+    ce = torch.nn.functional.cross_entropy(torch.from_numpy(x), torch.from_numpy(lab),
+                                           ignore_index=-100, reduction="none").numpy()
+    assert np.allclose(logp, -ce, atol=1e-12) and np.all(logp[[2, 5]] == 0.0)
+    assert np.allclose(lse, torch.logsumexp(torch.from_numpy(x), 1).numpy(), atol=1e-12)
+    c = np.full((2, V), 1.75)
+    lp, ls = Lo.token_logprobs(c, np.array([0, V - 1]))
+    assert np.allclose(ls, 1.75 + np.log(V), atol=1e-13) and np.allclose(lp, -np.log(V), atol=1e-13)
+    assert np.allclose(Lo.sequence_sums(logp, [0, 4, 9]), [logp[:4].sum(), logp[4:].sum()])
+
+
+def pin_token_grad_fd(Lo):
+    """dlogits of sum_s g_s * (sum of logp over sequence s): central finite
+    differences; each token's row sums to zero; ignored tokens and tokens
+    past the last sequence get zero."""
+    rng = np.random.default_rng(17)
+    T, V = 7, 5
+    x = rng.standard_normal((T, V))
+    lab = rng.integers(0, V, T)
+    lab[3] = -100
+    cu = np.array([0, 2, 6])  # token 6 is padding
+    g = np.array([0.7, -1.3])
+
+    def f(xx):
+        return float(np.dot(g, Lo.sequence_sums(Lo.token_logprobs(xx, lab)[0], cu)))
+
+    d = Lo.token_logprob_grad(x, lab, g, cu)
+    h = 1e-6
+    fd = np.zeros_like(x)
+    for t in range(T):
+        for v in range(V):
+            e = np.zeros_like(x)
+            e[t, v] = h
+            fd[t, v] = (f(x + e) - f(x - e)) / (2 * h)
+    assert np.allclose(d, fd, atol=1e-8)
+    assert np.allclose(d.sum(axis=1), 0.0, atol=1e-14)
+    assert np.all(d[3] == 0) and np.all(d[6] == 0)
+
+
+def pin_listing2_worked_example(Lo):
+    """The paper's Listing 2 numbers (golden fixture): w0 gradients 8 / 12
+    with the gradient-carrying all-reduce, 4 / 6 without, 10 locally."""
+    with open(os.path.join(os.path.dirname(__file__), "golden", "listing2_allreduce_grads.json")) as fh:
+        gold = json.load(fh)
+    x = gold["x_per_rank"]
+    assert Lo.listing2_w0_grads(x, autograd=True).tolist() == gold["w0_grad_nn_all_reduce"]
+    assert Lo.listing2_w0_grads(x, autograd=False).tolist() == gold["w0_grad_plain_all_reduce"]
+    assert Lo.listing2_w0_grads([gold["x_local"]], autograd=True).tolist() == [gold["w0_grad_local"]]
+    assert np.mean(Lo.listing2_w0_grads(x, autograd=True)) == gold["w0_grad_local"]
+
+
+def _linear_head_grads(Lo, h, W, lab, cu, sp, kind, autograd, ref_sums=None, beta=0.1, scale=1.0):
+    """Weight gradient of a shared linear head (logits = h W) averaged over
+    sp ranks that each hold a sequential slice of every sequence's tokens."""
+    L = h.shape[0]
+    Tl = L // sp
+    parts = []
+    for r in range(sp):
+        rows = np.arange(r * Tl, (r + 1) * Tl)
+        lp, _ = Lo.token_logprobs(h[rows] @ W, lab[rows])
+        # sequence boundaries inside the slice
+        cu_r = np.clip(np.asarray(cu) - r * Tl, 0, Tl)
+        parts.append((rows, cu_r, Lo.sequence_sums(lp, cu_r)))
+    ps = np.stack([p[2] for p in parts])
+    if kind == "sft":
+        loss, up = Lo.sft_loss(ps, scale=scale, autograd=autograd)
+    else:
+        loss, up = Lo.dpo_loss(ps, ref_sums, beta, autograd=autograd)
+    dW = np.zeros_like(W)
+    for r, (rows, cu_r, _) in enumerate(parts):
+        dW += h[rows].T @ Lo.token_logprob_grad(h[rows] @ W, lab[rows], up[r], cu_r)
+    return loss, dW / sp
+
+
+def pin_sp_loss_equals_no_sp(Lo):
+    """SFT and DPO with the all-reduced sums: with the gradient-carrying
+    all-reduce, the rank-averaged gradient of a shared linear head equals
+    the gradient without SP (and the loss is the same); with a plain
+    all-reduce it is 1/sp of it -- Listing 2's finding, for the losses of
+    Section 3.3.  DPO against torch float64 autograd of -logsigmoid."""
+    rng = np.random.default_rng(18)
+    L, d, V, sp = 24, 6, 11, 3
+    h = rng.standard_normal((L, d))
+    W = rng.standard_normal((d, V)) * 0.5
+    lab = rng.integers(0, V, L)
+    lab[[0, 13]] = -100
+    cu = np.array([0, 10, 24])  # DPO: sequence 0 chosen, sequence 1 rejected
+    ref = rng.standard_normal((1, 2)) * 3
+    for kind in ("sft", "dpo"):
+        kw = dict(ref_sums=ref, beta=0.3, scale=1.0 / 22)
+        loss1, g1 = _linear_head_grads(Lo, h, W, lab, cu, 1, kind, True, **kw)
+        lossn, gn = _linear_head_grads(Lo, h, W, lab, cu, sp, kind, True,
+                                       **dict(kw, ref_sums=np.vstack([ref] + [np.zeros((1, 2))] * (sp - 1))))
+        lossp, gp = _linear_head_grads(Lo, h, W, lab, cu, sp, kind, False,
+                                       **dict(kw, ref_sums=np.vstack([ref] + [np.zeros((1, 2))] * (sp - 1))))
+        assert abs(loss1 - lossn) <= 1e-12 and np.allclose(g1, gn, atol=1e-12), kind
+        assert np.allclose(gp * sp, g1, atol=1e-12), kind
+    # DPO loss and gradient against torch autograd on the reduced sums
+    ps = torch.tensor(rng.standard_normal((sp, 4)), dtype=torch.float64, requires_grad=True)
+    rs = rng.standard_normal((sp, 4))
+    tot, rtot = ps.sum(0), torch.from_numpy(rs.sum(0))
+    z = 0.3 * ((tot[0::2] - rtot[0::2]) - (tot[1::2] - rtot[1::2]))
+    lt = -torch.nn.functional.logsigmoid(z).mean()
+    lt.backward()
+    lo, up = Lo.dpo_loss(ps.detach().numpy(), rs, 0.3, autograd=False)
+    assert abs(lo - float(lt.detach())) <= 1e-12 and np.allclose(up, ps.grad.numpy(), atol=1e-12)
+
+
 ATTN_PINS = [pin_single_visible_key, pin_zero_query_uniform, pin_torch_sdpa,
              pin_finite_differences, pin_gradient_sums, pin_packed_equals_separate]
 SP_PINS = [pin_merge_identity, pin_pack_unpack, pin_unpack_add_adjoint, pin_unpack_add_bf16]
+LOSS_PINS = [pin_token_logprobs_torch, pin_token_grad_fd, pin_listing2_worked_example,
+             pin_sp_loss_equals_no_sp]
 BOTH_PINS = [pin_ring_fold, pin_zigzag_fold, pin_ulysses_equals_no_sp,
              pin_ulysses_backward_equals_no_sp, pin_usp_equals_no_sp]

@@ -32,6 +32,11 @@ def test_decomposition_pin(pin):
     pin(A, S)
 
 
+@pytest.mark.parametrize("pin", P.LOSS_PINS, ids=lambda f: f.__name__)
+def test_loss_pin(pin):
+    pin(oracle.loss)
+
+
 def test_listing1_golden():
     """Pad count and dummy placement from Listing 1 (golden fixture)."""
     with open(os.path.join(HERE, "golden", "listing1_pad_heads.json")) as f:
@@ -146,6 +151,36 @@ def test_pins_catch_mutant(mutant):
     for pin in P.BOTH_PINS:
         try:
             pin(ma, ms)
+        except Exception:
+            caught.append(pin.__name__)
+    assert caught, "no pin caught the planted mistake"
+
+
+# plausible mistakes in the loss oracle, each caught by a loss pin
+LOSS_MUTANTS = [
+    ("return np.broadcast_to(u.sum(axis=0), u.shape).copy() if autograd else u.copy()",
+     "return u.copy()"),
+    ("    d[0::2] = -beta * sig_neg / P", "    d[0::2] = -sig_neg / P"),
+    ("    return g[:, None] * (onehot - p)", "    return g[:, None] * (p - onehot)"),
+    ("    g[lab == ignore_index] = 0.0", "    pass"),
+    ("    lse = m + np.log(np.exp(x - m[:, None]).sum(axis=1))",
+     "    lse = np.log(np.exp(x - m[:, None]).sum(axis=1))"),
+    ("    loss = -scale * ps.sum()", "    loss = -scale * ps.sum() / ps.shape[0]"),
+]
+
+
+@pytest.mark.parametrize("mutant", LOSS_MUTANTS, ids=lambda m: m[1][:40])
+def test_loss_pins_catch_mutant(mutant):
+    old, new = mutant
+    with open(os.path.join(os.path.dirname(oracle.__file__), "loss.py")) as f:
+        src = f.read()
+    assert old in src, old
+    mod = types.ModuleType("loss_mutant")
+    exec(compile(src.replace(old, new), "loss_mutant", "exec"), mod.__dict__)
+    caught = []
+    for pin in P.LOSS_PINS:
+        try:
+            pin(mod)
         except Exception:
             caught.append(pin.__name__)
     assert caught, "no pin caught the planted mistake"
