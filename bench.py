@@ -377,7 +377,8 @@ def copy_calibration(torch, nbytes=1 << 30):
 def bandwidth(sp, torch, reps=24):
     """GB/s of the bandwidth kernels at the workloads' shapes: the Ulysses
     pack/unpack and the summing K/V-gradient unpack of the 7B-like (c1) and
-    long (c4) shards and the fp32 LSE
+    long (c4) shards, the loss path's token log-probs and their backward
+    (4096 tokens x 152064 vocabulary), and the fp32 LSE
     merge of the ring shard (c3).  Buffer sets rotate (>= 4 sets, > 1 GB in
     total) so that the 256 MB last-level cache cannot serve repeats; each
     call is timed with HIP events, the median is reported."""
@@ -438,6 +439,27 @@ def bandwidth(sp, torch, reps=24):
         run(f"unpack_add {name} [{spn},{Tl},{kw_},{D}] -> [{Tl},{sh.hkv},{D}]", ua_bytes,
             mk_unpack_add, lambda b, kmap=kmap, hkv=sh.hkv: sp.sp_ulysses_unpack_add(
                 b[0], kmap, hkv, dst=b[1]))
+
+    # loss path: token log-probs (reads the logits once) and their backward
+    # (reads them again, writes dlogits) at the loss workload's shape
+    from workloads import LOSS_WORKLOAD
+    Tl_, V_ = LOSS_WORKLOAD["T"], LOSS_WORKLOAD["V"]
+    cu_ = np.linspace(0, Tl_, LOSS_WORKLOAD["n_seqs"] + 1).astype(np.int32)
+
+    def mk_loss():
+        x = torch.empty((Tl_, V_), dtype=torch.bfloat16, device="cuda").normal_(0.0, 2.0)
+        lab = torch.randint(0, V_, (Tl_,), dtype=torch.int32, device="cuda")
+        lse = torch.empty(Tl_, dtype=torch.float32, device="cuda")
+        lp = torch.empty_like(lse)
+        ss = torch.empty(len(cu_) - 1, dtype=torch.float32, device="cuda")
+        g = torch.full((len(cu_) - 1,), 1.0 / Tl_, dtype=torch.float32, device="cuda")
+        sp.sp_token_logprob(x, lab, cu_, logp=lp, lse=lse, seq_sum=ss)
+        return x, lab, lse, lp, ss, g, torch.empty_like(x)
+
+    run(f"token_logprob {LOSS_WORKLOAD['name']} [{Tl_},{V_}] bf16", Tl_ * V_ * 2, mk_loss,
+        lambda b: sp.sp_token_logprob(b[0], b[1], cu_, logp=b[3], lse=b[2], seq_sum=b[4]))
+    run(f"token_logprob_bwd {LOSS_WORKLOAD['name']} [{Tl_},{V_}] bf16", 2 * Tl_ * V_ * 2, mk_loss,
+        lambda b: sp.sp_token_logprob_bwd(b[0], b[1], b[2], cu_, b[5], dlogits=b[6]))
 
     sh = workload("ring_L131072_8chunks_r4_q28kv4_d128")
     T, H, D = sh.chunk, sh.H_loc, sh.D

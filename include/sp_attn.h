@@ -276,6 +276,71 @@ sp_status sp_attn_schedule(const sp_attn_desc* desc, int32_t op, int32_t* items,
                            int32_t* n_items);
 
 /*
+ * SP-aware loss (Section 3.3, Correct Loss Calculation; Section 5.1 and
+ * Listing 2).  Each rank holds a slice of the sequence, so it forms the
+ * label log-probabilities of its own tokens only; the SFT loss (Eq. 1) is
+ * the sum over all tokens, and DPO (Eq. 2, read with the log on both
+ * ratios) needs the four sequence log-probabilities summed over the ranks
+ * before the sigmoid.  The sums cross ranks through an all-reduce that
+ * carries gradients (its backward all-reduces the upstream gradient).
+ *
+ * sp_token_logprob: for token t with label y = labels[t] (DEVICE int32 [T])
+ * inside a sequence and y in [0, V), y != ignore_index:
+ *   lse[t]  = log sum_v exp(logits[t, v])            (float32, natural log)
+ *   logp[t] = logits[t, y] - lse[t]                   (0 for other tokens)
+ *   seq_sum[s] = sum of logp over [cu[s], cu[s+1])   (fixed order: deterministic)
+ * logits: DEVICE bf16 [T, V] row-major, 16-byte aligned, V a multiple of 8.
+ * cu_seqlens: HOST, num_seqs + 1 non-decreasing entries, cu[0] >= 0,
+ * cu[num_seqs] <= T; tokens outside every sequence get logp = 0.  lse is
+ * written for every token (the backward reads it).  Limits: num_seqs <= 256
+ * (SP_ERR_UNSUPPORTED).  Reads T*V*2 bytes once.
+ */
+enum { SP_LOSS_SFT = 0, SP_LOSS_DPO = 1 };
+sp_status sp_token_logprob(const void* logits, const int32_t* labels, int32_t T, int32_t V,
+                           int32_t ignore_index, const int32_t* cu_seqlens, int32_t num_seqs,
+                           float* logp, float* lse, float* seq_sum, void* stream);
+
+/*
+ * Backward of sum_s grad_seq[s] * seq_sum[s] to the logits (DEVICE bf16
+ * [T, V] out): for a token t of sequence s with a counted label y,
+ *   dlogits[t, v] = g * (1[v == y] - exp(logits[t, v] - lse[t])),  g = grad_seq[s]
+ * rounded to bf16 (nearest-even); every other row is written as zeros.
+ * grad_seq: DEVICE float32 [num_seqs] (from sp_loss_reduce); lse from the
+ * forward.  Same shape rules as sp_token_logprob.  Reads T*V*2 bytes, writes
+ * T*V*2 bytes.
+ */
+sp_status sp_token_logprob_bwd(const void* logits, const int32_t* labels, const float* lse,
+                               int32_t T, int32_t V, int32_t ignore_index,
+                               const int32_t* cu_seqlens, int32_t num_seqs,
+                               const float* grad_seq, void* dlogits, void* stream);
+
+/*
+ * Loss over the ranks' partial sums and every rank's upstream gradient.
+ * partial_sums: DEVICE float32 [sp, num_seqs], row r = rank r's seq_sum
+ * (on one GPU all rows are available; across GPUs, the rows an all-gather
+ * delivers).  Totals are summed over ranks in ascending order.
+ *   SP_LOSS_SFT: loss = -coef * sum over sequences of the totals
+ *                (coef = 1 for Eq. 1, 1 / #tokens for a mean).
+ *   SP_LOSS_DPO: sequences are pairs (2p chosen, 2p+1 rejected);
+ *                z_p = coef * ((pi_w - ref_w) - (pi_l - ref_l)) with coef = beta
+ *                and ref totals from ref_partial_sums (DEVICE [sp, num_seqs],
+ *                the reference model's seq_sum, no gradient);
+ *                loss = mean over pairs of -log sigmoid(z_p).
+ * grad: DEVICE float32 [sp, num_seqs], rank r's upstream gradient for its
+ * own seq_sum: sp times d loss / d total, the gradient a gradient-carrying
+ * all-reduce returns to every rank (each rank computes the same loss, and
+ * the backward of the all-reduce sums their upstream gradients).  Averaging
+ * parameter gradients over the sp ranks then gives the gradient without SP
+ * (Listing 2: 8 and 12 average to the local 10; a plain all-reduce gives 4
+ * and 6).  loss: DEVICE float32 [1].  Errors: SP_ERR_INVALID_ARG for sp < 1,
+ * num_seqs < 1, an odd DPO count, missing pointers, non-finite coef;
+ * SP_ERR_UNSUPPORTED for num_seqs > 256.
+ */
+sp_status sp_loss_reduce(const float* partial_sums, const float* ref_partial_sums, int32_t sp,
+                         int32_t num_seqs, int32_t kind, float coef, float* loss, float* grad,
+                         void* stream);
+
+/*
  * Opt-in kernel timer (measurement support, per calling thread).  After
  * sp_profile_events(id, start, stop) with hipEvent_t handles created by the
  * caller, every launch of kernel `id` made by THIS thread records `start` on
@@ -291,7 +356,9 @@ enum {
   SP_KERNEL_PACK = 4,     /* Ulysses pack                                */
   SP_KERNEL_UNPACK = 5,   /* Ulysses unpack                              */
   SP_KERNEL_LSE_MERGE = 6,/* standalone LSE merge                        */
-  SP_KERNEL_UNPACK_ADD = 7/* summing unpack of GQA K/V gradients         */
+  SP_KERNEL_UNPACK_ADD = 7,/* summing unpack of GQA K/V gradients        */
+  SP_KERNEL_TOKEN_LOGPROB = 8,     /* token log-probabilities (forward)  */
+  SP_KERNEL_TOKEN_LOGPROB_BWD = 9  /* their backward to the logits       */
 };
 sp_status sp_profile_events(int32_t kernel_id, void* start_event, void* stop_event);
 

@@ -66,6 +66,9 @@ def load() -> ctypes.CDLL:
         "sp_ulysses_pack": (i32, [vp, i32, i32, i32, i32, i32, _i32p, vp, vp]),
         "sp_ulysses_unpack": (i32, [vp, i32, i32, i32, i32, _i32p, i32, vp, vp]),
         "sp_ulysses_unpack_add": (i32, [vp, i32, i32, i32, i32, _i32p, i32, vp, vp]),
+        "sp_token_logprob": (i32, [vp, vp, i32, i32, i32, _i32p, i32, vp, vp, vp, vp]),
+        "sp_token_logprob_bwd": (i32, [vp, vp, vp, i32, i32, i32, _i32p, i32, vp, vp, vp]),
+        "sp_loss_reduce": (i32, [vp, vp, i32, i32, i32, ctypes.c_float, vp, vp, vp]),
         "sp_attn_workspace_size": (i32, [D, i32, ctypes.POINTER(sz)]),
         "sp_attn_fwd": (i32, [D, vp, vp, vp, vp, vp, vp, sz, vp]),
         "sp_attn_bwd": (i32, [D, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
@@ -84,12 +87,14 @@ def load() -> ctypes.CDLL:
 
 
 EXPORTED = ["sp_status_string", "sp_version", "sp_ulysses_pack", "sp_ulysses_unpack",
-            "sp_ulysses_unpack_add",
+            "sp_ulysses_unpack_add", "sp_token_logprob", "sp_token_logprob_bwd", "sp_loss_reduce",
             "sp_attn_workspace_size", "sp_attn_fwd", "sp_attn_bwd", "sp_ring_step",
             "sp_lse_merge", "sp_f32_to_bf16", "sp_attn_schedule", "sp_profile_events"]
 
 SP_KERNEL_ATTN_FWD, SP_KERNEL_ATTN_DQ, SP_KERNEL_ATTN_DKDV = 1, 2, 3
 SP_KERNEL_PACK, SP_KERNEL_UNPACK, SP_KERNEL_LSE_MERGE, SP_KERNEL_UNPACK_ADD = 4, 5, 6, 7
+SP_KERNEL_TOKEN_LOGPROB, SP_KERNEL_TOKEN_LOGPROB_BWD = 8, 9
+SP_LOSS_SFT, SP_LOSS_DPO = 0, 1
 
 
 def status_string(s: int) -> str:
@@ -204,6 +209,60 @@ def sp_ulysses_unpack_add(src, head_map: Sequence[int], H_dst: int, dst=None, st
     _check(load().sp_ulysses_unpack_add(_ptr(src), T, Hs, D, sp, m.ctypes.data_as(_i32p), H_dst,
                                         _ptr(dst), _stream(stream)), "sp_ulysses_unpack_add")
     return dst
+
+
+def _cu(cu_seqlens):
+    cu = np.ascontiguousarray(np.asarray(cu_seqlens, dtype=np.int32))
+    return cu, len(cu) - 1
+
+
+def sp_token_logprob(logits, labels, cu_seqlens, ignore_index: int = -100, logp=None, lse=None,
+                     seq_sum=None, stream=None):
+    """logits [T, V] bf16, labels [T] int32 (device) -> (logp [T], lse [T],
+    seq_sum [num_seqs]) float32."""
+    import torch
+    T, V = logits.shape
+    cu, n = _cu(cu_seqlens)
+    dev = logits.device
+    logp = torch.empty(T, dtype=torch.float32, device=dev) if logp is None else logp
+    lse = torch.empty(T, dtype=torch.float32, device=dev) if lse is None else lse
+    if seq_sum is None:
+        seq_sum = torch.empty(max(n, 0), dtype=torch.float32, device=dev)
+    _check(load().sp_token_logprob(_ptr(logits), _ptr(labels), T, V, ignore_index,
+                                   cu.ctypes.data_as(_i32p), n, _ptr(logp), _ptr(lse),
+                                   _ptr(seq_sum) if n > 0 else None, _stream(stream)),
+           "sp_token_logprob")
+    return logp, lse, seq_sum
+
+
+def sp_token_logprob_bwd(logits, labels, lse, cu_seqlens, grad_seq, ignore_index: int = -100,
+                         dlogits=None, stream=None):
+    """-> dlogits [T, V] bf16 = g (onehot(label) - softmax(logits)) per
+    counted token, g = grad_seq[its sequence]."""
+    import torch
+    T, V = logits.shape
+    cu, n = _cu(cu_seqlens)
+    if dlogits is None:
+        dlogits = torch.empty_like(logits)
+    _check(load().sp_token_logprob_bwd(_ptr(logits), _ptr(labels), _ptr(lse), T, V, ignore_index,
+                                       cu.ctypes.data_as(_i32p), n, _ptr(grad_seq), _ptr(dlogits),
+                                       _stream(stream)), "sp_token_logprob_bwd")
+    return dlogits
+
+
+def sp_loss_reduce(partial_sums, kind: int, coef: float, ref_partial_sums=None, loss=None,
+                   grad=None, stream=None):
+    """partial_sums [sp, n] float32 -> (loss [1], grad [sp, n]): the loss over
+    the ranks' all-reduced sums and each rank's upstream gradient."""
+    import torch
+    spn, n = partial_sums.shape
+    dev = partial_sums.device
+    loss = torch.empty(1, dtype=torch.float32, device=dev) if loss is None else loss
+    grad = torch.empty((spn, n), dtype=torch.float32, device=dev) if grad is None else grad
+    _check(load().sp_loss_reduce(_ptr(partial_sums), _ptr(ref_partial_sums), spn, n, kind,
+                                 float(coef), _ptr(loss), _ptr(grad), _stream(stream)),
+           "sp_loss_reduce")
+    return loss, grad
 
 
 def sp_attn_fwd(desc: Desc, q, k, v, o=None, lse=None, workspace=None, stream=None):

@@ -14,7 +14,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libspattn.so")
 
-SOURCES = ["api.cpp", "k_bandwidth.hip", "k_attn_fwd.hip", "k_attn_bwd.hip"]
+SOURCES = ["api.cpp", "k_bandwidth.hip", "k_attn_fwd.hip", "k_attn_bwd.hip", "k_loss.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [

@@ -427,6 +427,70 @@ sp_status sp_ulysses_unpack_add(const void* src, int32_t T_loc, int32_t H_src_lo
   return SP_OK;
 }
 
+namespace {
+// Shared validation of the loss calls: vocabulary, sequences (host copy),
+// alignment.  Fills the kernel arguments.
+sp_status loss_args(int32_t T, int32_t V, int32_t ignore_index, const int32_t* cu,
+                    int32_t num_seqs, spk::LossArgs& a) {
+  if (T < 0 || V < 8 || V % 8 != 0 || num_seqs < 0) return SP_ERR_INVALID_ARG;
+  if (num_seqs > spk::kMaxLossSeqs) return SP_ERR_UNSUPPORTED;
+  if (num_seqs > 0 && !cu) return SP_ERR_INVALID_ARG;
+  a.T = T; a.V = V; a.ignore_index = ignore_index; a.n_seqs = num_seqs;
+  a.cu[0] = num_seqs > 0 ? cu[0] : 0;
+  if (a.cu[0] < 0) return SP_ERR_INVALID_ARG;
+  for (int s = 0; s < num_seqs; ++s) {
+    if (cu[s + 1] < cu[s]) return SP_ERR_INVALID_ARG;
+    a.cu[s + 1] = cu[s + 1];
+  }
+  if (a.cu[num_seqs] > T) return SP_ERR_INVALID_ARG;
+  return SP_OK;
+}
+}  // namespace
+
+sp_status sp_token_logprob(const void* logits, const int32_t* labels, int32_t T, int32_t V,
+                           int32_t ignore_index, const int32_t* cu_seqlens, int32_t num_seqs,
+                           float* logp, float* lse, float* seq_sum, void* stream) {
+  spk::LossArgs a;
+  sp_status st = loss_args(T, V, ignore_index, cu_seqlens, num_seqs, a);
+  if (st != SP_OK) return st;
+  if (T > 0 && (!logits || !labels || !logp || !lse || !aligned16(logits)))
+    return SP_ERR_INVALID_ARG;
+  if (num_seqs > 0 && !seq_sum) return SP_ERR_INVALID_ARG;
+  SP_HIP(spk::launch_token_logprob(a, logits, labels, logp, lse, seq_sum, (hipStream_t)stream));
+  return SP_OK;
+}
+
+sp_status sp_token_logprob_bwd(const void* logits, const int32_t* labels, const float* lse,
+                               int32_t T, int32_t V, int32_t ignore_index,
+                               const int32_t* cu_seqlens, int32_t num_seqs,
+                               const float* grad_seq, void* dlogits, void* stream) {
+  spk::LossArgs a;
+  sp_status st = loss_args(T, V, ignore_index, cu_seqlens, num_seqs, a);
+  if (st != SP_OK) return st;
+  if (T == 0) return SP_OK;
+  if (!logits || !labels || !lse || !dlogits || !aligned16(logits) || !aligned16(dlogits) ||
+      (num_seqs > 0 && !grad_seq))
+    return SP_ERR_INVALID_ARG;
+  SP_HIP(spk::launch_token_logprob_bwd(a, logits, labels, lse, grad_seq, dlogits,
+                                       (hipStream_t)stream));
+  return SP_OK;
+}
+
+sp_status sp_loss_reduce(const float* partial_sums, const float* ref_partial_sums, int32_t sp,
+                         int32_t num_seqs, int32_t kind, float coef, float* loss, float* grad,
+                         void* stream) {
+  if (sp < 1 || num_seqs < 1 || (kind != SP_LOSS_SFT && kind != SP_LOSS_DPO) || !partial_sums ||
+      !loss || !grad || !std::isfinite(coef))
+    return SP_ERR_INVALID_ARG;
+  if (kind == SP_LOSS_DPO && (num_seqs % 2 != 0 || !ref_partial_sums)) return SP_ERR_INVALID_ARG;
+  if (num_seqs > 256 || sp > 4096) return SP_ERR_UNSUPPORTED;
+  spk::LossReduceArgs a;
+  a.sp = sp; a.n = num_seqs; a.kind = kind; a.coef = coef;
+  SP_HIP(spk::launch_loss_reduce(a, partial_sums, ref_partial_sums, loss, grad,
+                                 (hipStream_t)stream));
+  return SP_OK;
+}
+
 sp_status sp_attn_workspace_size(const sp_attn_desc* desc, int32_t op, size_t* bytes) {
   if (!bytes) return SP_ERR_INVALID_ARG;
   if (op != SP_OP_FWD && op != SP_OP_BWD && op != SP_OP_RING_STEP) return SP_ERR_INVALID_ARG;

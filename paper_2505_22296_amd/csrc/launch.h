@@ -9,7 +9,7 @@ namespace spk {
 // SP_KERNEL_* constants of the public header).
 enum KernelId {
   kKFwd = 1, kKDq = 2, kKDkdv = 3, kKPack = 4, kKUnpack = 5, kKMerge = 6, kKUnpackAdd = 7,
-  kKCount = 8
+  kKLogprob = 8, kKLogprobBwd = 9, kKCount = 10
 };
 
 struct KernelTimer {
@@ -55,6 +55,18 @@ struct PackAddArgs {
   int sp, T, Hs, Hd, nch;
   int16_t start[kMaxAddDst + 1];
   int16_t slot[kMaxMap];
+};
+
+// Loss path: vocabulary size V (multiple of 8), the sequences' token
+// ranges [cu[s], cu[s+1]) (host copy by value) and the ignored label.
+static constexpr int kMaxLossSeqs = 256;
+struct LossArgs {
+  int T, V, ignore_index, n_seqs;
+  int cu[kMaxLossSeqs + 1];
+};
+struct LossReduceArgs {
+  int sp, n, kind;  // kind 0 = SFT, 1 = DPO
+  float coef;       // SFT: loss scale; DPO: beta
 };
 
 struct ReduceArgs {
@@ -118,6 +130,13 @@ struct DkdvArgs {
 hipError_t launch_pack(const void* src, void* dst, const PackArgs& a, hipStream_t st);
 hipError_t launch_unpack(const void* src, void* dst, const PackArgs& a, hipStream_t st);
 hipError_t launch_unpack_add(const void* src, void* dst, const PackAddArgs& a, hipStream_t st);
+hipError_t launch_token_logprob(const LossArgs& a, const void* logits, const int32_t* labels,
+                                float* logp, float* lse, float* seq_sum, hipStream_t st);
+hipError_t launch_token_logprob_bwd(const LossArgs& a, const void* logits, const int32_t* labels,
+                                    const float* lse, const float* grad_seq, void* dlogits,
+                                    hipStream_t st);
+hipError_t launch_loss_reduce(const LossReduceArgs& a, const float* ps, const float* refs,
+                              float* loss, float* grad, hipStream_t st);
 hipError_t launch_merge(float* o_acc, float* lse_acc, const void* o_part, bool part_bf16,
                         const float* lse_part, int T, int H, int D, void* o_out, hipStream_t st);
 hipError_t launch_zero_heads_bf16(void* x, int T, int H, int D, int h0, int h1, hipStream_t st);

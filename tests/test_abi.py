@@ -134,6 +134,40 @@ def test_pack_unpack_validation():
     assert lib.sp_ulysses_unpack_add(fake, 8, 257, 64, 2, pb, 2, fake, None) == sp.SP_ERR_UNSUPPORTED
 
 
+def test_loss_validation():
+    """The loss entry points reject bad shapes and sequence tables before any
+    launch."""
+    lib = sp.load()
+    i32p = ctypes.POINTER(ctypes.c_int32)
+
+    def cu(*v):
+        a = np.array(v, dtype=np.int32)
+        return a, a.ctypes.data_as(i32p)
+
+    fake = 1 << 20
+    a, c = cu(0, 4, 8)
+    assert lib.sp_token_logprob(fake, fake, 8, 60, -100, c, 2, fake, fake, fake, None) == sp.SP_ERR_INVALID_ARG
+    assert lib.sp_token_logprob(fake + 4, fake, 8, 64, -100, c, 2, fake, fake, fake, None) == sp.SP_ERR_INVALID_ARG
+    a, c = cu(0, 6, 4)  # decreasing
+    assert lib.sp_token_logprob(fake, fake, 8, 64, -100, c, 2, fake, fake, fake, None) == sp.SP_ERR_INVALID_ARG
+    a, c = cu(0, 4, 9)  # past T
+    assert lib.sp_token_logprob(fake, fake, 8, 64, -100, c, 2, fake, fake, fake, None) == sp.SP_ERR_INVALID_ARG
+    a, c = cu(0, 4, 8)
+    assert lib.sp_token_logprob(fake, fake, 8, 64, -100, c, 2, fake, fake, None, None) == sp.SP_ERR_INVALID_ARG
+    big, cb = cu(*range(258))
+    assert lib.sp_token_logprob(fake, fake, 300, 64, -100, cb, 257, fake, fake, fake, None) == sp.SP_ERR_UNSUPPORTED
+    assert lib.sp_token_logprob_bwd(fake, fake, fake, 8, 64, -100, c, 2, None, fake, None) == sp.SP_ERR_INVALID_ARG
+    assert lib.sp_token_logprob_bwd(fake, fake, fake, 8, 64, -100, c, 2, fake, fake + 2, None) == sp.SP_ERR_INVALID_ARG
+    assert lib.sp_token_logprob_bwd(fake, fake, fake, 0, 64, -100, None, 0, None, None, None) == sp.SP_OK
+    f = ctypes.c_float
+    assert lib.sp_loss_reduce(fake, None, 2, 3, sp.SP_LOSS_DPO, f(0.1), fake, fake, None) == sp.SP_ERR_INVALID_ARG
+    assert lib.sp_loss_reduce(fake, None, 2, 4, sp.SP_LOSS_DPO, f(0.1), fake, fake, None) == sp.SP_ERR_INVALID_ARG
+    assert lib.sp_loss_reduce(fake, fake, 0, 4, sp.SP_LOSS_SFT, f(1.0), fake, fake, None) == sp.SP_ERR_INVALID_ARG
+    assert lib.sp_loss_reduce(fake, fake, 2, 4, 7, f(1.0), fake, fake, None) == sp.SP_ERR_INVALID_ARG
+    assert lib.sp_loss_reduce(fake, fake, 2, 4, sp.SP_LOSS_SFT, f(float("nan")), fake, fake, None) == sp.SP_ERR_INVALID_ARG
+    assert lib.sp_loss_reduce(fake, fake, 2, 258, sp.SP_LOSS_SFT, f(1.0), fake, fake, None) == sp.SP_ERR_UNSUPPORTED
+
+
 # ------------------------------------------------------------- scheduler
 def _coverage_from_schedule(sh, items, kind):
     """Boolean [T_q, T_k] per real head: pairs the work list may make visible

@@ -23,7 +23,7 @@ import numpy as np
 __all__ = [
     "Shard", "WORKLOADS", "workload", "padded_heads", "bf16_bits_from_f32",
     "randn_bf16_bits", "varlen_lengths", "shard_inputs", "allowed_pairs",
-    "ulysses_q_head_map", "ulysses_kv_head_map", "usp_shard",
+    "ulysses_q_head_map", "ulysses_kv_head_map", "usp_shard", "loss_inputs", "LOSS_WORKLOAD",
 ]
 
 
@@ -380,3 +380,29 @@ def allowed_pairs(cu_q, cu_k, pos_q, pos_k, causal: bool = True,
         for_rows = np.clip(np.arange(nq, dtype=np.int64) + d + 1, 0, nk)
         total += int(for_rows.sum())
     return total
+
+
+# Loss path of one rank: the 7B-like shard's token slice (32768 tokens over
+# SP 8 = 4096 tokens) against a 152064-entry vocabulary (Qwen2.5's padded
+# vocabulary, from the public model config; the paper names the models, not
+# their vocabulary), two sequences (a DPO chosen / rejected pair).
+LOSS_WORKLOAD = dict(name="loss_T4096_V152064_dpo_pair", T=4096, V=152064, n_seqs=2, seed=700)
+
+
+def loss_inputs(T: int, V: int, n_seqs: int, seed: int, prompt_frac: float = 0.25,
+                logit_scale: float = 2.0, rows_per_block: int = 256):
+    """bf16 logit bits [T, V] (N(0, logit_scale^2), rows drawn in blocks of
+    rows_per_block with seed + block index), labels [T] int32 uniform in
+    [0, V) with the first prompt_frac of each sequence set to -100 (prompt
+    tokens are not scored), and cu_seqlens splitting T evenly into n_seqs."""
+    bits = np.empty((T, V), dtype=np.uint16)
+    for b0 in range(0, T, rows_per_block):
+        b1 = min(T, b0 + rows_per_block)
+        bits[b0:b1] = randn_bf16_bits((b1 - b0, V), seed + b0 // rows_per_block, logit_scale)
+    rng = np.random.default_rng(seed + 100000)
+    labels = rng.integers(0, V, T).astype(np.int32)
+    cu = np.linspace(0, T, n_seqs + 1).astype(np.int32)
+    for s in range(n_seqs):
+        a, b = int(cu[s]), int(cu[s + 1])
+        labels[a:a + int((b - a) * prompt_frac)] = -100
+    return bits, labels, cu
