@@ -199,7 +199,10 @@ sp_status sp_attn_workspace_size(const sp_attn_desc* desc, int32_t op, size_t* b
  * o: [T_q, H_loc, D] bf16 output; lse: [H_loc, T_q] float32 output.
  * Real head rows: O = softmax(scale q k^T + mask) v, LSE = log-sum-exp of the
  * masked scaled scores.  Rows without visible keys and all dummy slots:
- * O = +0.0, LSE = -inf.
+ * O = +0.0, LSE = -inf.  Empty inputs: pointers are only required for
+ * tensors with elements; T_q == 0 is a no-op, T_k == 0 gives every row
+ * O = +0.0 and LSE = -inf (the same holds for sp_ring_step, and sp_attn_bwd
+ * then writes dQ = +0.0; with T_q == 0 it writes dK = dV = +0.0).
  */
 sp_status sp_attn_fwd(const sp_attn_desc* desc, const void* q, const void* k, const void* v,
                       void* o, float* lse, void* workspace, size_t workspace_bytes,

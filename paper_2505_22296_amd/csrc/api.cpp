@@ -528,12 +528,16 @@ static sp_status fwd_common(const sp_attn_desc* d, const void* q, const void* k,
   Problem p;
   sp_status s = validate(d, p);
   if (s != SP_OK) return s;
-  if (!q || !k || !v) return SP_ERR_INVALID_ARG;
-  if (ring ? (!o_acc || !lse_acc) : (!o || !lse)) return SP_ERR_INVALID_ARG;
+  // pointers are required for tensors that have elements: no query rows is a
+  // no-op; no keys leaves every row with O = 0 and LSE = -inf
+  if (d->T_q > 0 && !q) return SP_ERR_INVALID_ARG;
+  if (d->T_k > 0 && (!k || !v)) return SP_ERR_INVALID_ARG;
+  if (d->T_q > 0 && (ring ? (!o_acc || !lse_acc) : (!o || !lse))) return SP_ERR_INVALID_ARG;
   if (!aligned16(q) || !aligned16(k) || !aligned16(v) || (o && !aligned16(o)) ||
       (o_acc && !aligned16(o_acc)) || (o_out && !aligned16(o_out)))
     return SP_ERR_INVALID_ARG;
   if (init != 0 && init != 1) return SP_ERR_INVALID_ARG;
+  if (d->T_q == 0) return SP_OK;
   const bool include_empty = !ring || init || o_out;
   std::vector<int32_t> items;
   schedule_rows(d, p, spk::kFwdBM, spk::kFwdBN, include_empty, items);
@@ -595,11 +599,21 @@ sp_status sp_attn_bwd(const sp_attn_desc* d, const void* q, const void* k, const
   Problem p;
   sp_status s = validate(d, p);
   if (s != SP_OK) return s;
-  if (!q || !k || !v || !o || !lse || !dout || !dk || !dv) return SP_ERR_INVALID_ARG;
-  if ((dq == nullptr) == (dq_acc == nullptr)) return SP_ERR_INVALID_ARG;
+  // pointers are required for tensors that have elements
+  if (d->T_q > 0 && (!q || !o || !lse || !dout || (dq == nullptr) == (dq_acc == nullptr)))
+    return SP_ERR_INVALID_ARG;
+  if (d->T_k > 0 && (!k || !v || !dk || !dv)) return SP_ERR_INVALID_ARG;
+  if (dq && dq_acc) return SP_ERR_INVALID_ARG;
   for (const void* ptr : {q, k, v, o, dout, (const void*)dk, (const void*)dv})
     if (!aligned16(ptr)) return SP_ERR_INVALID_ARG;
   if ((dq && !aligned16(dq)) || (dq_acc && !aligned16(dq_acc))) return SP_ERR_INVALID_ARG;
+  if (d->T_q == 0) {  // no rows: the keys receive no gradient
+    SP_HIP(spk::launch_zero_heads_bf16(dk, d->T_k, d->Hkv_loc, p.D, 0, d->Hkv_loc,
+                                       (hipStream_t)stream));
+    SP_HIP(spk::launch_zero_heads_bf16(dv, d->T_k, d->Hkv_loc, p.D, 0, d->Hkv_loc,
+                                       (hipStream_t)stream));
+    return SP_OK;
+  }
   std::vector<int32_t> it_dq, it_kv;
   schedule_rows(d, p, spk::kDqBM, spk::kDqBN, true, it_dq);
   schedule_keys(d, p, spk::kDkdvBN, spk::kDkdvBQ, it_kv);

@@ -388,3 +388,51 @@ def test_usp_ring_groups(sp, hs, hkv, D):
                 recv = torch.stack([got[j][i * Tl:(i + 1) * Tl] for j in range(hp)]).contiguous()
                 assert_close(from_dev(sp.sp_ulysses_unpack(recv, qmap, hs)), want[rows],
                              f"USP layer {what} group {r} slice {i}")
+
+
+def test_all_dummy_rank(sp):
+    """A rank whose slots are all dummies (ranks 14-15 of 40 heads padded to
+    48 for SP 16): nothing is computed, O / dQ are +0, LSE is -inf, the KV
+    slot gets dK = dV = +0."""
+    import torch
+    sh = make_shard("all_dummy", 700, 700, 128, 3, 42, 40, 48, 5, 1, 0, [400, 300], seed_base=3)
+    assert sh.n_real_loc == 0
+    q, k, v, do = shard_inputs(sh)
+    o, lse, gq, gk, gv = _run_fwd_bwd(sp, sh, q, k, v, do)
+    for t in (o, gq, gk, gv):
+        assert torch.all(t.view(torch.int16) == 0)
+    assert bool(torch.all(torch.isneginf(lse)))
+
+
+def test_empty_inputs(sp):
+    """Zero query rows: a no-op forward and dK = dV = +0; zero keys: every row
+    gets O = +0 and LSE = -inf, dQ = +0, and a first ring step leaves the
+    accumulators at (0, -inf)."""
+    import torch
+    D, H = 128, 2
+    e = lambda *shape: torch.empty(shape, dtype=torch.bfloat16, device="cuda")  # noqa: E731
+    # no rows, 100 keys
+    sh = make_shard("no_rows", 0, 100, D, H, 0, H, H, 1, H, 0, [0], [100])
+    d = lib_desc(sh)
+    k, v = to_dev(randn_bf16_bits((100, H, D), 1)), to_dev(randn_bf16_bits((100, H, D), 2))
+    o, lse = sp.sp_attn_fwd(d, e(0, H, D), k, v)
+    assert o.numel() == 0 and lse.numel() == 0
+    dk, dv = torch.full_like(k, 1.0), torch.full_like(v, 1.0)
+    sp.sp_attn_bwd(d, e(0, H, D), k, v, o, lse, e(0, H, D), dq=e(0, H, D), dk=dk, dv=dv)
+    torch.cuda.synchronize()
+    assert torch.all(dk.view(torch.int16) == 0) and torch.all(dv.view(torch.int16) == 0)
+    # 50 rows, no keys
+    sh = make_shard("no_keys", 50, 0, D, H, 0, H, H, 1, H, 0, [50], [0])
+    d = lib_desc(sh)
+    q, do = to_dev(randn_bf16_bits((50, H, D), 3)), to_dev(randn_bf16_bits((50, H, D), 4))
+    o, lse = sp.sp_attn_fwd(d, q, e(0, H, D), e(0, H, D))
+    torch.cuda.synchronize()
+    assert torch.all(o.view(torch.int16) == 0) and bool(torch.all(torch.isneginf(lse)))
+    dq, _, _ = sp.sp_attn_bwd(d, q, e(0, H, D), e(0, H, D), o, lse, do)
+    torch.cuda.synchronize()
+    assert torch.all(dq.view(torch.int16) == 0)
+    o_acc = torch.full((50, H, D), 7.0, dtype=torch.float32, device="cuda")
+    lse_acc = torch.full((H, 50), 7.0, dtype=torch.float32, device="cuda")
+    sp.sp_ring_step(d, q, e(0, H, D), e(0, H, D), o_acc, lse_acc, init=True)
+    torch.cuda.synchronize()
+    assert torch.all(o_acc == 0) and bool(torch.all(torch.isneginf(lse_acc)))
