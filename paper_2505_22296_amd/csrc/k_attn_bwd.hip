@@ -153,6 +153,15 @@ __global__ __launch_bounds__(NTQ, 1) void attn_dq_kernel(DqArgs a) {
       if (kt >= wave_kmax) continue;  // wholly past this wavefront's rows
       const u32x4* stg = smem + u * STAGE;
 
+      // K and V fragments of the tile, all read before the first MFMA
+      u32x4 kfr[KS], vfr[KS];
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        const int fo = (ks >> 1) * SUB + ((ks & 1) ? kf1 : kf0);
+        kfr[ks] = stg[fo];
+        vfr[ks] = stg[S::OFF_V + fo];
+      }
+      __builtin_amdgcn_sched_barrier(0);
       f32x16 s, dp;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
@@ -162,11 +171,22 @@ __global__ __launch_bounds__(NTQ, 1) void attn_dq_kernel(DqArgs a) {
       __builtin_amdgcn_s_setprio(1);
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
-        const int fo = (ks >> 1) * SUB + ((ks & 1) ? kf1 : kf0);
-        s = mfma32(stg[fo], qf[ks], s);
-        dp = mfma32(stg[S::OFF_V + fo], df[ks], dp);
+        s = mfma32(kfr[ks], qf[ks], s);
+        dp = mfma32(vfr[ks], df[ks], dp);
       }
       __builtin_amdgcn_s_setprio(0);
+      // K^T fragments of the dQ product, read while dS is formed
+      const uint16_t* stg16 = (const uint16_t*)stg;
+      u32x4 ktr[DB * 2];
+#pragma unroll
+      for (int d = 0; d < DB; ++d)
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+          const int o = d * SUB * 8 + ks * 16 * 32;
+          const u32x2 lo = lds_tr16(stg16 + kt0 + o), hi = lds_tr16(stg16 + kt1 + o);
+          ktr[d * 2 + ks] = u32x4{lo[0], lo[1], hi[0], hi[1]};
+        }
+      __builtin_amdgcn_sched_barrier(0);
       const bool need_mask = (kt < k0) | (kt + BN > k1) | (a.causal & (kt + BN - 1 > q0 + w * 32 + delta));
       if (need_mask) {
 #pragma unroll
@@ -185,16 +205,10 @@ __global__ __launch_bounds__(NTQ, 1) void attn_dq_kernel(DqArgs a) {
       u32x4 b0 = pack_bf16x8(ds[0], ds[1], ds[2], ds[3], ds[4], ds[5], ds[6], ds[7]);
       u32x4 b1 = pack_bf16x8(ds[8], ds[9], ds[10], ds[11], ds[12], ds[13], ds[14], ds[15]);
       __builtin_amdgcn_s_setprio(1);
-      const uint16_t* stg16 = (const uint16_t*)stg;
 #pragma unroll
-      for (int d = 0; d < DB; ++d) {
+      for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
-        for (int ks = 0; ks < 2; ++ks) {
-          const int o = d * SUB * 8 + ks * 16 * 32;
-          const u32x2 lo = lds_tr16(stg16 + kt0 + o), hi = lds_tr16(stg16 + kt1 + o);
-          acc[d] = mfma32(u32x4{lo[0], lo[1], hi[0], hi[1]}, ks ? b1 : b0, acc[d]);
-        }
-      }
+        for (int d = 0; d < DB; ++d) acc[d] = mfma32(ktr[d * 2 + ks], ks ? b1 : b0, acc[d]);
       __builtin_amdgcn_s_setprio(0);
     }
   }
@@ -332,19 +346,30 @@ SP_DEV void dkdv_body(const DkdvArgs& a, u32x4* smem, int w, int lane) {
     const u32x4* stg = smem + st * STAGE;
     const uint16_t* stg16 = (const uint16_t*)stg;
     u32x4* xs = smem + st * S::XSLOT + xo;
+    // all A fragments of S = Q K^T (resp. dP = dO V^T) before the first MFMA
+    u32x4 afr[KS];
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) afr[ks] = stg[(ks >> 1) * SUB + ((ks & 1) ? af1 : af0)];
+    __builtin_amdgcn_sched_barrier(0);
     f32x16 s;
 #pragma unroll
     for (int r = 0; r < 16; ++r) s[r] = 0.f;
     __builtin_amdgcn_s_setprio(1);
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks)
-      s = mfma32(stg[(ks >> 1) * SUB + ((ks & 1) ? af1 : af0)], bf[ks], s);
+    for (int ks = 0; ks < KS; ++ks) s = mfma32(afr[ks], bf[ks], s);
     __builtin_amdgcn_s_setprio(0);
-    auto tr_frag = [&](int d, int ks) {
-      const int o = d * SUB * 8 + ks * 16 * 32;
-      const u32x2 lo = lds_tr16(stg16 + tr0 + o), hi = lds_tr16(stg16 + tr1 + o);
-      return u32x4{lo[0], lo[1], hi[0], hi[1]};
-    };
+    // transposed fragments of the dV (resp. dK) product, read while P / dS
+    // are formed
+    u32x4 tfr[DB * 2];
+#pragma unroll
+    for (int d = 0; d < DB; ++d)
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks) {
+        const int o = d * SUB * 8 + ks * 16 * 32;
+        const u32x2 lo = lds_tr16(stg16 + tr0 + o), hi = lds_tr16(stg16 + tr1 + o);
+        tfr[d * 2 + ks] = u32x4{lo[0], lo[1], hi[0], hi[1]};
+      }
+    __builtin_amdgcn_sched_barrier(0);
     const f32x4* vLD = (const f32x4*)(stg + S::OFF_LD) + (PWAVE ? 0 : BQ / 4);
     u32x4 pb[2];
     if constexpr (PWAVE) {
@@ -388,10 +413,9 @@ SP_DEV void dkdv_body(const DkdvArgs& a, u32x4* smem, int w, int lane) {
     }
     __builtin_amdgcn_s_setprio(1);
 #pragma unroll
-    for (int d = 0; d < DB; ++d) {
-      acc[d] = mfma32(tr_frag(d, 0), pb[0], acc[d]);
-      acc[d] = mfma32(tr_frag(d, 1), pb[1], acc[d]);
-    }
+    for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+      for (int d = 0; d < DB; ++d) acc[d] = mfma32(tfr[d * 2 + ks], pb[ks], acc[d]);
     __builtin_amdgcn_s_setprio(0);
   };
 
