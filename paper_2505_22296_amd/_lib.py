@@ -123,6 +123,13 @@ class Desc:
             return a.ctypes.data_as(_i32p)
 
         cq = np.asarray(cu_seqlens_q, dtype=np.int32)
+        # the C ABI reads these host arrays by the counts in the descriptor
+        if len(np.asarray(cu_seqlens_k)) != len(cq):
+            raise ValueError("cu_seqlens_q and cu_seqlens_k need the same length (num_seqs + 1)")
+        for name, pos, T in (("position_ids_q", position_ids_q, T_q),
+                             ("position_ids_k", position_ids_k, T_k)):
+            if pos is not None and len(np.asarray(pos)) < T:
+                raise ValueError(f"{name} has fewer than {T} entries")
         self.c = SpAttnDesc(
             T_q=T_q, T_k=T_k, head_dim=head_dim, H_loc=H_loc, head_offset=head_offset,
             num_real_heads=num_real_heads, num_padded_heads=num_padded_heads,

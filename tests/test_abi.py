@@ -36,6 +36,13 @@ def _ws_status(d, op=sp.SP_OP_FWD):
     return sp.load().sp_attn_workspace_size(d.ref, op, ctypes.byref(n)), n.value
 
 
+def test_binding_checks_host_array_lengths():
+    with pytest.raises(ValueError):
+        _good(cu_seqlens_k=[0, 256])
+    with pytest.raises(ValueError):
+        _good(position_ids_q=np.arange(100))
+
+
 def test_unknown_descriptor_flags_rejected():
     d = _good()
     d.c.flags = 2

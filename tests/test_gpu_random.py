@@ -1,0 +1,126 @@
+"""Seeded random descriptors through the C ABI against the fp64 oracle.
+
+Each seed draws one small problem from the descriptor space the library
+accepts: D in {64, 128}; real head count, SP size and rank (so dummy slots
+and all-dummy ranks occur); MHA or a GQA group (one or several local KV
+heads); causal or not; and one of three layouts -- packed segments of one
+batch (some empty, padding rows after the last), segments whose query and
+key positions start at different offsets (ring-style, T_q != T_k), or pieces
+of one sequence (positions strictly increasing over the pieces).  The bars
+are the parity bars of the fixed cases; dK/dV use the magnitude-scaled
+absolute bar because large GQA groups push them past 4."""
+import numpy as np
+import pytest
+
+import oracle
+from tests.helpers import (assert_close, bits_from_dev, from_dev, lib_desc, make_shard, oracle_kw,
+                           scaled_max_abs, to_dev, LSE_MAX_ABS)
+from workloads import padded_heads, shard_inputs
+
+pytestmark = pytest.mark.gpu
+SEEDS = list(range(64))
+
+
+@pytest.fixture(scope="module")
+def sp():
+    import torch
+    assert torch.cuda.is_available()
+    import paper_2505_22296_amd as m
+    m.load()
+    return m
+
+
+def random_shard(seed):
+    rng = np.random.default_rng(7000 + seed)
+    D = int(rng.choice([64, 128]))
+    hs = int(rng.integers(1, 13))
+    spn = int(rng.integers(1, 5))
+    hs_new = padded_heads(hs, spn)
+    H = hs_new // spn
+    off = int(rng.integers(0, spn)) * H
+    g = int(rng.choice([d for d in range(1, hs + 1) if hs % d == 0]))
+    real = [h for h in range(off, off + H) if h < hs]
+    if g == 1:
+        Hkv, kvo = H, off
+    elif real:
+        kvo = real[0] // g
+        Hkv = real[-1] // g + 1 - kvo
+    else:
+        kvo, Hkv = 0, 1
+    causal = bool(rng.random() < 0.8)
+    mode = ["segments", "offsets", "pieces"][seed % 3]
+    pos_q = pos_k = None
+    single = False
+    if mode == "segments":
+        lens = [int(x) for x in rng.integers(0, 130, int(rng.integers(1, 4)))]
+        T_q = T_k = sum(lens) + int(rng.integers(0, 20))
+        seg_q, seg_k = lens, None
+    elif mode == "offsets":
+        n = int(rng.integers(1, 3))
+        seg_q = [int(x) for x in rng.integers(1, 120, n)]
+        seg_k = [int(x) for x in rng.integers(1, 160, n)]
+        T_q, T_k = sum(seg_q) + int(rng.integers(0, 10)), sum(seg_k)
+        pos_q = np.zeros(T_q, np.int32)
+        pos_k = np.zeros(T_k, np.int32)
+        a = b = 0
+        for lq, lk in zip(seg_q, seg_k):
+            kb = int(rng.integers(0, 200))
+            qb = kb + int(rng.integers(-60, 120))
+            pos_q[a:a + lq] = qb + np.arange(lq)
+            pos_k[b:b + lk] = kb + np.arange(lk)
+            a, b = a + lq, b + lk
+    else:
+        single = True
+
+        n_pieces = int(rng.integers(1, 4))  # one count for both sides (num_seqs)
+
+        def pieces(n):
+            lens = [int(x) for x in rng.integers(1, 90, n)]
+            pos, start = [], int(rng.integers(0, 50))
+            for ln in lens:
+                pos.append(start + np.arange(ln))
+                start += ln + int(rng.integers(0, 100))
+            return lens, np.concatenate(pos).astype(np.int32)
+
+        seg_q, pos_q = pieces(n_pieces)
+        seg_k, pos_k = pieces(n_pieces)
+        T_q, T_k = sum(seg_q), sum(seg_k)
+    sh = make_shard(f"rand{seed}_{mode}", T_q, T_k, D, H, off, hs, hs_new, g, Hkv, kvo, seg_q,
+                    seg_k, pos_q=pos_q, pos_k=pos_k, causal=causal, seed_base=900 + 8 * seed,
+                    single_sequence=single)
+    return sh
+
+
+@pytest.mark.parametrize("seed", SEEDS)
+def test_random_shard_parity(sp, seed):
+    import torch
+    sh = random_shard(seed)
+    print(f"{sh.name}: T_q={sh.T_q} T_k={sh.T_k} D={sh.D} H_loc={sh.H_loc} off={sh.head_offset} "
+          f"real={sh.n_real_loc} g={sh.gqa_group} Hkv={sh.Hkv_loc} causal={sh.causal}", flush=True)
+    q, k, v, do = shard_inputs(sh)
+    d = lib_desc(sh)
+    Q, K, V, dO = (to_dev(x) for x in (q, k, v, do))
+    o, lse = sp.sp_attn_fwd(d, Q, K, V)
+    gq, gk, gv = sp.sp_attn_bwd(d, Q, K, V, o, lse, dO)
+    torch.cuda.synchronize()
+    qf, kf, vf, dof = (oracle.bf16_bits_to_f64(x) for x in (q, k, v, do))
+    kw = oracle_kw(sh)
+    RO, RL = oracle.attn_forward(qf, kf, vf, **kw)
+    RdQ, RdK, RdV = oracle.attn_backward(qf, kf, vf, dof, **kw)
+    nr = sh.n_real_loc
+    GL = lse.cpu().numpy().astype(np.float64)
+    if nr:
+        assert_close(from_dev(o)[:, :nr], RO[:, :nr], "O", max_abs=scaled_max_abs(RO[:, :nr]))
+        fin = np.isfinite(RL[:nr])
+        assert np.array_equal(np.isfinite(GL[:nr]), fin)
+        if fin.any():
+            assert np.abs(GL[:nr][fin] - RL[:nr][fin]).max() <= LSE_MAX_ABS
+        assert_close(from_dev(gq)[:, :nr], RdQ[:, :nr], "dQ", max_abs=scaled_max_abs(RdQ[:, :nr]))
+        none = ~np.isfinite(RL[0])
+        if none.any():
+            assert np.all(bits_from_dev(o)[none][:, :nr] == 0)
+    assert_close(from_dev(gk), RdK, "dK", max_abs=scaled_max_abs(RdK))
+    assert_close(from_dev(gv), RdV, "dV", max_abs=scaled_max_abs(RdV))
+    if nr < sh.H_loc:
+        assert np.all(bits_from_dev(o)[:, nr:] == 0) and np.all(bits_from_dev(gq)[:, nr:] == 0)
+        assert np.all(np.isneginf(GL[nr:]))
