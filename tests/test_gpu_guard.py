@@ -1,0 +1,159 @@
+"""Guard bands: every output buffer (and the attention workspace) is a slice
+of a larger allocation whose margins hold a canary pattern; after the call
+the margins must be unchanged, so no kernel writes outside what it was
+given.  Ragged shapes, padding rows, dummy slots, GQA partials, ring steps,
+pack / unpack / summing unpack, the merge and the loss path are covered."""
+import numpy as np
+import pytest
+
+from tests.helpers import lib_desc, make_shard, to_dev
+from tests.test_gpu_random import random_shard
+from workloads import (randn_bf16_bits, shard_inputs, ulysses_kv_head_map, ulysses_q_head_map)
+
+pytestmark = pytest.mark.gpu
+PAD = 4096  # elements of margin on each side (keeps 16-byte alignment)
+
+
+@pytest.fixture(scope="module")
+def sp():
+    import torch
+    assert torch.cuda.is_available()
+    import paper_2505_22296_amd as m
+    m.load()
+    return m
+
+
+class Guarded:
+    """A tensor of `shape` inside a canary-filled buffer."""
+
+    CANARY = {2: 0x7FC1, 4: 0x7FC00001, 1: 0xA5}
+
+    def __init__(self, shape, dtype):
+        import torch
+        n = int(np.prod(shape)) if len(shape) else 1
+        self.n = n
+        self.buf = torch.empty(n + 2 * PAD, dtype=dtype, device="cuda")
+        size = self.buf.element_size()
+        self.iview = self.buf.view({2: torch.int16, 4: torch.int32, 1: torch.uint8}[size])
+        c = self.CANARY[size]
+        if size == 2 and c > 0x7FFF:
+            c -= 0x10000
+        self.canary = c
+        self.iview.fill_(c)
+        self.t = self.buf[PAD:PAD + n].view(shape)
+
+    def intact(self):
+        lo = self.iview[:PAD]
+        hi = self.iview[PAD + self.n:]
+        return bool((lo == self.canary).all()) and bool((hi == self.canary).all())
+
+
+def _attn_guarded(sp, sh, dq_acc_mode=False):
+    import torch
+    bf, f32 = torch.bfloat16, torch.float32
+    q, k, v, do = shard_inputs(sh)
+    Q, K, V, dO = (to_dev(x) for x in (q, k, v, do))
+    d = lib_desc(sh)
+    D = sh.D
+    o = Guarded((sh.T_q, sh.H_loc, D), bf)
+    lse = Guarded((sh.H_loc, sh.T_q), f32)
+    wsf = Guarded((sp.sp_attn_workspace_size(d, sp.SP_OP_FWD),), torch.uint8)
+    sp.sp_attn_fwd(d, Q, K, V, o.t, lse.t, workspace=wsf.t)
+    dk = Guarded((sh.T_k, sh.Hkv_loc, D), bf)
+    dv = Guarded((sh.T_k, sh.Hkv_loc, D), bf)
+    wsb = Guarded((sp.sp_attn_workspace_size(d, sp.SP_OP_BWD),), torch.uint8)
+    if dq_acc_mode:
+        dq = Guarded((sh.T_q, sh.H_loc, D), f32)
+        dq.t.zero_()
+        sp.sp_attn_bwd(d, Q, K, V, o.t, lse.t, dO, dq_acc=dq.t, dk=dk.t, dv=dv.t, workspace=wsb.t)
+    else:
+        dq = Guarded((sh.T_q, sh.H_loc, D), bf)
+        sp.sp_attn_bwd(d, Q, K, V, o.t, lse.t, dO, dq=dq.t, dk=dk.t, dv=dv.t, workspace=wsb.t)
+    torch.cuda.synchronize()
+    for name, g in (("o", o), ("lse", lse), ("ws_fwd", wsf), ("dq", dq), ("dk", dk), ("dv", dv),
+                    ("ws_bwd", wsb)):
+        assert g.intact(), f"{sh.name}: write outside {name}"
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2, 4, 8, 9, 11, 13, 18, 20])
+def test_attention_guard_bands(sp, seed):
+    sh = random_shard(seed)
+    print(f"guard {sh.name}", flush=True)
+    _attn_guarded(sp, sh, dq_acc_mode=(seed % 2 == 1))
+
+
+def test_attention_guard_gqa_partials(sp):
+    # 333 ragged rows, padding rows, GQA group 4 across 2 KV heads (partial mode)
+    sh = make_shard("gqa_partials", 333, 333, 128, 8, 0, 8, 8, 4, 2, 0, [200, 100], seed_base=5)
+    _attn_guarded(sp, sh)
+
+
+def test_ring_step_guard_bands(sp):
+    import torch
+    sh = make_shard("ring", 150, 210, 64, 3, 0, 3, 3, 3, 1, 0, [150], [210],
+                    pos_q=300 + np.arange(150), pos_k=200 + np.arange(210))
+    q, k, v, _ = shard_inputs(sh)
+    d = lib_desc(sh)
+    oa = Guarded((150, 3, 64), torch.float32)
+    la = Guarded((3, 150), torch.float32)
+    ob = Guarded((150, 3, 64), torch.bfloat16)
+    ws = Guarded((sp.sp_attn_workspace_size(d, sp.SP_OP_RING_STEP),), torch.uint8)
+    sp.sp_ring_step(d, to_dev(q), to_dev(k), to_dev(v), oa.t, la.t, init=True, o_out=ob.t, workspace=ws.t)
+    sp.sp_ring_step(d, to_dev(q), to_dev(k), to_dev(v), oa.t, la.t, init=False, o_out=ob.t, workspace=ws.t)
+    torch.cuda.synchronize()
+    assert oa.intact() and la.intact() and ob.intact() and ws.intact()
+
+
+def test_data_movement_guard_bands(sp):
+    import torch
+    bf = torch.bfloat16
+    T, hs, spn, D = 333, 7, 4, 64
+    hm = ulysses_q_head_map(hs, spn)
+    H = len(hm) // spn
+    src = to_dev(randn_bf16_bits((T, hs, D), 1))
+    dst = Guarded((spn, T, H, D), bf)
+    sp.sp_ulysses_pack(src, spn, H, hm, dst=dst.t)
+    back = Guarded((T, hs, D), bf)
+    sp.sp_ulysses_unpack(dst.t, hm, hs, dst=back.t)
+    km = ulysses_kv_head_map(28, 4, 8)
+    kw = len(km) // 8
+    recv = to_dev(randn_bf16_bits((8, T, kw, 128), 2))
+    acc = Guarded((T, 4, 128), bf)
+    sp.sp_ulysses_unpack_add(recv, km, 4, dst=acc.t)
+    oa = Guarded((T, 3, 128), torch.float32)
+    la = Guarded((3, T), torch.float32)
+    ob = Guarded((T, 3, 128), bf)
+    oa.t.normal_()
+    la.t.normal_()
+    op = torch.randn((T, 3, 128), device="cuda").to(bf)
+    lp = torch.randn((3, T), device="cuda")
+    sp.sp_lse_merge(oa.t, la.t, op, lp, o_out=ob.t)
+    cv = Guarded((T * 3 * 128,), bf)
+    sp.sp_f32_to_bf16(oa.t.reshape(-1), cv.t)
+    torch.cuda.synchronize()
+    for name, g in (("pack", dst), ("unpack", back), ("unpack_add", acc), ("merge o", oa),
+                    ("merge lse", la), ("merge out", ob), ("f32_to_bf16", cv)):
+        assert g.intact(), f"write outside {name}"
+
+
+def test_loss_guard_bands(sp):
+    import torch
+    T, V = 37, 1000
+    x = to_dev(randn_bf16_bits((T, V), 3))
+    lab = torch.from_numpy(np.random.default_rng(1).integers(0, V, T).astype(np.int32)).cuda()
+    cu = np.array([2, 20, 33], np.int32)
+    lp = Guarded((T,), torch.float32)
+    ls = Guarded((T,), torch.float32)
+    ss = Guarded((2,), torch.float32)
+    sp.sp_token_logprob(x, lab, cu, logp=lp.t, lse=ls.t, seq_sum=ss.t)
+    parts = torch.stack([ss.t, ss.t])
+    loss = Guarded((1,), torch.float32)
+    grad = Guarded((2, 2), torch.float32)
+    sp.sp_loss_reduce(parts, sp.SP_LOSS_DPO, 0.1, ref_partial_sums=parts * 0.5, loss=loss.t,
+                      grad=grad.t)
+    dl = Guarded((T, V), torch.bfloat16)
+    sp.sp_token_logprob_bwd(x, lab, ls.t, cu, grad.t[0].contiguous(), dlogits=dl.t)
+    torch.cuda.synchronize()
+    for name, g in (("logp", lp), ("lse", ls), ("seq_sum", ss), ("loss", loss), ("grad", grad),
+                    ("dlogits", dl)):
+        assert g.intact(), f"write outside {name}"
