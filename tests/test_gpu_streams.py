@@ -108,3 +108,38 @@ def test_side_stream_runs_after_its_own_queue(sp):
     for k, r in ref.items():
         g = _bits(got[k])
         assert g.shape == r.shape and np.array_equal(g, r), f"{k} differs on the side stream"
+
+
+def test_concurrent_host_threads(sp):
+    """Two host threads run the whole path at once, each on its own stream
+    (the library holds no shared mutable state: schedules and uploads are
+    per call, the optional kernel timers per thread).  Each thread's outputs
+    match the single-threaded run bit for bit."""
+    import threading
+    import torch
+    sh, src = _sources()
+    ref = {k: _bits(v) for k, v in _path(sp, sh, src).items()}
+    torch.cuda.synchronize()
+    results, errors = [None, None], []
+
+    def worker(i):
+        try:
+            s = torch.cuda.Stream()
+            with torch.cuda.stream(s):
+                outs = [_path(sp, sh, src) for _ in range(3)]
+            s.synchronize()
+            results[i] = [{k: _bits(v) for k, v in o.items()} for o in outs]
+        except Exception as e:  # reported below
+            errors.append(repr(e))
+
+    threads = [threading.Thread(target=worker, args=(i,)) for i in range(2)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join(timeout=120)
+    assert not errors, errors
+    for i in range(2):
+        assert results[i] is not None, f"thread {i} did not finish"
+        for o in results[i]:
+            for k, r in ref.items():
+                assert np.array_equal(o[k], r), f"{k} differs in thread {i}"
