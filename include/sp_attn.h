@@ -35,6 +35,15 @@
  *   Threading   The library holds no state (apart from the opt-in per-thread
  *               kernel timer of sp_profile_events); calls are reentrant.  Calls
  *               that share a workspace must be ordered on one stream.
+ *   Graphs      The attention entry points (sp_attn_fwd, sp_ring_step,
+ *               sp_attn_bwd) copy their host-built work lists into the
+ *               workspace on every call; a HIP graph would replay that copy
+ *               from freed host memory, so on a stream that is being
+ *               captured they return SP_ERR_UNSUPPORTED (after argument and
+ *               workspace validation) and enqueue nothing.  Calls with no
+ *               query rows, which at most zero-fill outputs, are unaffected.
+ *               Every other entry point passes its host arrays by value in
+ *               the kernel arguments and may be recorded into a graph.
  *
  * Numerics: bf16 operands, float32 accumulation, float32 softmax statistics,
  * outputs rounded to bf16 with round-to-nearest-even.
@@ -52,7 +61,7 @@ extern "C" {
 typedef enum sp_status {
   SP_OK = 0,
   SP_ERR_INVALID_ARG = 1, /* inconsistent shapes, heads, segments, positions, pointers */
-  SP_ERR_UNSUPPORTED = 2, /* valid but not implemented (e.g. head_dim not 64/128) */
+  SP_ERR_UNSUPPORTED = 2, /* valid but not supported (head_dim not 64/128, a limit, a capturing stream) */
   SP_ERR_WORKSPACE = 3,   /* workspace missing, misaligned or too small */
   SP_ERR_HIP = 4          /* a HIP launch or copy failed */
 } sp_status;

@@ -303,6 +303,15 @@ sp_status upload(void* dst, const std::vector<int32_t>& v, hipStream_t st) {
   return SP_OK;
 }
 
+// The attention entry points upload host-built work lists on every call,
+// which a captured graph would replay from freed host memory: they refuse a
+// stream that is being captured.
+sp_status refuse_capture(hipStream_t st) {
+  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+  if (hipStreamIsCapturing(st, &cs) != hipSuccess) return SP_ERR_HIP;
+  return cs == hipStreamCaptureStatusNone ? SP_OK : SP_ERR_UNSUPPORTED;
+}
+
 sp_status check_ws(const Layout& L, void* ws, size_t ws_bytes) {
   if (!ws || ws_bytes < L.total || ((uintptr_t)ws & 255u) != 0) return SP_ERR_WORKSPACE;
   return SP_OK;
@@ -546,6 +555,7 @@ static sp_status fwd_common(const sp_attn_desc* d, const void* q, const void* k,
   Layout L = layout_for(d, p, ring ? SP_OP_RING_STEP : SP_OP_FWD, na, nb);
   if ((s = check_ws(L, ws, ws_bytes)) != SP_OK) return s;
   hipStream_t st = (hipStream_t)stream;
+  if ((s = refuse_capture(st)) != SP_OK) return s;
   const int n_items = (int)(items.size() / kItemInts);
   if (n_items > 0) {
     if ((s = upload(at(ws, L.items_dq), items, st)) != SP_OK) return s;
@@ -621,6 +631,7 @@ sp_status sp_attn_bwd(const sp_attn_desc* d, const void* q, const void* k, const
   Layout L = layout_for(d, p, SP_OP_BWD, na, nb);
   if ((s = check_ws(L, ws, ws_bytes)) != SP_OK) return s;
   hipStream_t st = (hipStream_t)stream;
+  if ((s = refuse_capture(st)) != SP_OK) return s;
   const int D = p.D;
   if (p.n_real > 0) {
     if ((s = upload(at(ws, L.items_dq), it_dq, st)) != SP_OK) return s;
