@@ -244,7 +244,7 @@ void schedule_keys(const sp_attn_desc* d, const Problem& p, int BNK, int BQ,
 
 // Workspace layout.
 struct Layout {
-  size_t items_dq = 0, items_kv = 0, delta = 0, lse2 = 0, part_k = 0, part_v = 0, total = 0;
+  size_t items_dq = 0, items_kv = 0, neg_d = 0, lse2 = 0, part_k = 0, part_v = 0, total = 0;
 };
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
@@ -264,7 +264,7 @@ Layout layout_for(const sp_attn_desc* d, const Problem& p, int op, size_t n_item
   } else {
     L.items_dq = take(n_items_a * kItemInts * 4);
     L.items_kv = take(n_items_b * kItemInts * 4);
-    L.delta = take((size_t)std::max(p.n_real, 1) * d->T_q * 4);
+    L.neg_d = take((size_t)std::max(p.n_real, 1) * d->T_q * 4);
     L.lse2 = take((size_t)std::max(p.n_real, 1) * d->T_q * 4);
     if (!p.direct) {
       L.part_k = take((size_t)p.n_real * d->T_k * D * 4);
@@ -636,14 +636,14 @@ sp_status sp_attn_bwd(const sp_attn_desc* d, const void* q, const void* k, const
   if (p.n_real > 0) {
     if ((s = upload(at(ws, L.items_dq), it_dq, st)) != SP_OK) return s;
     if ((s = upload(at(ws, L.items_kv), it_kv, st)) != SP_OK) return s;
-    float* delta = (float*)at(ws, L.delta);
+    float* neg_d = (float*)at(ws, L.neg_d);
     float* lse2 = (float*)at(ws, L.lse2);
-    SP_HIP(spk::launch_rowdot(o, dout, lse, delta, lse2, d->T_q, d->H_loc, p.n_real, D, st));
+    SP_HIP(spk::launch_rowdot(o, dout, lse, neg_d, lse2, d->T_q, d->H_loc, p.n_real, D, st));
     const float sl2 = d->softmax_scale * 1.4426950408889634f;
     spk::DqArgs a{};
     a.q = (const uint16_t*)q; a.k = (const uint16_t*)k; a.v = (const uint16_t*)v;
     a.dout = (const uint16_t*)dout;
-    a.lse = lse; a.delta = delta; a.dq = (uint16_t*)dq; a.dq_acc = dq_acc;
+    a.lse = lse; a.neg_d = neg_d; a.dq = (uint16_t*)dq; a.dq_acc = dq_acc;
     a.items = (const int32_t*)at(ws, L.items_dq);
     a.T_q = d->T_q; a.T_k = d->T_k; a.H = d->H_loc; a.Hkv = d->Hkv_loc;
     a.scale_log2 = sl2; a.scale = d->softmax_scale; a.causal = d->causal;
@@ -652,7 +652,7 @@ sp_status sp_attn_bwd(const sp_attn_desc* d, const void* q, const void* k, const
     spk::DkdvArgs b{};
     b.q = (const uint16_t*)q;
     b.dout = (const uint16_t*)dout;
-    b.lse2 = lse2; b.delta = delta; b.k = (const uint16_t*)k; b.v = (const uint16_t*)v;
+    b.lse2 = lse2; b.neg_d = neg_d; b.k = (const uint16_t*)k; b.v = (const uint16_t*)v;
     b.dk = (uint16_t*)dk; b.dv = (uint16_t*)dv;
     b.part_k = p.direct ? nullptr : (float*)at(ws, L.part_k);
     b.part_v = p.direct ? nullptr : (float*)at(ws, L.part_v);

@@ -1,6 +1,6 @@
 // Attention backward for one SP rank's real heads on gfx950 (deterministic:
 // no atomics).  P is recomputed from the forward's LSE; with
-// D_i = dO_i . O_i (precomputed per row):
+// D_i = dO_i . O_i (precomputed per row and stored negated):
 //   dP = dO V^T,  dS = P (dP - D),  dQ = scale dS K,
 //   dK = scale dS^T Q,  dV = P^T dO.
 //
@@ -85,7 +85,7 @@ __global__ __launch_bounds__(NTQ, 1) void attn_dq_kernel(DqArgs a) {
   }
   const float lse = a.lse[(int64_t)head * a.T_q + lrow];
   const float l2 = (lse == neg_inf()) ? __builtin_inff() : lse * kLog2e;
-  const float drow = a.delta[(int64_t)head * a.T_q + lrow];
+  const float ndrow = a.neg_d[(int64_t)head * a.T_q + lrow];
   const float c2 = a.scale_log2;
 
   f32x16 acc[DB];
@@ -200,7 +200,7 @@ __global__ __launch_bounds__(NTQ, 1) void attn_dq_kernel(DqArgs a) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[r], c2, -l2));
-        ds[r] = p * (dp[r] - drow);
+        ds[r] = p * (dp[r] + ndrow);
       }
       u32x4 b0 = pack_bf16x8(ds[0], ds[1], ds[2], ds[3], ds[4], ds[5], ds[6], ds[7]);
       u32x4 b1 = pack_bf16x8(ds[8], ds[9], ds[10], ds[11], ds[12], ds[13], ds[14], ds[15]);
@@ -287,7 +287,7 @@ SP_DEV void dkdv_body(const DkdvArgs& a, u32x4* smem, int w, int lane) {
   const uint16_t* qh = a.q + (int64_t)head * D;
   const uint16_t* oh = a.dout + (int64_t)head * D;
   const float* lh = a.lse2 + (int64_t)head * a.T_q;
-  const float* dh = a.delta + (int64_t)head * a.T_q;
+  const float* dh = a.neg_d + (int64_t)head * a.T_q;
   const int wave_qmin = wk0 >= k1 ? 0x7fffffff : a.causal ? wk0 - delta - BQ + 1 : -0x7fffffff;
 
   // DMA: blocks w + 8j of each chunk's Q / dO tiles (kinds wave-uniform)
@@ -350,10 +350,25 @@ SP_DEV void dkdv_body(const DkdvArgs& a, u32x4* smem, int w, int lane) {
     u32x4 afr[KS];
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) afr[ks] = stg[(ks >> 1) * SUB + ((ks & 1) ? af1 : af0)];
-    __builtin_amdgcn_sched_barrier(0);
+    // per-row statistic of the lane's 16 C rows: L (P-wavefront) or -D
+    const f32x4* vLD = (const f32x4*)(stg + S::OFF_LD) + (PWAVE ? 0 : BQ / 4);
     f32x16 s;
+    if constexpr (PWAVE) {
 #pragma unroll
-    for (int r = 0; r < 16; ++r) s[r] = 0.f;
+      for (int r = 0; r < 16; ++r) s[r] = 0.f;
+    } else {
+      // dP starts from -D of its row, so the MFMAs leave dP - D
+#pragma unroll
+      for (int half = 0; half < 2; ++half) {
+        const f32x4 x = vLD[half * 4 + hh * 2], y = vLD[half * 4 + hh * 2 + 1];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          s[half * 8 + i] = x[i];
+          s[half * 8 + 4 + i] = y[i];
+        }
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);
     __builtin_amdgcn_s_setprio(1);
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) s = mfma32(afr[ks], bf[ks], s);
@@ -370,7 +385,6 @@ SP_DEV void dkdv_body(const DkdvArgs& a, u32x4* smem, int w, int lane) {
         tfr[d * 2 + ks] = u32x4{lo[0], lo[1], hi[0], hi[1]};
       }
     __builtin_amdgcn_sched_barrier(0);
-    const f32x4* vLD = (const f32x4*)(stg + S::OFF_LD) + (PWAVE ? 0 : BQ / 4);
     u32x4 pb[2];
     if constexpr (PWAVE) {
       // S -> masked -> P; P to the partner (fp16) and into dV (bf16)
@@ -399,15 +413,13 @@ SP_DEV void dkdv_body(const DkdvArgs& a, u32x4* smem, int w, int lane) {
         xs[half * 64] = __builtin_bit_cast(u32x4, __builtin_convertvector(p, f16x8));
       }
     } else {
-      // dP (in s) and the partner's P -> dS
+      // dP - D (in s) and the partner's P -> dS
 #pragma unroll
       for (int half = 0; half < 2; ++half) {
-        const f32x4 Da = vLD[half * 4 + hh * 2], Db = vLD[half * 4 + hh * 2 + 1];
-        const float Dr[8] = {Da[0], Da[1], Da[2], Da[3], Db[0], Db[1], Db[2], Db[3]};
         const f32x8 p = __builtin_convertvector(__builtin_bit_cast(f16x8, xs[half * 64]), f32x8);
         f32x8 ds;
 #pragma unroll
-        for (int i = 0; i < 8; ++i) ds[i] = p[i] * (s[half * 8 + i] - Dr[i]);
+        for (int i = 0; i < 8; ++i) ds[i] = p[i] * s[half * 8 + i];
         pb[half] = __builtin_bit_cast(u32x4, __builtin_convertvector(ds, bf16x8));
       }
     }

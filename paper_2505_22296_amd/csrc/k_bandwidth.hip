@@ -277,13 +277,14 @@ hipError_t launch_f32_to_bf16(const float* s, void* d, int64_t n, hipStream_t st
 }
 
 // ---------------------------------------------------------------- row dot
-// delta[y][t] = sum_d dO[t][y][d] * O[t][y][d]  (float32), y < nh, t < T;
+// neg_d[y][t] = -sum_d dO[t][y][d] * O[t][y][d]  (float32, -D of the
+// backward), y < nh, t < T;
 // lse2[y][t] = LSE[y][t] * log2(e) (+inf where LSE = -inf: rows without keys).
 template <int D>
 __global__ __launch_bounds__(kBlock) void rowdot_kernel(const uint16_t* __restrict__ o,
                                                         const uint16_t* __restrict__ dout,
                                                         const float* __restrict__ lse,
-                                                        float* __restrict__ delta,
+                                                        float* __restrict__ neg_d,
                                                         float* __restrict__ lse2, int T, int H,
                                                         int nh) {
   constexpr int NC = D / 8;  // lanes per row
@@ -307,23 +308,23 @@ __global__ __launch_bounds__(kBlock) void rowdot_kernel(const uint16_t* __restri
   for (int m = NC / 2; m >= 1; m >>= 1) s += __shfl_xor(s, m);
   if (row < rows && c == 0) {
     const int64_t i = (int64_t)y * T + t;
-    delta[i] = s;
+    neg_d[i] = -s;
     const float l = lse[i];
     lse2[i] = (l == neg_inf()) ? __builtin_inff() : l * kLog2e;
   }
 }
 
-hipError_t launch_rowdot(const void* o, const void* dout, const float* lse, float* delta,
+hipError_t launch_rowdot(const void* o, const void* dout, const float* lse, float* neg_d,
                          float* lse2, int T, int H, int nh, int D, hipStream_t st) {
   int64_t n = (int64_t)T * nh * (D / 8);
   if (n == 0) return hipSuccess;
   int grid = (int)((n + kBlock - 1) / kBlock);
   if (D == 128)
     hipLaunchKernelGGL(rowdot_kernel<128>, dim3(grid), dim3(kBlock), 0, st, (const uint16_t*)o,
-                       (const uint16_t*)dout, lse, delta, lse2, T, H, nh);
+                       (const uint16_t*)dout, lse, neg_d, lse2, T, H, nh);
   else
     hipLaunchKernelGGL(rowdot_kernel<64>, dim3(grid), dim3(kBlock), 0, st, (const uint16_t*)o,
-                       (const uint16_t*)dout, lse, delta, lse2, T, H, nh);
+                       (const uint16_t*)dout, lse, neg_d, lse2, T, H, nh);
   return hipGetLastError();
 }
 

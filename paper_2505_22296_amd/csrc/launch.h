@@ -101,7 +101,7 @@ struct DqArgs {
   const uint16_t* v;     // [T_k, Hkv, D]
   const uint16_t* dout;  // [T_q, H, D]
   const float* lse;      // [H, T_q]
-  const float* delta;    // [n_real, T_q]
+  const float* neg_d;    // -D = -(dO . O) per row: [n_real, T_q]
   uint16_t* dq;          // bf16 [T_q, H, D] or null
   float* dq_acc;         // float32 [T_q, H, D] (+=) or null
   const int32_t* items;
@@ -114,7 +114,7 @@ struct DkdvArgs {
   const uint16_t* q;     // [T_q, H, D]
   const uint16_t* dout;  // [T_q, H, D]
   const float* lse2;     // [n_real, T_q]: LSE * log2(e), +inf for rows without keys
-  const float* delta;    // [n_real, T_q]
+  const float* neg_d;    // -D = -(dO . O) per row: [n_real, T_q]
   const uint16_t* k;     // [T_k, Hkv, D]
   const uint16_t* v;     // [T_k, Hkv, D]
   uint16_t* dk;          // bf16 [T_k, Hkv, D] (direct mode)
@@ -143,7 +143,7 @@ hipError_t launch_zero_heads_bf16(void* x, int T, int H, int D, int h0, int h1, 
 hipError_t launch_zero_heads_f32(float* x, int T, int H, int D, int h0, int h1, hipStream_t st);
 hipError_t launch_fill_f32(float* x, int64_t n, float v, hipStream_t st);
 hipError_t launch_f32_to_bf16(const float* s, void* d, int64_t n, hipStream_t st);
-hipError_t launch_rowdot(const void* o, const void* dout, const float* lse, float* delta,
+hipError_t launch_rowdot(const void* o, const void* dout, const float* lse, float* neg_d,
                          float* lse2, int T, int H, int nh, int D, hipStream_t st);
 hipError_t launch_reduce_kv(const float* part, void* out, const ReduceArgs& a, hipStream_t st);
 
