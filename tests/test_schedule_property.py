@@ -1,0 +1,99 @@
+"""Property test of the block-skip scheduler (host only, no GPU): for random
+valid descriptors -- packed segments of random lengths (empty ones
+included) with random position bases (neat packing, Section 3.2; ring-style
+offsets, Section 2.1), pieces of one sequence (zigzag chunks), causal or
+not, padding rows and keys, GQA groups and dummy head slots (Section 4.1)
+-- the forward and dK/dV work lists cover every allowed (row, key) pair of
+every real head exactly once and no other pair, tile every row (key) of a
+real head exactly once, name no dummy slot, and come longest first.  The
+allowed set is the oracle's mask."""
+import numpy as np
+import pytest
+from hypothesis import HealthCheck, given, settings, strategies as st
+
+import oracle.attention as A
+import paper_2505_22296_amd as sp
+from tests.helpers import lib_desc, make_shard, oracle_kw
+from tests.test_abi import _coverage_from_schedule
+
+
+@st.composite
+def shards(draw):
+    n = draw(st.integers(0, 6))
+    single = n >= 1 and draw(st.booleans())
+    causal = draw(st.booleans())
+    lq = draw(st.lists(st.integers(0, 70), min_size=n, max_size=n))
+    same = not single and draw(st.booleans())
+    lk = list(lq) if same else draw(st.lists(st.integers(0, 70), min_size=n, max_size=n))
+    T_q = sum(lq) + draw(st.integers(0, 20))
+    T_k = sum(lk) + draw(st.integers(0, 20))
+
+    def positions(lens, T):
+        pos = np.zeros(T, np.int64)
+        at, nxt = 0, draw(st.integers(0, 50))
+        for ln in lens:
+            base = nxt + draw(st.integers(0, 40)) if single else draw(st.integers(0, 300))
+            pos[at:at + ln] = base + np.arange(ln)
+            at += ln
+            nxt = base + ln
+        if single:  # padding after the pieces keeps rising
+            pos[at:] = nxt + np.arange(T - at)
+        return pos.astype(np.int32)
+
+    pos_q, pos_k = positions(lq, T_q), positions(lk, T_k)
+    spn = draw(st.sampled_from([1, 2, 4]))
+    H = draw(st.integers(1, 4))
+    padded = spn * H
+    g = draw(st.sampled_from([1, 2, 3, 4]))
+    reals = [r for r in range(max(1, padded - spn + 1), padded + 1) if r % g == 0]
+    if not reals:
+        g = 1
+        reals = list(range(max(1, padded - spn + 1), padded + 1))
+    real = draw(st.sampled_from(reals))
+    rank = draw(st.integers(0, spn - 1))
+    off = rank * H
+    if off < real:
+        last = min(off + H, real) - 1
+        kv_off, Hkv = off // g, last // g - off // g + 1
+    else:  # an all-dummy rank
+        kv_off, Hkv = 0, 1
+    D = draw(st.sampled_from([64, 128]))
+    return make_shard("prop", T_q, T_k, D, H, off, real, padded, g, Hkv, kv_off, lq, lk,
+                      pos_q=pos_q, pos_k=pos_k, causal=causal, single_sequence=single)
+
+
+@settings(max_examples=200, deadline=None, derandomize=True,
+          suppress_health_check=[HealthCheck.too_slow, HealthCheck.data_too_large])
+@given(shards())
+def test_schedule_matches_the_mask(sh):
+    d = lib_desc(sh)
+    kw = oracle_kw(sh)
+    # (pieces of one sequence are one segment to the oracle)
+    seg_q, seg_k = A.segment_ids(kw["cu_q"], sh.T_q), A.segment_ids(kw["cu_k"], sh.T_k)
+    mask = A.allowed_mask(np.arange(sh.T_q), seg_q, seg_k, sh.pos_q, sh.pos_k, sh.causal)
+    real = [h for h in range(sh.H_loc) if sh.head_offset + h < sh.num_real_heads]
+    for op, kind in ((sp.SP_OP_FWD, "rows"), (sp.SP_OP_BWD, "keys")):
+        items = sp.sp_attn_schedule(d, op)
+        assert set(int(h) for h in items[:, 5]) <= set(real)
+        if sh.T_q > 0 and sh.T_k > 0 and mask.any():
+            assert set(int(h) for h in items[:, 5]) == set(real)
+        for it in items:
+            assert it[6] == sh.kv_of(int(it[5]))
+        cov = _coverage_from_schedule(sh, items, kind)
+        for h in real:
+            got = cov.get(h, np.zeros((sh.T_q, sh.T_k), np.int32))
+            assert np.array_equal(got, mask.astype(np.int32)), (op, h)
+        # every row (forward) / key (dK/dV) of a real head tiled at most once,
+        # and the forward tiles every row once (its O / LSE get written)
+        n_ax = sh.T_q if kind == "rows" else sh.T_k
+        for h in real:
+            cnt = np.zeros(n_ax, np.int32)
+            for it in items[items[:, 5] == h]:
+                cnt[it[0]:it[1]] += 1
+            assert cnt.max(initial=0) <= 1, (op, h)
+            if kind == "rows":
+                assert np.all(cnt == 1), (op, h)
+        a, b, step = (2, 3, 64) if kind == "rows" else (2, 3, 32)
+        cost = np.array([-(-(int(it[b]) - (int(it[a]) & ~7)) // step) if it[b] > it[a] else 0
+                         for it in items])
+        assert np.all(np.diff(cost) <= 0), (op, cost[:20])
