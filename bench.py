@@ -58,6 +58,7 @@ class KernelTimers:
     def __init__(self, sp, torch):
         self.sp, self.torch = sp, torch
         self.pool, self.used, self.on = [], [], False
+        self.only = None  # set of kernel ids to time (None: every kernel)
 
     def reserve(self, n):
         """Create (and record once) n event pairs ahead of the timed region."""
@@ -69,7 +70,7 @@ class KernelTimers:
             self.pool.append((a, b))
 
     def arm(self, kid, flops):
-        if not self.on:
+        if not self.on or (self.only is not None and kid not in self.only):
             return
         self.reserve(len(self.used) + 1)
         pair = self.pool[len(self.used)]
@@ -304,7 +305,12 @@ def cpu_baseline(sh, budget_s=15.0):
             "seconds": round(dt, 2)}
 
 
-def measure(sp, torch, name, steps, warmup, per_kernel=True, warmup_s=1.5):
+def measure(sp, torch, name, steps, warmup, per_kernel=True, warmup_s=1.5, kernel_steps=10):
+    """Times `steps` steps after a warmup.  Returns the step time, the
+    dominant kernel's event timings over the timed steps (the warmup names
+    the dominant kernel; only its launches carry events in the timed region,
+    since every event pair adds ~11 us to a step), and every kernel's
+    timings from `kernel_steps` further, untimed steps."""
     sh = workload(name)
     timers = KernelTimers(sp, torch)
     st = Step(sp, torch, sh, timers)
@@ -327,8 +333,12 @@ def measure(sp, torch, name, steps, warmup, per_kernel=True, warmup_s=1.5):
         n_w += 1
         if n_w % 4 == 0:
             torch.cuda.synchronize()
-    timers.used = []
     torch.cuda.synchronize()
+    warm = timers.summary()
+    dom = max(warm, key=lambda k: warm[k]["ms"]) if warm else None
+    timers.used = []
+    timers.disarm()
+    timers.only = {dom} if dom is not None else set()
     t0 = time.perf_counter()
     for i in range(steps):
         marks[i].record()
@@ -336,11 +346,20 @@ def measure(sp, torch, name, steps, warmup, per_kernel=True, warmup_s=1.5):
     marks[steps].record()
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
+    ks_dom = timers.summary()
+    # every kernel, from further untimed steps
+    timers.used = []
+    timers.disarm()
+    timers.only = None
+    for _ in range(kernel_steps if per_kernel else 0):
+        st.run()
+    torch.cuda.synchronize()
+    ks_all = timers.summary()
     timers.on = False
     timers.disarm()
     ms = dt * 1e3 / steps
     per_step = sorted(marks[i].elapsed_time(marks[i + 1]) for i in range(steps))
-    return sh, st, ms, timers.summary(), per_step
+    return sh, st, ms, ks_dom, ks_all, per_step
 
 
 def measured_traffic(kernel, workload_name):
@@ -508,18 +527,20 @@ def main():
         return
     names = WORKLOADS if args.all else [args.workload]
     for name in names:
-        sh, st, ms, ks, per_step = measure(sp, torch, name, args.steps, args.warmup,
-                                           warmup_s=args.warmup_seconds)
+        kernel_steps = 10
+        sh, st, ms, ks_dom, ks, per_step = measure(sp, torch, name, args.steps, args.warmup,
+                                                   warmup_s=args.warmup_seconds,
+                                                   kernel_steps=kernel_steps)
         value = st.flops_metric / (ms * 1e-3) / 1e12
-        # dominant kernel: most time per step
-        dom = max(ks.items(), key=lambda kv: kv[1]["ms"]) if ks else None
+        # dominant kernel (most time per step), timed over the timed steps
+        dom = max(ks_dom.items(), key=lambda kv: kv[1]["ms"]) if ks_dom else None
         roof = None
         kern = {}
         for kid, s in ks.items():
             avg = s["ms"] / s["n"]
             med = sorted(s["all"])[len(s["all"]) // 2]
             kern[KNAMES[kid]] = {"avg_ms": round(avg, 4), "median_ms": round(med, 4),
-                                 "launches_per_step": s["n"] / args.steps,
+                                 "launches_per_step": s["n"] / kernel_steps,
                                  "tflops": round(s["flops"] / s["n"] / (avg * 1e-3) / 1e12, 1)
                                  if s["flops"] else None,
                                  "tflops_at_median": round(s["flops"] / s["n"] / (med * 1e-3) / 1e12, 1)
@@ -551,7 +572,9 @@ def main():
             "ms_per_step_median": round(per_step[len(per_step) // 2], 4),
             "ms_per_step_min": round(per_step[0], 4),
             "tflops_at_median_step": round(st.flops_metric / (per_step[len(per_step) // 2] * 1e-3) / 1e12, 2),
+            # every kernel, from further untimed steps with all kernels timed
             "kernels": kern,
+            "kernels_steps": kernel_steps,
             "roofline": roof,
         }
         if args.dummy_overhead and sh.n_real_loc < sh.H_loc:
