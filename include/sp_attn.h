@@ -96,6 +96,11 @@ enum { SP_OP_FWD = 0, SP_OP_BWD = 1, SP_OP_RING_STEP = 2 };
  * segment's first position matters, so ring chunks express their global
  * offsets here (Q chunk r at r*C.., KV chunk c at c*C..).  NULL means
  * positions 0,1,.. restarting at every segment.
+ *
+ * Limits.  T_q, T_k < 2^30 and, per segment, |(first key position - first
+ * key index) - (first query position - first query index)| <= 2^30
+ * (SP_ERR_INVALID_ARG beyond); Hkv_loc <= 64 and H_loc <= 4096
+ * (SP_ERR_UNSUPPORTED beyond).
  */
 /*
  * SP_DESC_SINGLE_SEQUENCE: the num_seqs segments on each side are PIECES of
