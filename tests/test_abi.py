@@ -102,6 +102,10 @@ def test_entry_points_reject_before_launch():
     # merge: head_dim must be a power of two in [8, 512]
     assert lib.sp_lse_merge(fake, fake, fake, 1, fake, 4, 2, 96, None, None) == sp.SP_ERR_INVALID_ARG
     assert lib.sp_f32_to_bf16(fake, fake, -1, None) == sp.SP_ERR_INVALID_ARG
+    # kernel timer: ids outside the enum are rejected (arming nothing)
+    for bad in (0, -1, 99):
+        assert lib.sp_profile_events(bad, None, None) == sp.SP_ERR_INVALID_ARG
+    assert lib.sp_profile_events(sp.SP_KERNEL_ATTN_FWD, None, None) == sp.SP_OK
 
 
 def test_pack_unpack_validation():
