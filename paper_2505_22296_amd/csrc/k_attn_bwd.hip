@@ -369,10 +369,8 @@ SP_DEV void dkdv_body(const DkdvArgs& a, u32x4* smem, int w, int lane) {
       }
     }
     __builtin_amdgcn_sched_barrier(0);
-    __builtin_amdgcn_s_setprio(1);
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) s = mfma32(afr[ks], bf[ks], s);
-    __builtin_amdgcn_s_setprio(0);
     // transposed fragments of the dV (resp. dK) product, read while P / dS
     // are formed
     u32x4 tfr[DB * 2];
@@ -423,12 +421,10 @@ SP_DEV void dkdv_body(const DkdvArgs& a, u32x4* smem, int w, int lane) {
         pb[half] = __builtin_bit_cast(u32x4, __builtin_convertvector(ds, bf16x8));
       }
     }
-    __builtin_amdgcn_s_setprio(1);
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
       for (int d = 0; d < DB; ++d) acc[d] = mfma32(tfr[d * 2 + ks], pb[ks], acc[d]);
-    __builtin_amdgcn_s_setprio(0);
   };
 
   constexpr int NGS = NSTF / TPBF;  // groups per stage cycle

@@ -172,12 +172,10 @@ __global__ __launch_bounds__(NT, 1) void attn_fwd_kernel(FwdArgs a) {
       for (int g = 0; g < 2; ++g)
 #pragma unroll
         for (int r = 0; r < 16; ++r) s[g][r] = 0.f;
-      __builtin_amdgcn_s_setprio(1);
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
         for (int g = 0; g < 2; ++g) s[g] = mfma32(kfr[g * KS + ks], qf[ks], s[g]);
-      __builtin_amdgcn_s_setprio(0);
       // V^T fragments of this tile, read while the softmax runs
       const uint16_t* stg16 = (const uint16_t*)stg;
       u32x4 vfr[DB * 4];
@@ -244,12 +242,10 @@ __global__ __launch_bounds__(NT, 1) void attn_fwd_kernel(FwdArgs a) {
       l_part += (ps[0] + ps[1]) + (ps[2] + ps[3]);
 
       // ---- O^T += V^T P^T
-      __builtin_amdgcn_s_setprio(1);
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks)
 #pragma unroll
         for (int d = 0; d < DB; ++d) oacc[d] = mfma32(vfr[d * 4 + ks], pb[ks], oacc[d]);
-      __builtin_amdgcn_s_setprio(0);
     }
   }
 
