@@ -346,7 +346,8 @@ SP_DEV void dkdv_body(const DkdvArgs& a, u32x4* smem, int w, int lane) {
     const u32x4* stg = smem + st * STAGE;
     const uint16_t* stg16 = (const uint16_t*)stg;
     u32x4* xs = smem + st * S::XSLOT + xo;
-    // all A fragments of S = Q K^T (resp. dP = dO V^T) before the first MFMA
+    // A fragments of S = Q K^T (resp. dP = dO V^T), issued ahead of the
+    // MFMAs, which the compiler places among them
     u32x4 afr[KS];
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) afr[ks] = stg[(ks >> 1) * SUB + ((ks & 1) ? af1 : af0)];
@@ -368,7 +369,6 @@ SP_DEV void dkdv_body(const DkdvArgs& a, u32x4* smem, int w, int lane) {
         }
       }
     }
-    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) s = mfma32(afr[ks], bf[ks], s);
     // transposed fragments of the dV (resp. dK) product, read while P / dS
@@ -382,7 +382,6 @@ SP_DEV void dkdv_body(const DkdvArgs& a, u32x4* smem, int w, int lane) {
         const u32x2 lo = lds_tr16(stg16 + tr0 + o), hi = lds_tr16(stg16 + tr1 + o);
         tfr[d * 2 + ks] = u32x4{lo[0], lo[1], hi[0], hi[1]};
       }
-    __builtin_amdgcn_sched_barrier(0);
     u32x4 pb[2];
     if constexpr (PWAVE) {
       // S -> masked -> P; P to the partner (fp16) and into dV (bf16)

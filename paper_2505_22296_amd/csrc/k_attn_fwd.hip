@@ -157,16 +157,16 @@ __global__ __launch_bounds__(NT, 1) void attn_fwd_kernel(FwdArgs a) {
       }
       const u32x4* stg = smem + u * STAGE;
 
-      // ---- S^T = K Q^T for the two 32-key halves of the tile.  All K
-      // fragments are read before the first MFMA, so the LDS latency is
-      // paid once per tile instead of once per MFMA.
+      // ---- S^T = K Q^T for the two 32-key halves of the tile.  The K
+      // fragment reads are issued together ahead of the MFMAs; the compiler
+      // places the MFMAs among them (measured faster than holding every
+      // MFMA behind the last read).
       u32x4 kfr[2 * KS];
 #pragma unroll
       for (int g = 0; g < 2; ++g)
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks)
           kfr[g * KS + ks] = stg[(ks >> 1) * SUB + g * 128 + ((ks & 1) ? kf1 : kf0)];
-      __builtin_amdgcn_sched_barrier(0);
       f32x16 s[2];
 #pragma unroll
       for (int g = 0; g < 2; ++g)
