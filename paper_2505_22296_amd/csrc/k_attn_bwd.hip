@@ -313,8 +313,10 @@ SP_DEV void dkdv_body(const DkdvArgs& a, u32x4* smem, int w, int lane) {
       if (tail) o += (min(qc + row_of[j], Tq1) - qc - row_of[j]) * hstride;
       dma16((k == 1 ? oh : qh) + (int64_t)qc * hstride + o, k == 2 ? smem + S::JUNK : stg + b * 64);
     }
-    const int rr = min(qc + (lane & (BQ - 1)), Tq1);
-    dma4((lane < BQ ? lh : dh) + rr, stg + S::OFF_LD);
+    if (w == 0) {  // the chunk's L and -D rows: one copy is enough
+      const int rr = min(qc + (lane & (BQ - 1)), Tq1);
+      dma4((lane < BQ ? lh : dh) + rr, stg + S::OFF_LD);
+    }
   };
 
   // B operands: K rows (P-wavefront) or V rows (dS-wavefront) of this pair's keys
