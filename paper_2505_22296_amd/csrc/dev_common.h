@@ -144,6 +144,13 @@ SP_DEV void dma16(const void* gsrc, void* lds_block) {
   asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
                :: "v"(gsrc), "s"(lds_addr(lds_block)) : "memory", "m0");
 }
+// The same 16-byte copy from a wavefront-uniform base (SGPR pair) plus a
+// per-lane 32-bit byte offset (global saddr addressing): a tile's base moves
+// with scalar arithmetic and the lane offsets stay fixed from tile to tile.
+SP_DEV void dma16s(const void* sbase, uint32_t voff, void* lds_block) {
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1"
+               :: "v"(voff), "s"(sbase), "s"(lds_addr(lds_block)) : "memory", "m0");
+}
 SP_DEV void dma4(const void* gsrc, void* lds_block) {
   asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dword %0, off"
                :: "v"(gsrc), "s"(lds_addr(lds_block)) : "memory", "m0");

@@ -109,7 +109,7 @@ __global__ __launch_bounds__(NTQ, 1) void attn_dq_kernel(DqArgs a) {
     const int t = (k == 1 ? b - S::RB : k == 0 ? b : 0) * 64 + lane;
     const int ts = t % SUB, r = ts / 4;
     key_of[j] = r;
-    off[j] = r * kstride + (t / SUB) * 32 + blk_chunk(r, ts % 4) * 8;
+    off[j] = 2 * (r * kstride + (t / SUB) * 32 + blk_chunk(r, ts % 4) * 8);  // bytes
   }
   const uint16_t* kbase = a.k + (int64_t)kvh * D;
   const uint16_t* vbase = a.v + (int64_t)kvh * D;
@@ -117,14 +117,18 @@ __global__ __launch_bounds__(NTQ, 1) void attn_dq_kernel(DqArgs a) {
     const int kt = kt_first + n * BN;
     u32x4* stg = smem + (n % NSTQ) * STAGE;
     const int64_t rowoff = (int64_t)kt * kstride;
-    const bool tail = kt + BN > k1;  // keys past k1 (masked) are clamped to k1-1
-#pragma unroll
-    for (int j = 0; j < NBW; ++j) {
+    auto copy = [&](int j, int o) {
       const int b = w + NWQ * j;
       const int k = S::kind(b);
-      int o = off[j];
-      if (tail) o += (min(kt + key_of[j], k1 - 1) - kt - key_of[j]) * kstride;
-      dma16((k == 1 ? vbase : kbase) + rowoff + o, k == 2 ? smem + S::JUNK : stg + b * 64);
+      dma16s((k == 1 ? vbase : kbase) + rowoff, o, k == 2 ? smem + S::JUNK : stg + b * 64);
+    };
+    if (kt + BN <= k1) {
+#pragma unroll
+      for (int j = 0; j < NBW; ++j) copy(j, off[j]);
+    } else {  // keys past k1 (masked) are clamped to k1-1
+#pragma unroll
+      for (int j = 0; j < NBW; ++j)
+        copy(j, off[j] + 2 * (min(kt + key_of[j], k1 - 1) - kt - key_of[j]) * kstride);
     }
   };
   // lane-constant LDS offsets of the fragments (see the forward kernel)
@@ -299,19 +303,24 @@ SP_DEV void dkdv_body(const DkdvArgs& a, u32x4* smem, int w, int lane) {
     const int t = (k == 1 ? b - S::RB : k == 0 ? b : 0) * 64 + lane;
     const int ts = t % SUB, r = ts / 4;
     row_of[j] = r;
-    off[j] = r * hstride + (t / SUB) * 32 + blk_chunk(r, ts % 4) * 8;
+    off[j] = 2 * (r * hstride + (t / SUB) * 32 + blk_chunk(r, ts % 4) * 8);  // bytes
   }
   auto issue = [&](int c) {
     const int qc = qc_last - c * BQ;
     u32x4* stg = smem + (c % NSTF) * STAGE;
     const bool tail = qc + BQ > a.T_q;
-#pragma unroll
-    for (int j = 0; j < NBW; ++j) {
+    auto copy = [&](int j, int o) {
       const int b = w + 2 * NPF * j;
       const int k = S::kind(b);
-      int o = off[j];
-      if (tail) o += (min(qc + row_of[j], Tq1) - qc - row_of[j]) * hstride;
-      dma16((k == 1 ? oh : qh) + (int64_t)qc * hstride + o, k == 2 ? smem + S::JUNK : stg + b * 64);
+      dma16s((k == 1 ? oh : qh) + (int64_t)qc * hstride, o, k == 2 ? smem + S::JUNK : stg + b * 64);
+    };
+    if (!tail) {
+#pragma unroll
+      for (int j = 0; j < NBW; ++j) copy(j, off[j]);
+    } else {  // rows past T_q are clamped to the last row
+#pragma unroll
+      for (int j = 0; j < NBW; ++j)
+        copy(j, off[j] + 2 * (min(qc + row_of[j], Tq1) - qc - row_of[j]) * hstride);
     }
     if (w == 0) {  // the chunk's L and -D rows: one copy is enough
       const int rr = min(qc + (lane & (BQ - 1)), Tq1);

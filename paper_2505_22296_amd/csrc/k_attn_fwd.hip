@@ -108,7 +108,7 @@ __global__ __launch_bounds__(NT, 1) void attn_fwd_kernel(FwdArgs a) {
     const int t = (w + NW * j) * 64 + lane;   // chunk slot within the tile
     const int ts = t % S::SUB, r = ts / 4;
     key_of[j] = r;
-    off[j] = r * kstride + (t / S::SUB) * 32 + blk_chunk(r, ts % 4) * 8;
+    off[j] = 2 * (r * kstride + (t / S::SUB) * 32 + blk_chunk(r, ts % 4) * 8);  // bytes
   }
   const uint16_t* kbase = a.k + (int64_t)kvh * D;
   const uint16_t* vbase = a.v + (int64_t)kvh * D;
@@ -116,13 +116,19 @@ __global__ __launch_bounds__(NT, 1) void attn_fwd_kernel(FwdArgs a) {
     const int kt = kt_first + n * BN;
     u32x4* stg = smem + (n % NST) * STAGE + w * 64;
     const int64_t rowoff = (int64_t)kt * kstride;
-    const bool tail = kt + BN > k1;  // keys past k1 (masked) are clamped to k1-1
+    if (kt + BN <= k1) {
 #pragma unroll
-    for (int j = 0; j < NBK; ++j) {
-      int o = off[j];
-      if (tail) o += (min(kt + key_of[j], k1 - 1) - kt - key_of[j]) * kstride;
-      dma16(kbase + rowoff + o, stg + NW * j * 64);
-      dma16(vbase + rowoff + o, stg + S::OFF_V + NW * j * 64);
+      for (int j = 0; j < NBK; ++j) {
+        dma16s(kbase + rowoff, off[j], stg + NW * j * 64);
+        dma16s(vbase + rowoff, off[j], stg + S::OFF_V + NW * j * 64);
+      }
+    } else {  // keys past k1 (masked) are clamped to k1-1
+#pragma unroll
+      for (int j = 0; j < NBK; ++j) {
+        const int o = off[j] + 2 * (min(kt + key_of[j], k1 - 1) - kt - key_of[j]) * kstride;
+        dma16s(kbase + rowoff, o, stg + NW * j * 64);
+        dma16s(vbase + rowoff, o, stg + S::OFF_V + NW * j * 64);
+      }
     }
   };
   // Lane-constant LDS offsets of the fragments.  K fragment (g, ks): tile row
