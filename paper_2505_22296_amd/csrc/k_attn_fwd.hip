@@ -209,17 +209,19 @@ __global__ __launch_bounds__(NT, 1) void attn_fwd_kernel(FwdArgs a) {
           }
       }
 
-      // ---- online softmax (lazy rescale); tree reductions keep the
-      // dependency chains short
-      float mx8[8];
+      // ---- online softmax (lazy rescale).  Row max of the lane's 32
+      // scores (finite or -inf): four chains of three-input maxima, 18 VALU
+      // operations (a wavefront's dependent VALU operations issue back to
+      // back, so short chains buy nothing)
+      float mx4[4];
 #pragma unroll
-      for (int i = 0; i < 8; ++i)
-        mx8[i] = fmaxf(fmaxf(s[0][i], s[0][i + 8]), fmaxf(s[1][i], s[1][i + 8]));
-#pragma unroll
-      for (int w2 = 4; w2 >= 1; w2 >>= 1)
-#pragma unroll
-        for (int i = 0; i < w2; ++i) mx8[i] = fmaxf(mx8[i], mx8[i + w2]);
-      const float mx = wave_max_xor32(mx8[0]);
+      for (int i = 0; i < 4; ++i) {
+        mx4[i] = max3_nonan(s[0][i], s[0][i + 4], s[0][i + 8]);
+        mx4[i] = max3_nonan(mx4[i], s[0][i + 12], s[1][i]);
+        mx4[i] = max3_nonan(mx4[i], s[1][i + 4], s[1][i + 8]);
+        mx4[i] = max3_nonan(mx4[i], s[1][i + 12], s[1][i + 12]);
+      }
+      const float mx = wave_max_xor32(max3_nonan(max3_nonan(mx4[0], mx4[1], mx4[2]), mx4[3], mx4[3]));
       const float m_new = fmaxf(m_run, mx);
       const bool need = (m_new - m_run) * c2 > 8.f;  // NaN (both -inf) -> false
       if (__ballot(need)) {
