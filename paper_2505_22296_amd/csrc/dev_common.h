@@ -115,13 +115,14 @@ SP_DEV int blk_tr_off2(int lane) {
 // (a VALU op; a shuffle would go through LDS with ds_bpermute).  Called with
 // the same register as both operands, the swap returns {x[l & 31], x[l | 32]}
 // in some order on every lane, so max / sum of the two is the xor-32 result.
-// max(a, b, c) as one v_max3_f32.  fmaxf in IEEE mode first quiets each
-// operand that might be a signalling NaN (one v_max_f32 per MFMA result);
-// for operands known not to be NaN (scores: finite or -inf) that is wasted.
+// max(a, b, c) as one gfx950 v_maximum3_f32 (NaN-propagating maximum).
+// fmaxf in IEEE mode first quiets every operand that could be a signalling
+// NaN (one v_max_f32 per MFMA result); the NaN-propagating form needs no
+// quieting and, for operands that are never NaN (scores: finite or -inf),
+// gives the same value.  Compiler-visible, so the wait states after the
+// MFMAs that produce the operands are inserted as for any VALU read.
 SP_DEV float max3_nonan(float a, float b, float c) {
-  float r;
-  asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
-  return r;
+  return __builtin_elementwise_maximum(a, __builtin_elementwise_maximum(b, c));
 }
 SP_DEV float wave_max_xor32(float x) {
   const uint32_t u = __float_as_uint(x);
