@@ -144,24 +144,26 @@ SP_DEV float wave_sum_xor32(float x) {
 // an LDS DMA it can see as a pending write to all of LDS and inserts
 // s_waitcnt vmcnt(0) before every later LDS read and barrier, which drains
 // the multi-stage prefetch on every tile.  Hidden from it, the only vmcnt
-// waits are the explicit ones of the staging protocol.
+// waits are the explicit ones of the staging protocol.  The s_nop is the one
+// wait state the gfx9 family requires between an SALU write of M0 and an LDS
+// DMA that reads it (the compiler adds it for the DMAs it generates itself).
 SP_DEV uint32_t lds_addr(const void* lds_block) {
   return __builtin_amdgcn_readfirstlane(
       (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const void*)lds_block);
 }
 SP_DEV void dma16(const void* gsrc, void* lds_block) {
-  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
                :: "v"(gsrc), "s"(lds_addr(lds_block)) : "memory", "m0");
 }
 // The same 16-byte copy from a wavefront-uniform base (SGPR pair) plus a
 // per-lane 32-bit byte offset (global saddr addressing): a tile's base moves
 // with scalar arithmetic and the lane offsets stay fixed from tile to tile.
 SP_DEV void dma16s(const void* sbase, uint32_t voff, void* lds_block) {
-  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1"
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
                :: "v"(voff), "s"(sbase), "s"(lds_addr(lds_block)) : "memory", "m0");
 }
 SP_DEV void dma4(const void* gsrc, void* lds_block) {
-  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dword %0, off"
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dword %0, off"
                :: "v"(gsrc), "s"(lds_addr(lds_block)) : "memory", "m0");
 }
 // s_waitcnt vmcnt(N) leaving expcnt / lgkmcnt unconstrained (gfx9 encoding).
