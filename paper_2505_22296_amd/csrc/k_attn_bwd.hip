@@ -87,6 +87,11 @@ __global__ __launch_bounds__(NTQ, 1) void attn_dq_kernel(DqArgs a) {
   const float l2 = (lse == neg_inf()) ? __builtin_inff() : lse * kLog2e;
   const float ndrow = a.neg_d[(int64_t)head * a.T_q + lrow];
   const float c2 = a.scale_log2;
+  // -D of the lane's row in every C register (the lane's row is fixed for
+  // the item): the accumulator input of each tile's first dP MFMA
+  f32x16 ndv;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) ndv[r] = ndrow;
 
   f32x16 acc[DB];
 #pragma unroll
@@ -166,12 +171,9 @@ __global__ __launch_bounds__(NTQ, 1) void attn_dq_kernel(DqArgs a) {
         vfr[ks] = stg[S::OFF_V + fo];
       }
       __builtin_amdgcn_sched_barrier(0);
-      f32x16 s, dp;
+      f32x16 s, dp = ndv;  // dP starts from -D, so the MFMAs leave dP - D
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        s[r] = 0.f;
-        dp[r] = 0.f;
-      }
+      for (int r = 0; r < 16; ++r) s[r] = 0.f;
       __builtin_amdgcn_s_setprio(1);
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
@@ -204,7 +206,7 @@ __global__ __launch_bounds__(NTQ, 1) void attn_dq_kernel(DqArgs a) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[r], c2, -l2));
-        ds[r] = p * (dp[r] + ndrow);
+        ds[r] = p * dp[r];
       }
       u32x4 b0 = pack_bf16x8(ds[0], ds[1], ds[2], ds[3], ds[4], ds[5], ds[6], ds[7]);
       u32x4 b1 = pack_bf16x8(ds[8], ds[9], ds[10], ds[11], ds[12], ds[13], ds[14], ds[15]);
