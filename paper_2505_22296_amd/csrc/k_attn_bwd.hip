@@ -426,10 +426,12 @@ SP_DEV void dkdv_body(const DkdvArgs& a, u32x4* smem, int w, int lane) {
       // dP - D (in s) and the partner's P -> dS
 #pragma unroll
       for (int half = 0; half < 2; ++half) {
-        const f32x8 p = __builtin_convertvector(__builtin_bit_cast(f16x8, xs[half * 64]), f32x8);
+        // P (fp16) times dP - D as one mixed-precision FMA with a zero addend
+        // (v_fma_mix_f32 reads the fp16 half directly: no conversion)
+        const f16x8 p = __builtin_bit_cast(f16x8, xs[half * 64]);
         f32x8 ds;
 #pragma unroll
-        for (int i = 0; i < 8; ++i) ds[i] = p[i] * s[half * 8 + i];
+        for (int i = 0; i < 8; ++i) ds[i] = __builtin_fmaf((float)p[i], s[half * 8 + i], 0.f);
         pb[half] = __builtin_bit_cast(u32x4, __builtin_convertvector(ds, bf16x8));
       }
     }
