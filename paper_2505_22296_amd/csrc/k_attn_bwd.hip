@@ -174,13 +174,11 @@ __global__ __launch_bounds__(NTQ, 1) void attn_dq_kernel(DqArgs a) {
       f32x16 s, dp = ndv;  // dP starts from -D, so the MFMAs leave dP - D
 #pragma unroll
       for (int r = 0; r < 16; ++r) s[r] = 0.f;
-      __builtin_amdgcn_s_setprio(1);
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
         s = mfma32(kfr[ks], qf[ks], s);
         dp = mfma32(vfr[ks], df[ks], dp);
       }
-      __builtin_amdgcn_s_setprio(0);
       // K^T fragments of the dQ product, read while dS is formed
       const uint16_t* stg16 = (const uint16_t*)stg;
       u32x4 ktr[DB * 2];
