@@ -111,10 +111,6 @@ SP_DEV int blk_tr_off2(int lane) {
   return row * 32 + blk_chunk(row, col >> 3) * 8 + (col & 7);
 }
 
-// Combine a value with the one of lane l^32 through v_permlane32_swap_b32
-// (a VALU op; a shuffle would go through LDS with ds_bpermute).  Called with
-// the same register as both operands, the swap returns {x[l & 31], x[l | 32]}
-// in some order on every lane, so max / sum of the two is the xor-32 result.
 // max(a, b, c) as one gfx950 v_maximum3_f32 (NaN-propagating maximum).
 // fmaxf in IEEE mode first quiets every operand that could be a signalling
 // NaN (one v_max_f32 per MFMA result); the NaN-propagating form needs no
@@ -124,10 +120,17 @@ SP_DEV int blk_tr_off2(int lane) {
 SP_DEV float max3_nonan(float a, float b, float c) {
   return __builtin_elementwise_maximum(a, __builtin_elementwise_maximum(b, c));
 }
+
+// Combine a value with the one of lane l^32 through v_permlane32_swap_b32
+// (a VALU op; a shuffle would go through LDS with ds_bpermute).  Called with
+// the same register as both operands, the swap returns {x[l & 31], x[l | 32]}
+// in some order on every lane, so max / sum of the two is the xor-32 result.
+// The max is the NaN-propagating one: its operands (row maxima of scores)
+// are never NaN, and it needs no quieting.
 SP_DEV float wave_max_xor32(float x) {
   const uint32_t u = __float_as_uint(x);
   const auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
-  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+  return __builtin_elementwise_maximum(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
 SP_DEV float wave_sum_xor32(float x) {
   const uint32_t u = __float_as_uint(x);

@@ -94,6 +94,11 @@ __global__ __launch_bounds__(NT, 1) void attn_fwd_kernel(FwdArgs a) {
     for (int r = 0; r < 16; ++r) oacc[d][r] = 0.f;
   float m_run = neg_inf(), l_part = 0.f;
   const float c2 = a.scale_log2;
+  // Carried with the running max (they change only when it is raised):
+  // msc = m_run * c2 (0 while m_run is -inf), and the score above which the
+  // max is raised, m_run + 8 / c2 (-inf while m_run is -inf)
+  const float raise_by = 8.f / c2;
+  float msc = 0.f, m_thr = neg_inf();
 
   const int kt_first = k0 & ~7;
   const int n_tiles = (k1 > k0) ? (k1 - kt_first + BN - 1) / BN : 0;
@@ -222,18 +227,20 @@ __global__ __launch_bounds__(NT, 1) void attn_fwd_kernel(FwdArgs a) {
         mx4[i] = max3_nonan(mx4[i], s[1][i + 12], s[1][i + 12]);
       }
       const float mx = wave_max_xor32(max3_nonan(max3_nonan(mx4[0], mx4[1], mx4[2]), mx4[3], mx4[3]));
-      const float m_new = fmaxf(m_run, mx);
-      const bool need = (m_new - m_run) * c2 > 8.f;  // NaN (both -inf) -> false
+      const bool need = mx > m_thr;  // false while every score is -inf
       if (__ballot(need)) {
-        float alpha = need ? exp2f((m_run - m_new) * c2) : 1.f;
-        if (need) m_run = m_new;
+        float alpha = need ? exp2f((m_run - mx) * c2) : 1.f;
+        if (need) {
+          m_run = mx;
+          msc = mx * c2;
+          m_thr = mx + raise_by;
+        }
         l_part *= alpha;
 #pragma unroll
         for (int d = 0; d < DB; ++d)
 #pragma unroll
           for (int r = 0; r < 16; ++r) oacc[d][r] *= alpha;
       }
-      const float msc = (m_run == neg_inf()) ? 0.f : m_run * c2;
       u32x4 pb[4];
       float ps[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
