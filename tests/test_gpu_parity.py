@@ -10,8 +10,9 @@ import pytest
 import oracle
 from tests.helpers import (assert_close, bits_from_dev, from_dev, lib_desc, make_shard,
                            oracle_kw, scaled_max_abs, to_dev, LSE_MAX_ABS)
-from workloads import (padded_heads, randn_bf16_bits, shard_inputs, ulysses_kv_head_map,
-                       ulysses_q_head_map, usp_shard, workload, WORKLOADS)
+from workloads import (bf16_bits_from_f32, padded_heads, randn_bf16_bits, shard_inputs,
+                       ulysses_kv_head_map, ulysses_q_head_map, usp_shard, workload,
+                       WORKLOADS)
 
 pytestmark = pytest.mark.gpu
 
@@ -212,6 +213,39 @@ def test_peaky_inputs_exercise_rescale(sp):
                        (from_dev(gk), RdK, "dK"), (from_dev(gv), RdV, "dV")):
         assert_close(g, r, what, max_abs=scaled_max_abs(r))
     assert np.abs(lse.cpu().numpy() - RL).max() <= LSE_MAX_ABS
+
+
+@pytest.mark.parametrize("causal", [True, False])
+def test_rising_scores_raise_the_max_every_tile(sp, causal):
+    """Scores that climb along the keys (a ramp in one dimension of K, met by
+    a constant in Q: about 1.6 per key before scaling, against the raise
+    threshold 8 / (scale log2 e) ~ 63 per 64-key tile) raise the forward's
+    running max in most tiles of every row, so the carried threshold, the
+    scaled max and the O / row-sum rescale run tile after tile; T = 333
+    leaves a ragged last tile.  Checked: O, LSE and dV (P^T dO, built from
+    the forward's LSE).  dQ and dK are left to the other tests: with |K| up
+    to ~133 in the ramp column, dQ there is scale * sum_j dS_j K_j with
+    sum_j dS_j = 0 per row, a small difference of large terms in which the
+    bf16 rounding of dS (as in any bf16 backward) is magnified ~100-fold."""
+    T, H, D = 333, 2, 128
+    sh = make_shard("ramp", T, T, D, H, 0, H, H, 1, H, 0, [T], [T], causal=causal)
+    q = randn_bf16_bits((T, H, D), 81)
+    k = randn_bf16_bits((T, H, D), 82)
+    v = randn_bf16_bits((T, H, D), 83)
+    do = randn_bf16_bits((T, H, D), 84)
+    q[:, :, 0] = bf16_bits_from_f32(np.full((T, H), 4.0, np.float32))
+    k[:, :, 0] = bf16_bits_from_f32(np.repeat((0.4 * np.arange(T, dtype=np.float32))[:, None], H, 1))
+    o, lse, gq, gk, gv = _run_fwd_bwd(sp, sh, q, k, v, do)
+    Q, K, V, dO = (_dec(x) for x in (q, k, v, do))
+    kw = oracle_kw(sh)
+    RO, RL = oracle.attn_forward(Q, K, V, **kw)
+    _, _, RdV = oracle.attn_backward(Q, K, V, dO, **kw)
+    assert_close(from_dev(o), RO, "O")
+    assert np.abs(lse.cpu().numpy() - RL).max() <= LSE_MAX_ABS
+    # without the causal mask every row's weight piles onto the top keys,
+    # whose dV sums all 333 rows of dO (|dV| past 16, where one bf16 ulp is
+    # 0.125): two bf16 ulps of the largest reference value, rel-L2 unchanged
+    assert_close(from_dev(gv), RdV, "dV", max_abs=scaled_max_abs(RdV))
 
 
 def test_deterministic(sp):
