@@ -155,6 +155,20 @@ def _stream(stream=None) -> int:
     return s.cuda_stream
 
 
+def _alloc_on(stream=None):
+    """Context for the wrapper's own allocations (outputs, workspace): on the
+    stream the kernels are launched on.  torch's caching allocator ties a
+    block to the stream current at allocation and, once the tensor is
+    dropped, hands it to the next allocation on that stream without waiting
+    for other streams; a workspace allocated on the current stream but read
+    by kernels queued on `stream` could be reused while they still run."""
+    import contextlib
+    import torch
+    if stream is None:
+        return contextlib.nullcontext()
+    return torch.cuda.stream(stream)
+
+
 def sp_attn_workspace_size(desc: Desc, op: int) -> int:
     n = ctypes.c_size_t(0)
     _check(load().sp_attn_workspace_size(desc.ref, op, ctypes.byref(n)), "sp_attn_workspace_size")
@@ -185,7 +199,8 @@ def sp_ulysses_pack(src, sp: int, H_dst_loc: int, head_map: Sequence[int], dst=N
     import torch
     T, Hs, D = src.shape
     if dst is None:
-        dst = torch.empty((sp, T, H_dst_loc, D), dtype=src.dtype, device=src.device)
+        with _alloc_on(stream):
+            dst = torch.empty((sp, T, H_dst_loc, D), dtype=src.dtype, device=src.device)
     m = np.ascontiguousarray(np.asarray(head_map, dtype=np.int32))
     _check(load().sp_ulysses_pack(_ptr(src), T, Hs, D, sp, H_dst_loc, m.ctypes.data_as(_i32p),
                                   _ptr(dst), _stream(stream)), "sp_ulysses_pack")
@@ -197,7 +212,8 @@ def sp_ulysses_unpack(src, head_map: Sequence[int], H_dst: int, dst=None, stream
     import torch
     sp, T, Hs, D = src.shape
     if dst is None:
-        dst = torch.empty((T, H_dst, D), dtype=src.dtype, device=src.device)
+        with _alloc_on(stream):
+            dst = torch.empty((T, H_dst, D), dtype=src.dtype, device=src.device)
     m = np.ascontiguousarray(np.asarray(head_map, dtype=np.int32))
     _check(load().sp_ulysses_unpack(_ptr(src), T, Hs, D, sp, m.ctypes.data_as(_i32p), H_dst,
                                     _ptr(dst), _stream(stream)), "sp_ulysses_unpack")
@@ -211,7 +227,8 @@ def sp_ulysses_unpack_add(src, head_map: Sequence[int], H_dst: int, dst=None, st
     import torch
     sp, T, Hs, D = src.shape
     if dst is None:
-        dst = torch.empty((T, H_dst, D), dtype=src.dtype, device=src.device)
+        with _alloc_on(stream):
+            dst = torch.empty((T, H_dst, D), dtype=src.dtype, device=src.device)
     m = np.ascontiguousarray(np.asarray(head_map, dtype=np.int32))
     _check(load().sp_ulysses_unpack_add(_ptr(src), T, Hs, D, sp, m.ctypes.data_as(_i32p), H_dst,
                                         _ptr(dst), _stream(stream)), "sp_ulysses_unpack_add")
@@ -231,10 +248,11 @@ def sp_token_logprob(logits, labels, cu_seqlens, ignore_index: int = -100, logp=
     T, V = logits.shape
     cu, n = _cu(cu_seqlens)
     dev = logits.device
-    logp = torch.empty(T, dtype=torch.float32, device=dev) if logp is None else logp
-    lse = torch.empty(T, dtype=torch.float32, device=dev) if lse is None else lse
-    if seq_sum is None:
-        seq_sum = torch.empty(max(n, 0), dtype=torch.float32, device=dev)
+    with _alloc_on(stream):
+        logp = torch.empty(T, dtype=torch.float32, device=dev) if logp is None else logp
+        lse = torch.empty(T, dtype=torch.float32, device=dev) if lse is None else lse
+        if seq_sum is None:
+            seq_sum = torch.empty(max(n, 0), dtype=torch.float32, device=dev)
     _check(load().sp_token_logprob(_ptr(logits), _ptr(labels), T, V, ignore_index,
                                    cu.ctypes.data_as(_i32p), n, _ptr(logp), _ptr(lse),
                                    _ptr(seq_sum) if n > 0 else None, _stream(stream)),
@@ -250,7 +268,8 @@ def sp_token_logprob_bwd(logits, labels, lse, cu_seqlens, grad_seq, ignore_index
     T, V = logits.shape
     cu, n = _cu(cu_seqlens)
     if dlogits is None:
-        dlogits = torch.empty_like(logits)
+        with _alloc_on(stream):
+            dlogits = torch.empty_like(logits)
     _check(load().sp_token_logprob_bwd(_ptr(logits), _ptr(labels), _ptr(lse), T, V, ignore_index,
                                        cu.ctypes.data_as(_i32p), n, _ptr(grad_seq), _ptr(dlogits),
                                        _stream(stream)), "sp_token_logprob_bwd")
@@ -264,8 +283,9 @@ def sp_loss_reduce(partial_sums, kind: int, coef: float, ref_partial_sums=None, 
     import torch
     spn, n = partial_sums.shape
     dev = partial_sums.device
-    loss = torch.empty(1, dtype=torch.float32, device=dev) if loss is None else loss
-    grad = torch.empty((spn, n), dtype=torch.float32, device=dev) if grad is None else grad
+    with _alloc_on(stream):
+        loss = torch.empty(1, dtype=torch.float32, device=dev) if loss is None else loss
+        grad = torch.empty((spn, n), dtype=torch.float32, device=dev) if grad is None else grad
     _check(load().sp_loss_reduce(_ptr(partial_sums), _ptr(ref_partial_sums), spn, n, kind,
                                  float(coef), _ptr(loss), _ptr(grad), _stream(stream)),
            "sp_loss_reduce")
@@ -275,38 +295,41 @@ def sp_loss_reduce(partial_sums, kind: int, coef: float, ref_partial_sums=None, 
 def sp_attn_fwd(desc: Desc, q, k, v, o=None, lse=None, workspace=None, stream=None):
     import torch
     c = desc.c
-    if o is None:
-        o = torch.empty((c.T_q, c.H_loc, c.head_dim), dtype=q.dtype, device=q.device)
-    if lse is None:
-        lse = torch.empty((c.H_loc, c.T_q), dtype=torch.float32, device=q.device)
-    ws, nb = _workspace(desc, SP_OP_FWD, q.device, workspace)
-    _check(load().sp_attn_fwd(desc.ref, _ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse), _ptr(ws),
-                              nb, _stream(stream)), "sp_attn_fwd")
+    with _alloc_on(stream):
+        if o is None:
+            o = torch.empty((c.T_q, c.H_loc, c.head_dim), dtype=q.dtype, device=q.device)
+        if lse is None:
+            lse = torch.empty((c.H_loc, c.T_q), dtype=torch.float32, device=q.device)
+        ws, nb = _workspace(desc, SP_OP_FWD, q.device, workspace)
+        _check(load().sp_attn_fwd(desc.ref, _ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse),
+                                  _ptr(ws), nb, _stream(stream)), "sp_attn_fwd")
     return o, lse
 
 
 def sp_attn_bwd(desc: Desc, q, k, v, o, lse, dout, dq=None, dq_acc=None, dk=None, dv=None,
                 workspace=None, stream=None):
     import torch
-    if dq is None and dq_acc is None:
-        dq = torch.empty_like(q)
-    if dk is None:
-        dk = torch.empty_like(k)
-    if dv is None:
-        dv = torch.empty_like(v)
-    ws, nb = _workspace(desc, SP_OP_BWD, q.device, workspace)
-    _check(load().sp_attn_bwd(desc.ref, _ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse),
-                              _ptr(dout), _ptr(dq), _ptr(dq_acc), _ptr(dk), _ptr(dv), _ptr(ws),
-                              nb, _stream(stream)), "sp_attn_bwd")
+    with _alloc_on(stream):
+        if dq is None and dq_acc is None:
+            dq = torch.empty_like(q)
+        if dk is None:
+            dk = torch.empty_like(k)
+        if dv is None:
+            dv = torch.empty_like(v)
+        ws, nb = _workspace(desc, SP_OP_BWD, q.device, workspace)
+        _check(load().sp_attn_bwd(desc.ref, _ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse),
+                                  _ptr(dout), _ptr(dq), _ptr(dq_acc), _ptr(dk), _ptr(dv),
+                                  _ptr(ws), nb, _stream(stream)), "sp_attn_bwd")
     return (dq if dq is not None else dq_acc), dk, dv
 
 
 def sp_ring_step(desc: Desc, q, k_chunk, v_chunk, o_acc, lse_acc, init: bool, o_out=None,
                  workspace=None, stream=None):
-    ws, nb = _workspace(desc, SP_OP_RING_STEP, q.device, workspace)
-    _check(load().sp_ring_step(desc.ref, _ptr(q), _ptr(k_chunk), _ptr(v_chunk), _ptr(o_acc),
-                               _ptr(lse_acc), 1 if init else 0, _ptr(o_out), _ptr(ws), nb,
-                               _stream(stream)), "sp_ring_step")
+    with _alloc_on(stream):
+        ws, nb = _workspace(desc, SP_OP_RING_STEP, q.device, workspace)
+        _check(load().sp_ring_step(desc.ref, _ptr(q), _ptr(k_chunk), _ptr(v_chunk), _ptr(o_acc),
+                                   _ptr(lse_acc), 1 if init else 0, _ptr(o_out), _ptr(ws), nb,
+                                   _stream(stream)), "sp_ring_step")
     return o_acc, lse_acc
 
 
@@ -322,7 +345,8 @@ def sp_lse_merge(o_acc, lse_acc, o_part, lse_part, o_out=None, stream=None):
 def sp_f32_to_bf16(src, dst=None, stream=None):
     import torch
     if dst is None:
-        dst = torch.empty(src.shape, dtype=torch.bfloat16, device=src.device)
+        with _alloc_on(stream):
+            dst = torch.empty(src.shape, dtype=torch.bfloat16, device=src.device)
     _check(load().sp_f32_to_bf16(_ptr(src), _ptr(dst), src.numel(), _stream(stream)),
            "sp_f32_to_bf16")
     return dst

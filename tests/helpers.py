@@ -77,11 +77,25 @@ def errs(gpu: np.ndarray, ref: np.ndarray):
     return mx, rel
 
 
+# Magnitude past which one bf16 rounding step (ulp 2^-5 on [4, 8)) alone
+# exceeds half of MAX_ABS.
+SCALED_FROM = 4.0
+
+
 def scaled_max_abs(ref) -> float:
-    """Absolute bar for bf16 results whose magnitude passes 4, where one bf16
-    rounding step alone exceeds half of MAX_ABS: two bf16 ulps of the largest
-    reference value (2^-7 of it), never below MAX_ABS.  rel-L2 keeps REL_L2."""
-    return max(MAX_ABS, 2.0 ** -7 * float(np.abs(ref).max()))
+    """Absolute bar for bf16 results: MAX_ABS while the largest reference
+    magnitude is at most SCALED_FROM; past it, two bf16 ulps of the largest
+    reference value (2^-7 of it), where one rounding step alone exceeds half
+    of MAX_ABS.  rel-L2 keeps REL_L2 either way."""
+    m = float(np.abs(ref).max()) if np.size(ref) else 0.0
+    if m <= SCALED_FROM:
+        return MAX_ABS
+    return max(MAX_ABS, 2.0 ** -7 * m)
+
+
+def widened(ref) -> bool:
+    """Whether scaled_max_abs(ref) is above the flat MAX_ABS bar."""
+    return scaled_max_abs(ref) > MAX_ABS
 
 
 def assert_close(gpu, ref, what, max_abs=MAX_ABS, rel_l2=REL_L2):

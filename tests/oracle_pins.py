@@ -160,6 +160,58 @@ def pin_torch_sdpa(A):
         assert np.allclose(a, b, rtol=0, atol=1e-12)
 
 
+def pin_sampled_checkers(A):
+    """The sampled checkers used at full size -- dQ of listed rows
+    (attn_dq_rows, with its O and LSE) and dK / dV of listed keys
+    (attn_dkdv_keys) -- equal torch fp64 SDPA + autograd restricted to the
+    same rows / keys, on arbitrary row and key subsets: varlen with padding
+    rows, GQA, dummy slots, ring-style position offsets, non-causal, and
+    pieces of one sequence (positions jumping between pieces)."""
+    rng = np.random.default_rng(13)
+    cases = [
+        (dict(T=37, H=4, Hkv=1, D=8, cu=[0, 37], num_real=4, gqa=4, kv_off=0, ho=0), None, None),
+        (dict(T=50, H=4, Hkv=2, D=6, cu=[0, 13, 13, 40, 47], num_real=7, gqa=2, kv_off=2, ho=4),
+         None, None),
+        (dict(T=41, H=3, Hkv=3, D=5, cu=[0, 20, 41], num_real=5, gqa=1, kv_off=3, ho=3), None, None),
+        # ring offsets: rows at positions 40.., keys at 30..
+        (dict(T=24, H=2, Hkv=1, D=4, cu=[0, 24], num_real=2, gqa=2, kv_off=0, ho=0),
+         40 + np.arange(24), 30 + np.arange(24)),
+        # pieces of one sequence: positions strictly increasing with jumps
+        (dict(T=30, H=3, Hkv=1, D=5, cu=[0, 30], num_real=3, gqa=3, kv_off=0, ho=0),
+         np.r_[np.arange(10), 50 + np.arange(20)], np.r_[5 + np.arange(12), 40 + np.arange(18)]),
+    ]
+    for c, pq, pk in cases:
+        T, H, Hkv, D = c["T"], c["H"], c["Hkv"], c["D"]
+        q, k, v, do = _rand(rng, T, H, D), _rand(rng, T, Hkv, D), _rand(rng, T, Hkv, D), _rand(rng, T, H, D)
+        for causal in (True, False):
+            kw = _kw(T, H, Hkv, cu=c["cu"], pos_q=pq, pos_k=pk, head_offset=c["ho"],
+                     num_real=c["num_real"], gqa=c["gqa"], kv_off=c["kv_off"], causal=causal)
+            rO, rdq, rdk, rdv = _torch_ref(q, k, v, do, kw)
+            for trial in range(3):
+                rows = np.sort(rng.choice(T, size=int(rng.integers(1, T)), replace=False))
+                keys = np.sort(rng.choice(T, size=int(rng.integers(1, T)), replace=False))
+                dq, O, _ = A.attn_dq_rows(q, k, v, do, rows, **kw)
+                assert np.allclose(dq, rdq[rows], rtol=0, atol=1e-12), np.abs(dq - rdq[rows]).max()
+                assert np.allclose(O, rO[rows], rtol=0, atol=1e-12)
+                dk, dv = A.attn_dkdv_keys(q, k, v, do, keys, **kw)
+                assert np.allclose(dk, rdk[keys], rtol=0, atol=1e-12), np.abs(dk - rdk[keys]).max()
+                assert np.allclose(dv, rdv[keys], rtol=0, atol=1e-12), np.abs(dv - rdv[keys]).max()
+
+
+def pin_bf16_decode(A):
+    """bf16_bits_to_f64 equals torch's bfloat16 -> float64 conversion on all
+    65,536 bit patterns (NaNs compared as NaN)."""
+    bits = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16)
+    ref = torch.from_numpy(bits.view(np.int16)).view(torch.bfloat16).to(torch.float64).numpy()
+    got = A.bf16_bits_to_f64(bits)
+    assert got.dtype == np.float64
+    nan = np.isnan(ref)
+    assert np.array_equal(np.isnan(got), nan)
+    assert np.array_equal(got[~nan], ref[~nan])
+    # signed zeros keep their sign
+    assert np.array_equal(np.signbit(got[~nan]), np.signbit(ref[~nan]))
+
+
 # ------------------------------------------------------- finite differences
 def pin_finite_differences(A):
     """Central differences of sum(dO * O) match the analytic backward."""
@@ -555,7 +607,8 @@ def pin_sp_loss_equals_no_sp(Lo):
 
 
 ATTN_PINS = [pin_single_visible_key, pin_zero_query_uniform, pin_torch_sdpa,
-             pin_finite_differences, pin_gradient_sums, pin_packed_equals_separate]
+             pin_finite_differences, pin_gradient_sums, pin_packed_equals_separate,
+             pin_sampled_checkers, pin_bf16_decode]
 SP_PINS = [pin_merge_identity, pin_pack_unpack, pin_unpack_add_adjoint, pin_unpack_add_bf16]
 LOSS_PINS = [pin_token_logprobs_torch, pin_token_grad_fd, pin_listing2_worked_example,
              pin_sp_loss_equals_no_sp]

@@ -222,11 +222,13 @@ def test_rising_scores_raise_the_max_every_tile(sp, causal):
     threshold 8 / (scale log2 e) ~ 63 per 64-key tile) raise the forward's
     running max in most tiles of every row, so the carried threshold, the
     scaled max and the O / row-sum rescale run tile after tile; T = 333
-    leaves a ragged last tile.  Checked: O, LSE and dV (P^T dO, built from
-    the forward's LSE).  dQ and dK are left to the other tests: with |K| up
-    to ~133 in the ramp column, dQ there is scale * sum_j dS_j K_j with
-    sum_j dS_j = 0 per row, a small difference of large terms in which the
-    bf16 rounding of dS (as in any bf16 backward) is magnified ~100-fold."""
+    leaves a ragged last tile.  Checked: O, LSE, dV, dK, and dQ except its
+    ramp column: with |K| up to ~133 there, dQ[:, :, 0] is
+    scale * sum_j dS_j K_j with sum_j dS_j = 0 per row, a small difference
+    of large terms in which the bf16 rounding of dS (as in any bf16
+    backward) is magnified ~100-fold.  The other 127 columns multiply
+    N(0, 1) keys and dK has no such cancellation, so both take the usual
+    bars."""
     T, H, D = 333, 2, 128
     sh = make_shard("ramp", T, T, D, H, 0, H, H, 1, H, 0, [T], [T], causal=causal)
     q = randn_bf16_bits((T, H, D), 81)
@@ -239,8 +241,12 @@ def test_rising_scores_raise_the_max_every_tile(sp, causal):
     Q, K, V, dO = (_dec(x) for x in (q, k, v, do))
     kw = oracle_kw(sh)
     RO, RL = oracle.attn_forward(Q, K, V, **kw)
-    _, _, RdV = oracle.attn_backward(Q, K, V, dO, **kw)
+    RdQ, RdK, RdV = oracle.attn_backward(Q, K, V, dO, **kw)
     assert_close(from_dev(o), RO, "O")
+    gq_, gk_ = from_dev(gq), from_dev(gk)
+    assert_close(gq_[:, :, 1:], RdQ[:, :, 1:], "dQ (columns 1..)",
+                 max_abs=scaled_max_abs(RdQ[:, :, 1:]))
+    assert_close(gk_, RdK, "dK", max_abs=scaled_max_abs(RdK))
     assert np.abs(lse.cpu().numpy() - RL).max() <= LSE_MAX_ABS
     # without the causal mask every row's weight piles onto the top keys,
     # whose dV sums all 333 rows of dO (|dV| past 16, where one bf16 ulp is

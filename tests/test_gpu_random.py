@@ -7,14 +7,17 @@ heads); causal or not; and one of three layouts -- packed segments of one
 batch (some empty, padding rows after the last), segments whose query and
 key positions start at different offsets (ring-style, T_q != T_k), or pieces
 of one sequence (positions strictly increasing over the pieces).  The bars
-are the parity bars of the fixed cases; dK/dV use the magnitude-scaled
-absolute bar because large GQA groups push them past 4."""
+are the parity bars of the fixed cases: max-abs 2e-2 and rel-L2 5e-3.  The absolute bar is
+widened (two bf16 ulps of the largest reference value) only for an output
+whose reference magnitude passes 4 -- large GQA groups sum several query
+heads into one dK / dV -- and the test prints every seed and output where
+that happened."""
 import numpy as np
 import pytest
 
 import oracle
 from tests.helpers import (assert_close, bits_from_dev, from_dev, lib_desc, make_shard, oracle_kw,
-                           scaled_max_abs, to_dev, LSE_MAX_ABS)
+                           scaled_max_abs, to_dev, widened, LSE_MAX_ABS)
 from workloads import padded_heads, shard_inputs
 
 pytestmark = pytest.mark.gpu
@@ -109,6 +112,11 @@ def test_random_shard_parity(sp, seed):
     RdQ, RdK, RdV = oracle.attn_backward(qf, kf, vf, dof, **kw)
     nr = sh.n_real_loc
     GL = lse.cpu().numpy().astype(np.float64)
+    refs = {"O": RO[:, :nr], "dQ": RdQ[:, :nr], "dK": RdK, "dV": RdV}
+    wide = [n for n, r in refs.items() if np.size(r) and widened(r)]
+    if wide:
+        print(f"seed {seed}: widened absolute bar for {wide} "
+              f"(max |ref| {[round(float(np.abs(refs[n]).max()), 2) for n in wide]})", flush=True)
     if nr:
         assert_close(from_dev(o)[:, :nr], RO[:, :nr], "O", max_abs=scaled_max_abs(RO[:, :nr]))
         fin = np.isfinite(RL[:nr])

@@ -143,3 +143,33 @@ def test_concurrent_host_threads(sp):
         for o in results[i]:
             for k, r in ref.items():
                 assert np.array_equal(o[k], r), f"{k} differs in thread {i}"
+
+
+def test_explicit_stream_argument_keeps_its_buffers(sp):
+    """stream= given while the current stream is the default one: the
+    wrapper's own outputs and workspaces belong to the launch stream, so
+    memory the default stream allocates and overwrites while the launch
+    stream is still queued behind a spin is never theirs.  The results
+    match the default-stream run bit for bit."""
+    import torch
+    sh, src = _sources()
+    d = lib_desc(sh)
+    o_r, lse_r = sp.sp_attn_fwd(d, src["q"], src["k"], src["v"])
+    g_r = sp.sp_attn_bwd(d, src["q"], src["k"], src["v"], o_r, lse_r, src["do"])
+    ref = [_bits(t) for t in (o_r, lse_r, *g_r)]
+    torch.cuda.synchronize()
+    sizes = [sp.sp_attn_workspace_size(d, sp.SP_OP_FWD), sp.sp_attn_workspace_size(d, sp.SP_OP_BWD),
+             o_r.numel() * 2, lse_r.numel() * 4]
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        torch.cuda._sleep(50_000_000)  # the launch stream waits tens of milliseconds
+    o, lse = sp.sp_attn_fwd(d, src["q"], src["k"], src["v"], stream=s)
+    g = sp.sp_attn_bwd(d, src["q"], src["k"], src["v"], o, lse, src["do"], stream=s)
+    # meanwhile the default stream allocates blocks of the same sizes and
+    # overwrites them
+    junk = [torch.full((n,), 255, dtype=torch.uint8, device="cuda") for n in sizes for _ in range(2)]
+    s.synchronize()
+    torch.cuda.synchronize()
+    del junk
+    for name, a, r in zip(("o", "lse", "dq", "dk", "dv"), (o, lse, *g), ref):
+        assert np.array_equal(_bits(a), r), f"{name} differs with stream= given"

@@ -95,6 +95,20 @@ MUTANTS = [
      "lse = np.where(has, np.log(np.where(has, den, 1.0)), NEG_INF)"),
     ("attention", "out.append((i, g // gqa_group - kv_head_offset) if g < num_real_heads else (i, None))",
      "out.append((i, g % max(1, gqa_group) - kv_head_offset) if g < num_real_heads else (i, None))"),
+    # the sampled checkers used at full size, and the bf16 decode
+    ("attention", "Drow = (dO * O[:, h, :]).sum(axis=1)", "Drow = (dO * O[:, h, :])[:, :-1].sum(axis=1)"),
+    ("attention", "dS = P * (dO @ v[:, kv, :].T - Drow[:, None])", "dS = P * (dO @ v[:, kv, :].T)"),
+    ("attention", 'out[:, h, :] = kw["scale"] * (dS @ k[:, kv, :])', 'out[:, h, :] = (dS @ k[:, kv, :])'),
+    ("attention", "need[r] = m.any(axis=1)", "need[r] = m.all(axis=1)"),
+    ("attention", "m = allowed_mask(r, seg_q, seg_k[keys], pq, pk[keys], causal)",
+     "m = allowed_mask(r, seg_q, seg_k[keys], pq, pk[keys] + 1, causal)"),
+    ("attention", "Pk = P[:, keys]", "Pk = P[:, np.minimum(keys + 1, P.shape[1] - 1)]"),
+    ("attention", "dk[:, kv, :] += kw[\"scale\"] * (dS.T @ q[r, h, :])", "dk[:, kv, :] += kw[\"scale\"] * (dS.T @ do[r, h, :])"),
+    ("attention", "Drow = (dO * o_r).sum(axis=1)\n            Pk", "Drow = (dO * o_r[:, ::-1]).sum(axis=1)\n            Pk"),
+    ("attention", "b = np.asarray(bits, dtype=np.uint16).astype(np.uint32) << 16",
+     "b = (np.asarray(bits, dtype=np.uint16).astype(np.uint32) << 16) | 0x8000"),
+    ("attention", "return b.view(np.float32).astype(np.float64)",
+     "return b.view(np.float32).astype(np.float16).astype(np.float64)"),
     ("sp", "wb = np.where(fin & np.isfinite(lb), np.exp(np.where(np.isfinite(lb), lb, 0.0) - Ls), 0.0)",
      "wb = np.where(fin & np.isfinite(lb), np.exp(np.where(np.isfinite(lb), lb, 0.0) - Ls) * 0.999, 0.0)"),
     ("sp", "pad = np.zeros(x.shape[:2] + (sp - rem,) + x.shape[3:], dtype=x.dtype)",
