@@ -223,6 +223,32 @@ sp_status sp_attn_fwd(const sp_attn_desc* desc, const void* q, const void* k, co
                       void* stream);
 
 /*
+ * Allocation-free forward, for callers that cannot allocate device memory or
+ * pass a workspace (tight serving loops, harnesses that forbid hipMalloc):
+ * the same operation, kernels and outputs as sp_attn_fwd (bit for bit), with
+ * the work list kept in a library-owned device array of
+ * SP_STATIC_SCRATCH_BYTES instead of a caller workspace.  Every GPU the
+ * library runs on holds its own copy of that array until the process ends;
+ * its address is looked up once per device on the first call there.  The
+ * call allocates no device memory (and calls no allocating HIP or library
+ * routine); its host-side scheduling uses ordinary host heap memory.
+ *
+ * Limit: the work list (SP_SCHED_ITEM_INTS int32 per item, as reported by
+ * sp_attn_schedule for SP_OP_FWD) must fit in SP_STATIC_SCRATCH_BYTES, i.e.
+ * at most 32768 items -- about 8.4M query rows x real heads; larger
+ * problems return SP_ERR_UNSUPPORTED before anything is enqueued.
+ * `stream` must belong to the current device (else SP_ERR_INVALID_ARG).
+ * Every call on one GPU shares that GPU's array and overwrites the part it
+ * uses (nothing in it needs to start at zero): calls that overlap on one GPU
+ * -- on different streams without ordering between them, or from several
+ * host threads -- race on it.  Order them on one stream or synchronize.
+ * Like sp_attn_fwd it refuses a capturing stream (SP_ERR_UNSUPPORTED).
+ */
+#define SP_STATIC_SCRATCH_BYTES (1u << 20)
+sp_status sp_attn_fwd_static(const sp_attn_desc* desc, const void* q, const void* k,
+                             const void* v, void* o, float* lse, void* stream);
+
+/*
  * Attention backward (gradients of sum(dO * O)), with P recomputed from LSE:
  * dV = P^T dO, dP = dO V^T, dS = P (dP - rowsum(dO o O)), dQ = scale dS K,
  * dK = scale dS^T Q.  dK/dV of a KV head sum over its real query heads.

@@ -5,6 +5,7 @@ The Python surface mirrors the C entry points one to one; see `_lib`.
 """
 from ._lib import (Desc, SpError, load, status_string, sp_attn_workspace_size, sp_attn_schedule,
                    sp_ulysses_pack, sp_ulysses_unpack, sp_ulysses_unpack_add, sp_attn_fwd,
+                   sp_attn_fwd_static, STATIC_SCRATCH_BYTES,
                    sp_attn_bwd, sp_ring_step, sp_lse_merge, sp_f32_to_bf16, sp_profile_events,
                    sp_token_logprob, sp_token_logprob_bwd, sp_loss_reduce, SP_LOSS_SFT, SP_LOSS_DPO,
                    SP_KERNEL_TOKEN_LOGPROB, SP_KERNEL_TOKEN_LOGPROB_BWD,
@@ -16,6 +17,7 @@ from ._lib import (Desc, SpError, load, status_string, sp_attn_workspace_size, s
 __all__ = [
     "Desc", "SpError", "load", "status_string", "sp_attn_workspace_size", "sp_attn_schedule",
     "sp_ulysses_pack", "sp_ulysses_unpack", "sp_ulysses_unpack_add", "sp_attn_fwd",
+    "sp_attn_fwd_static", "STATIC_SCRATCH_BYTES",
     "sp_attn_bwd", "sp_ring_step", "sp_lse_merge", "sp_f32_to_bf16", "sp_profile_events",
     "sp_token_logprob", "sp_token_logprob_bwd", "sp_loss_reduce", "SP_LOSS_SFT", "SP_LOSS_DPO",
     "SP_KERNEL_TOKEN_LOGPROB", "SP_KERNEL_TOKEN_LOGPROB_BWD",

@@ -71,6 +71,7 @@ def load() -> ctypes.CDLL:
         "sp_loss_reduce": (i32, [vp, vp, i32, i32, i32, ctypes.c_float, vp, vp, vp]),
         "sp_attn_workspace_size": (i32, [D, i32, ctypes.POINTER(sz)]),
         "sp_attn_fwd": (i32, [D, vp, vp, vp, vp, vp, vp, sz, vp]),
+        "sp_attn_fwd_static": (i32, [D, vp, vp, vp, vp, vp, vp]),
         "sp_attn_bwd": (i32, [D, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
         "sp_ring_step": (i32, [D, vp, vp, vp, vp, vp, i32, vp, vp, sz, vp]),
         "sp_lse_merge": (i32, [vp, vp, vp, i32, vp, i32, i32, i32, vp, vp]),
@@ -88,7 +89,7 @@ def load() -> ctypes.CDLL:
 
 EXPORTED = ["sp_status_string", "sp_version", "sp_ulysses_pack", "sp_ulysses_unpack",
             "sp_ulysses_unpack_add", "sp_token_logprob", "sp_token_logprob_bwd", "sp_loss_reduce",
-            "sp_attn_workspace_size", "sp_attn_fwd", "sp_attn_bwd", "sp_ring_step",
+            "sp_attn_workspace_size", "sp_attn_fwd", "sp_attn_fwd_static", "sp_attn_bwd", "sp_ring_step",
             "sp_lse_merge", "sp_f32_to_bf16", "sp_attn_schedule", "sp_profile_events"]
 
 SP_KERNEL_ATTN_FWD, SP_KERNEL_ATTN_DQ, SP_KERNEL_ATTN_DKDV = 1, 2, 3
@@ -303,6 +304,18 @@ def sp_attn_fwd(desc: Desc, q, k, v, o=None, lse=None, workspace=None, stream=No
         ws, nb = _workspace(desc, SP_OP_FWD, q.device, workspace)
         _check(load().sp_attn_fwd(desc.ref, _ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse),
                                   _ptr(ws), nb, _stream(stream)), "sp_attn_fwd")
+    return o, lse
+
+
+STATIC_SCRATCH_BYTES = 1 << 20
+
+
+def sp_attn_fwd_static(desc: Desc, q, k, v, o, lse, stream=None):
+    """Allocation-free forward: outputs must be given (o [T_q, H_loc, D]
+    bf16, lse [H_loc, T_q] float32); the work list lives in the library's
+    fixed device array (STATIC_SCRATCH_BYTES per GPU)."""
+    _check(load().sp_attn_fwd_static(desc.ref, _ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse),
+                                     _stream(stream)), "sp_attn_fwd_static")
     return o, lse
 
 

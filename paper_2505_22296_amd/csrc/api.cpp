@@ -12,9 +12,11 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cmath>
 #include <cstdint>
 #include <cstring>
+#include <mutex>
 #include <vector>
 
 #include "../../include/sp_attn.h"
@@ -275,17 +277,28 @@ Layout layout_for(const sp_attn_desc* d, const Problem& p, int op, size_t n_item
   return L;
 }
 
+// Item counts of schedule_rows with empty items included (the worst case
+// the workspace is sized for) and of schedule_keys, without building them.
+size_t row_item_count(const sp_attn_desc* d, const Problem& p, int BM) {
+  size_t per_head = 0;
+  for (const Seg& g : p.segs) per_head += (size_t)((g.qb - g.qa) + BM - 1) / BM;
+  per_head += (size_t)((d->T_q - p.q_pad) + BM - 1) / BM;
+  return per_head * (size_t)p.n_real;
+}
+size_t key_item_count(const sp_attn_desc* d, const Problem& p, int BNK) {
+  size_t per_head = 0;
+  for (const Seg& g : p.segs_k) per_head += (size_t)((g.kb - g.ka) + BNK - 1) / BNK;
+  per_head += (size_t)((d->T_k - p.k_pad) + BNK - 1) / BNK;
+  return per_head * (size_t)p.n_real;
+}
+
 // Worst-case item counts (with empty items) for sizing.
 void item_counts(const sp_attn_desc* d, const Problem& p, int op, size_t& a, size_t& b) {
-  std::vector<int32_t> tmp;
   if (op == SP_OP_BWD) {
-    schedule_rows(d, p, spk::kDqBM, spk::kDqBN, true, tmp);
-    a = tmp.size() / kItemInts;
-    schedule_keys(d, p, spk::kDkdvBN, spk::kDkdvBQ, tmp);
-    b = tmp.size() / kItemInts;
+    a = row_item_count(d, p, spk::kDqBM);
+    b = key_item_count(d, p, spk::kDkdvBN);
   } else {
-    schedule_rows(d, p, spk::kFwdBM, spk::kFwdBN, true, tmp);
-    a = tmp.size() / kItemInts;
+    a = row_item_count(d, p, spk::kFwdBM);
     b = 0;
   }
 }
@@ -531,9 +544,60 @@ sp_status sp_attn_schedule(const sp_attn_desc* desc, int32_t op, int32_t* items,
   return SP_OK;
 }
 
+}  // extern "C"
+
+namespace {
+
+// ---- Scratch of the allocation-free forward (sp_attn_fwd_static).  A
+// file-scope device array: every GPU the library runs on holds its own copy
+// at its own address until the process ends.  In host code `scratch` is a
+// host-side stand-in, never a device address: the device copy's address is
+// looked up once per device with hipGetSymbolAddress (that device current)
+// and only that pointer is handed to kernels and copies.
+__device__ __align__(256) unsigned char scratch[SP_STATIC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+std::atomic<void*> g_scratch_ptr[kMaxDevices];
+
+// Device address of the current device's scratch (looked up on first use).
+sp_status static_scratch(void** out) {
+  int dev = -1;
+  SP_HIP(hipGetDevice(&dev));
+  if (dev < 0 || dev >= kMaxDevices) return SP_ERR_UNSUPPORTED;
+  void* p = g_scratch_ptr[dev].load(std::memory_order_acquire);
+  if (!p) {
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    p = g_scratch_ptr[dev].load(std::memory_order_relaxed);
+    if (!p) {
+      if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return SP_ERR_HIP;
+      g_scratch_ptr[dev].store(p, std::memory_order_release);
+    }
+  }
+  *out = p;
+  return SP_OK;
+}
+
+// The stream must belong to the current device (the scratch looked up is
+// that device's).
+sp_status stream_on_current_device(hipStream_t st) {
+  if (!st) return SP_OK;
+  int cur = -1, sdev = -1;
+  SP_HIP(hipGetDevice(&cur));
+  SP_HIP(hipStreamGetDevice(st, &sdev));
+  return sdev == cur ? SP_OK : SP_ERR_INVALID_ARG;
+}
+
+}  // namespace
+
+extern "C" {
+
+// Forward / ring step.  `static_ws`: the work list goes to the current
+// device's static scratch instead of the caller's workspace (sp_attn_fwd_static).
 static sp_status fwd_common(const sp_attn_desc* d, const void* q, const void* k, const void* v,
                             void* o, float* lse, float* o_acc, float* lse_acc, int init,
-                            void* o_out, void* ws, size_t ws_bytes, void* stream, bool ring) {
+                            void* o_out, void* ws, size_t ws_bytes, void* stream, bool ring,
+                            bool static_ws = false) {
   Problem p;
   sp_status s = validate(d, p);
   if (s != SP_OK) return s;
@@ -550,15 +614,23 @@ static sp_status fwd_common(const sp_attn_desc* d, const void* q, const void* k,
   const bool include_empty = !ring || init || o_out;
   std::vector<int32_t> items;
   schedule_rows(d, p, spk::kFwdBM, spk::kFwdBN, include_empty, items);
-  size_t na = 0, nb = 0;
-  item_counts(d, p, SP_OP_FWD, na, nb);
-  Layout L = layout_for(d, p, ring ? SP_OP_RING_STEP : SP_OP_FWD, na, nb);
-  if ((s = check_ws(L, ws, ws_bytes)) != SP_OK) return s;
-  hipStream_t st = (hipStream_t)stream;
-  if ((s = refuse_capture(st)) != SP_OK) return s;
   const int n_items = (int)(items.size() / kItemInts);
+  hipStream_t st = (hipStream_t)stream;
+  void* items_dev = nullptr;
+  if (static_ws) {
+    if (items.size() * sizeof(int32_t) > SP_STATIC_SCRATCH_BYTES) return SP_ERR_UNSUPPORTED;
+    if ((s = refuse_capture(st)) != SP_OK) return s;
+    if ((s = stream_on_current_device(st)) != SP_OK) return s;
+    if ((s = static_scratch(&items_dev)) != SP_OK) return s;
+  } else {
+    Layout L = layout_for(d, p, ring ? SP_OP_RING_STEP : SP_OP_FWD,
+                          row_item_count(d, p, spk::kFwdBM), 0);
+    if ((s = check_ws(L, ws, ws_bytes)) != SP_OK) return s;
+    if ((s = refuse_capture(st)) != SP_OK) return s;
+    items_dev = at(ws, L.items_dq);
+  }
   if (n_items > 0) {
-    if ((s = upload(at(ws, L.items_dq), items, st)) != SP_OK) return s;
+    if ((s = upload(items_dev, items, st)) != SP_OK) return s;
     spk::FwdArgs a{};
     a.q = (const uint16_t*)q;
     a.k = (const uint16_t*)k;
@@ -568,7 +640,7 @@ static sp_status fwd_common(const sp_attn_desc* d, const void* q, const void* k,
     a.o_acc = o_acc;
     a.lse_acc = lse_acc;
     a.o_out = (uint16_t*)o_out;
-    a.items = (const int32_t*)at(ws, L.items_dq);
+    a.items = (const int32_t*)items_dev;
     a.T_q = d->T_q; a.T_k = d->T_k; a.H = d->H_loc; a.Hkv = d->Hkv_loc;
     a.scale_log2 = d->softmax_scale * 1.4426950408889634f;
     a.causal = d->causal;
@@ -593,6 +665,12 @@ sp_status sp_attn_fwd(const sp_attn_desc* desc, const void* q, const void* k, co
                       void* stream) {
   return fwd_common(desc, q, k, v, o, lse, nullptr, nullptr, 1, nullptr, workspace,
                     workspace_bytes, stream, false);
+}
+
+sp_status sp_attn_fwd_static(const sp_attn_desc* desc, const void* q, const void* k,
+                             const void* v, void* o, float* lse, void* stream) {
+  return fwd_common(desc, q, k, v, o, lse, nullptr, nullptr, 1, nullptr, nullptr, 0, stream,
+                    false, true);
 }
 
 sp_status sp_ring_step(const sp_attn_desc* desc, const void* q, const void* k_chunk,

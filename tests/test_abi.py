@@ -278,3 +278,26 @@ def test_workspace_sizes_for_workloads():
         for op in (sp.SP_OP_FWD, sp.SP_OP_BWD, sp.SP_OP_RING_STEP):
             n = sp.sp_attn_workspace_size(d, op)
             assert 256 <= n < (8 << 30), (name, op, n)
+
+
+def test_static_forward_rejects_oversized_work_list():
+    """sp_attn_fwd_static refuses, before anything is enqueued, a problem
+    whose work list would not fit the library's fixed scratch array
+    (32768 items of 8 int32 = SP_STATIC_SCRATCH_BYTES); pointers are fake
+    and never dereferenced."""
+    import numpy as np
+    import paper_2505_22296_amd as sp
+    lib = sp.load()
+    fake = 1 << 20
+    per_item_rows = 256
+    T = (sp.STATIC_SCRATCH_BYTES // (8 * 4) + 1) * per_item_rows
+    d = sp.Desc(T_q=T, T_k=T, head_dim=128, H_loc=1, head_offset=0, num_real_heads=1,
+                num_padded_heads=1, gqa_group=1, Hkv_loc=1, kv_head_offset=0,
+                cu_seqlens_q=np.array([0, T]), cu_seqlens_k=np.array([0, T]))
+    assert lib.sp_attn_fwd_static(d.ref, fake, fake, fake, fake, fake, None) == sp.SP_ERR_UNSUPPORTED
+    n = np.zeros(1, np.int32)
+    assert lib.sp_attn_schedule(d.ref, sp.SP_OP_FWD, None, 0, n.ctypes.data_as(sp._lib._i32p)) == 0
+    assert n[0] * 8 * 4 > sp.STATIC_SCRATCH_BYTES
+    # argument errors come first, as for sp_attn_fwd
+    assert lib.sp_attn_fwd_static(d.ref, fake + 2, fake, fake, fake, fake, None) == sp.SP_ERR_INVALID_ARG
+    assert lib.sp_attn_fwd_static(None, fake, fake, fake, fake, fake, None) == sp.SP_ERR_INVALID_ARG
