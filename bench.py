@@ -45,7 +45,12 @@ from workloads import (allowed_pairs, ring_chunk_positions, shard_inputs, randn_
 METRIC = "attn fwd+bwd TFLOP/s (real heads) per SP-rank shard; % of bf16 MFMA peak"
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA, published
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E, published
-DEFAULT_WORKLOAD = "ulysses_7b_L32768_q28kv4_sp8_r6_d128"
+# the largest single-GPU shard: ring rank 4 of 8 over a 131072-token
+# sequence (Q chunk of 16384 against KV chunks 0..4), 28 query / 4 KV heads
+DEFAULT_WORKLOAD = "ring_L131072_8chunks_r4_q28kv4_d128"
+# shards with dummy slots, for the dummy-head overhead (1 of 4 and 2 of 3)
+DUMMY_WORKLOADS = ("ulysses_tiny_L1024_mha7of8_sp2_r1_d64",
+                   "ulysses_long_L131072_4x32768_q40kv8_sp16_r13_d128")
 
 
 def log(*a):
@@ -225,7 +230,9 @@ class Step:
         if self.ulysses:
             t.arm(sp.SP_KERNEL_PACK, 0.0)
             sp.sp_ulysses_pack(self.q_pre, sh.sp, sh.H_loc, self.qmap, dst=self.send_q)
+            t.arm(sp.SP_KERNEL_PACK, 0.0)
             sp.sp_ulysses_pack(self.k_pre, sh.sp, self.kw, self.kmap, dst=self.send_k)
+            t.arm(sp.SP_KERNEL_PACK, 0.0)
             sp.sp_ulysses_pack(self.v_pre, sh.sp, self.kw, self.kmap, dst=self.send_v)
         if self.ring:
             n = len(self.descs)
@@ -242,6 +249,7 @@ class Step:
             t.arm(sp.SP_KERNEL_UNPACK, 0.0)
             sp.sp_ulysses_unpack(self.o.view(sh.sp, self.Tl, sh.H_loc, sh.D), self.qmap, sh.hs,
                                  dst=self.o_pre)
+            t.arm(sp.SP_KERNEL_PACK, 0.0)
             sp.sp_ulysses_pack(self.do_pre, sh.sp, sh.H_loc, self.qmap, dst=self.send_do)
         if self.ring:
             self.dq_acc.zero_()
@@ -258,51 +266,114 @@ class Step:
             sp.sp_attn_bwd(self.desc, self.q, self.k, self.v, self.o, self.lse, self.do,
                            dq=self.dq, dk=self.dk, dv=self.dv, workspace=self.ws_b)
         if self.ulysses:
+            t.arm(sp.SP_KERNEL_UNPACK, 0.0)
             sp.sp_ulysses_unpack(self.dq.view(sh.sp, self.Tl, sh.H_loc, sh.D), self.qmap, sh.hs,
                                  dst=self.dq_pre)
             if self.mha and not self.ring:
+                t.arm(sp.SP_KERNEL_UNPACK, 0.0)
                 sp.sp_ulysses_unpack(self.dk.view(sh.sp, self.Tl, sh.H_loc, sh.D), self.qmap,
                                      sh.hkv, dst=self.dk_pre)
+                t.arm(sp.SP_KERNEL_UNPACK, 0.0)
                 sp.sp_ulysses_unpack(self.dv.view(sh.sp, self.Tl, sh.H_loc, sh.D), self.qmap,
                                      sh.hkv, dst=self.dv_pre)
             elif not self.mha:
                 t.arm(sp.SP_KERNEL_UNPACK_ADD, 0.0)
                 sp.sp_ulysses_unpack_add(self.recv_dk, self.kmap, sh.hkv, dst=self.dk_pre)
+                t.arm(sp.SP_KERNEL_UNPACK_ADD, 0.0)
                 sp.sp_ulysses_unpack_add(self.recv_dv, self.kmap, sh.hkv, dst=self.dv_pre)
 
 
-def cpu_baseline(sh, budget_s=15.0):
-    """The fp64 oracle, as it stands, on a causal prefix of the workload's first
-    segment (all real heads), sized for ~budget_s of CPU work."""
+def cpu_model():
+    """The host CPU's model name (/proc/cpuinfo), or None."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
+def monolithic_problem(sh):
+    """The shard as one attention problem for the oracle: bf16 bits of Q, K,
+    V, dO and its oracle keyword arguments (ring / zigzag: the rank's rows
+    against the concatenated keys of all its steps, positions deciding
+    visibility), plus the pairs-per-head counter of a row subset."""
     import oracle
-    from threadpoolctl import threadpool_info
-    seg0 = int(sh.cu_q[1] - sh.cu_q[0])
-    rng_bits = shard_inputs(sh, chunk=0 if sh.ring_chunks else None)
+    if sh.ring_chunks and sh.zigzag_sp:
+        q, do = zigzag_inputs(sh)
+        kv = [zigzag_inputs(sh, s) for s in range(sh.ring_chunks)]
+        k = np.concatenate([a for a, _ in kv])
+        v = np.concatenate([b for _, b in kv])
+        pos_k = np.concatenate([zigzag_step_positions(sh, s) for s in range(sh.ring_chunks)])
+        cu_q, cu_k = np.array([0, sh.T_q]), np.array([0, len(pos_k)])
+    elif sh.ring_chunks:
+        q, _, _, do = shard_inputs(sh, chunk=0)
+        kv = [shard_inputs(sh, chunk=c)[1:3] for c in range(sh.ring_chunks)]
+        k = np.concatenate([a for a, _ in kv])
+        v = np.concatenate([b for _, b in kv])
+        pos_k = np.concatenate([ring_chunk_positions(sh, c) for c in range(sh.ring_chunks)])
+        cu_q, cu_k = np.array([0, sh.T_q]), np.array([0, len(pos_k)])
+    else:
+        q, k, v, do = shard_inputs(sh)
+        pos_k, cu_q, cu_k = sh.pos_k, sh.cu_q, sh.cu_k
+    kw = dict(cu_q=cu_q, cu_k=cu_k, pos_q=sh.pos_q, pos_k=pos_k, H_loc=sh.H_loc,
+              head_offset=sh.head_offset, num_real_heads=sh.num_real_heads,
+              gqa_group=sh.gqa_group, kv_head_offset=sh.kv_head_offset, scale=sh.scale,
+              causal=sh.causal)
+    seg_q = oracle.segment_ids(cu_q, sh.T_q)
+    seg_k = oracle.segment_ids(cu_k, len(pos_k))
 
-    def run(L):
-        q, k, v, do = (oracle.bf16_bits_to_f64(x[:L]) for x in rng_bits)
-        cu = np.array([0, L])
-        pos = np.arange(L)
-        kw = dict(cu_q=cu, cu_k=cu, pos_q=pos, pos_k=pos, H_loc=sh.H_loc,
-                  head_offset=sh.head_offset, num_real_heads=sh.num_real_heads,
-                  gqa_group=sh.gqa_group, kv_head_offset=sh.kv_head_offset, scale=sh.scale)
-        t0 = time.perf_counter()
-        o, lse = oracle.attn_forward(q, k, v, **kw)
-        oracle.attn_backward(q, k, v, do, o=o, lse=lse, **kw)
-        return time.perf_counter() - t0
+    def pairs(rows):
+        n = 0
+        for b0 in range(0, len(rows), 256):
+            n += int(oracle.allowed_mask(rows[b0:b0 + 256], seg_q, seg_k, np.asarray(sh.pos_q),
+                                         np.asarray(pos_k), sh.causal).sum())
+        return n
+    return (q, k, v, do), kw, seg_q, pairs
 
-    L0 = min(1024, seg0)
-    t0 = run(L0)
-    L = int(min(seg0, L0 * math.sqrt(max(1.0, budget_s / max(t0, 1e-3)))))
-    L = max(L0, L // 256 * 256)
-    dt = run(L)
-    pairs = L * (L + 1) // 2
-    flops = 14.0 * sh.D * pairs * sh.n_real_loc
-    threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
-    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
-            "sample": (f"fp64 oracle fwd+bwd on the causal prefix L={L} of the first segment, "
-                       f"{sh.n_real_loc} real heads, D={sh.D}; {dt:.1f} s"),
-            "seconds": round(dt, 2)}
+
+def cpu_baseline(sh, st, budget_s=15.0):
+    """The fp64 oracle as it stands (forward, then its analytic backward) on a
+    bounded sample of the shard, on every host core this process may use:
+    evenly spaced query rows of the rank (a 32-row probe first, then as many
+    rows as fit the time budget), every real head, against all keys the
+    shard gives them.  Reported as the oracle's rate in the metric's unit
+    (14 D per allowed pair per real head over the sample), with the full
+    shard's oracle time extrapolated at that rate."""
+    import oracle
+    from threadpoolctl import threadpool_limits
+    cores = len(os.sched_getaffinity(0))
+    bits, kw, seg_q, pairs = monolithic_problem(sh)
+    q, k, v, do = (oracle.bf16_bits_to_f64(x) for x in bits)
+    valid = np.nonzero(seg_q >= 0)[0]
+
+    def run(m):
+        rows = valid[np.unique(np.linspace(0, len(valid) - 1, m).astype(np.int64))]
+        cu = np.concatenate([[0], np.cumsum(np.bincount(seg_q[rows], minlength=len(kw["cu_q"]) - 1))])
+        sub = dict(kw, cu_q=cu, pos_q=np.asarray(kw["pos_q"])[rows])
+        with threadpool_limits(limits=cores):
+            t0 = time.perf_counter()
+            o, lse = oracle.attn_forward(q[rows], k, v, **sub)
+            oracle.attn_backward(q[rows], k, v, do[rows], o=o, lse=lse, **sub)
+            dt = time.perf_counter() - t0
+        return rows, dt
+
+    m = min(32, len(valid))
+    rows, dt = run(m)
+    if dt < budget_s / 4 and m < len(valid):
+        m = int(min(len(valid), max(m + 1, m * budget_s / max(dt, 1e-3) * 0.8)))
+        rows, dt = run(m)
+    flops = 14.0 * sh.D * pairs(rows) * sh.n_real_loc
+    rate = flops / dt
+    return {"value": round(rate / 1e12, 6), "unit": "TFLOP/s", "cores": cores, "kind": "oracle",
+            "sample": (f"fp64 oracle forward + analytic backward on {len(rows)} evenly spaced of "
+                       f"the {len(valid)} query rows, {sh.n_real_loc} real heads, against all "
+                       f"{len(kw['pos_k'])} keys of the shard, D={sh.D}: {flops:.3e} FLOP "
+                       f"(14 D per allowed pair) in {dt:.1f} s"),
+            "cpu_model": cpu_model(), "seconds": round(dt, 2),
+            "full_shard_seconds_extrapolated": round(st.flops_metric / rate, 1)}
 
 
 def measure(sp, torch, name, steps, warmup, per_kernel=True, warmup_s=1.5, kernel_steps=10):
@@ -504,7 +575,8 @@ def main():
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD, choices=WORKLOADS)
     ap.add_argument("--all", action="store_true", help="one JSON line per workload")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--dummy-overhead", action="store_true")
+    ap.add_argument("--no-dummy-overhead", action="store_true",
+                    help="skip the dummy-slot overhead measurement (tiny and long Ulysses shards)")
     ap.add_argument("--warmup-seconds", type=float, default=1.5,
                     help="keep warming up until this much time has passed")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -577,38 +649,71 @@ def main():
             "kernels_steps": kernel_steps,
             "roofline": roof,
         }
-        if args.dummy_overhead and sh.n_real_loc < sh.H_loc:
-            out["dummy_overhead"] = dummy_overhead(sp, torch, sh, args.steps)
+        if not args.no_dummy_overhead and name == names[0]:
+            log("timing the dummy-slot overhead ...")
+            out["dummy_overhead"] = dummy_overhead(sp, torch)
         if not args.no_cpu_baseline and name == names[0]:
             log("timing the CPU oracle baseline ...")
-            out["cpu_baseline"] = cpu_baseline(sh)
+            cb = cpu_baseline(sh, st)
+            cb["gpu_speedup_at_this_rate"] = round(value / cb["value"], 1) if cb["value"] else None
+            out["cpu_baseline"] = cb
         print(json.dumps(out), flush=True)
 
 
-def dummy_overhead(sp, torch, sh, steps):
-    """fwd+bwd time with dummy slots vs the same real heads without them."""
-    res = {}
-    for tag, s in (("with_dummies", sh), ("without", sh.without_dummies())):
-        desc = lib_desc(sp, s)
-        q, k, v, do = (to_dev(torch, x) for x in shard_inputs(s))
-        o, lse = torch.empty_like(q), torch.empty((s.H_loc, s.T_q), dtype=torch.float32, device="cuda")
-        dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
-        wf = torch.empty(sp.sp_attn_workspace_size(desc, sp.SP_OP_FWD), dtype=torch.uint8, device="cuda")
-        wb = torch.empty(sp.sp_attn_workspace_size(desc, sp.SP_OP_BWD), dtype=torch.uint8, device="cuda")
+def dummy_overhead(sp, torch, names=DUMMY_WORKLOADS, target_s=0.6):
+    """Dummy-slot cost: attention fwd+bwd of a shard with dummy slots against
+    the same real heads described without them (same inputs), each call
+    pair timed with HIP events, the two variants alternating; medians."""
+    out = {}
+    for name in names:
+        sh = workload(name)
+        if sh.n_real_loc >= sh.H_loc:
+            continue
+        runs = {}
+        for tag, s in (("with_dummies", sh), ("without", sh.without_dummies())):
+            desc = lib_desc(sp, s)
+            q, k, v, do = (to_dev(torch, x) for x in shard_inputs(s))
+            o = torch.empty_like(q)
+            lse = torch.empty((s.H_loc, s.T_q), dtype=torch.float32, device="cuda")
+            dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+            wf = torch.empty(sp.sp_attn_workspace_size(desc, sp.SP_OP_FWD), dtype=torch.uint8,
+                             device="cuda")
+            wb = torch.empty(sp.sp_attn_workspace_size(desc, sp.SP_OP_BWD), dtype=torch.uint8,
+                             device="cuda")
 
-        def run():
-            sp.sp_attn_fwd(desc, q, k, v, o, lse, workspace=wf)
-            sp.sp_attn_bwd(desc, q, k, v, o, lse, do, dq=dq, dk=dk, dv=dv, workspace=wb)
-
-        run()
+            def run(desc=desc, q=q, k=k, v=v, do=do, o=o, lse=lse, dq=dq, dk=dk, dv=dv, wf=wf,
+                    wb=wb):
+                sp.sp_attn_fwd(desc, q, k, v, o, lse, workspace=wf)
+                sp.sp_attn_bwd(desc, q, k, v, o, lse, do, dq=dq, dk=dk, dv=dv, workspace=wb)
+            runs[tag] = run
+        for _ in range(5):
+            for r in runs.values():
+                r()
         torch.cuda.synchronize()
         t0 = time.perf_counter()
-        for _ in range(steps):
-            run()
+        runs["with_dummies"]()
         torch.cuda.synchronize()
-        res[tag + "_ms"] = round((time.perf_counter() - t0) * 1e3 / steps, 4)
-    res["overhead_pct"] = round(100.0 * (res["with_dummies_ms"] / res["without_ms"] - 1.0), 2)
-    return res
+        one = time.perf_counter() - t0
+        reps = int(max(20, min(2000, target_s / max(one, 1e-5) / 2)))
+        ev = {tag: [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                    for _ in range(reps)] for tag in runs}
+        for i in range(reps):
+            order = ("with_dummies", "without") if i % 2 == 0 else ("without", "with_dummies")
+            for tag in order:
+                a, b = ev[tag][i]
+                a.record()
+                runs[tag]()
+                b.record()
+        torch.cuda.synchronize()
+        med = {}
+        for tag in runs:
+            ts = sorted(a.elapsed_time(b) for a, b in ev[tag])
+            med[tag] = ts[len(ts) // 2]
+        out[name] = {"with_dummies_ms": round(med["with_dummies"], 4),
+                     "without_ms": round(med["without"], 4), "reps": reps,
+                     "dummy_slots": sh.H_loc - sh.n_real_loc, "slots": sh.H_loc,
+                     "overhead_pct": round(100.0 * (med["with_dummies"] / med["without"] - 1.0), 2)}
+    return out
 
 
 if __name__ == "__main__":

@@ -312,7 +312,11 @@ sp_status sp_f32_to_bf16(const float* src, void* dst, int64_t n, void* stream);
  *   SP_OP_BWD, dK/dV items: {k_begin, k_end, q_begin, q_end, delta, head,
  *       kv_head, 1}.
  * Writes at most `capacity` items to `items` (may be NULL) and the total
- * count to *n_items.
+ * count to *n_items.  Not listed: the zero fills of dummy query slots (and,
+ * for one query head per KV head, of KV heads no real query head reads),
+ * which the entry points put at the front of the same launch as fill items
+ * of up to 8192 rows (keys) of one head, so a rank with dummy slots
+ * launches no extra kernel.
  */
 #define SP_SCHED_ITEM_INTS 8
 sp_status sp_attn_schedule(const sp_attn_desc* desc, int32_t op, int32_t* items, int32_t capacity,

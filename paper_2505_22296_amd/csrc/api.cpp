@@ -244,6 +244,46 @@ void schedule_keys(const sp_attn_desc* d, const Problem& p, int BNK, int BQ,
   sort_items(items, out);
 }
 
+// Zero fills as work items of the same launch (no extra kernels): dummy
+// query slots (O = +0 and LSE = -inf, in the ring variant the accumulators'
+// identity; dQ = +0) and, in the direct dK/dV mode, KV heads no real query
+// head reads (dK = dV = +0).  One item covers kFillRows rows of one head;
+// the items go to the FRONT of the list, so they finish in microseconds on
+// a few CUs while the longest items start.
+std::vector<int32_t> row_fills(const sp_attn_desc* d, const Problem& p) {
+  std::vector<int32_t> out;
+  for (int y = p.n_real; y < d->H_loc; ++y)
+    for (int a = 0; a < d->T_q; a += spk::kFillRows) {
+      const int32_t it[kItemInts] = {a, std::min(a + spk::kFillRows, d->T_q), 0, 0, 0, y, 0,
+                                     spk::kItemFillQ};
+      out.insert(out.end(), it, it + kItemInts);
+    }
+  return out;
+}
+bool kv_unread(const Problem& p, int kv) { return p.n_real == 0 || p.kv_hi[kv] == p.kv_lo[kv]; }
+std::vector<int32_t> key_fills(const sp_attn_desc* d, const Problem& p) {
+  std::vector<int32_t> out;
+  if (!p.direct && p.n_real > 0) return out;  // the GQA reduction writes every KV head
+  for (int kv = 0; kv < d->Hkv_loc; ++kv) {
+    if (!kv_unread(p, kv)) continue;
+    for (int a = 0; a < d->T_k; a += spk::kFillRows) {
+      const int32_t it[kItemInts] = {a, std::min(a + spk::kFillRows, d->T_k), 0, 0, 0, 0, kv,
+                                     spk::kItemFillKV};
+      out.insert(out.end(), it, it + kItemInts);
+    }
+  }
+  return out;
+}
+void prepend(std::vector<int32_t> fills, std::vector<int32_t>& items) {
+  if (!fills.empty()) items.insert(items.begin(), fills.begin(), fills.end());
+}
+int n_unread_kv(const sp_attn_desc* d, const Problem& p) {
+  if (!p.direct && p.n_real > 0) return 0;
+  int n = 0;
+  for (int kv = 0; kv < d->Hkv_loc; ++kv) n += kv_unread(p, kv);
+  return n;
+}
+
 // Workspace layout.
 struct Layout {
   size_t items_dq = 0, items_kv = 0, neg_d = 0, lse2 = 0, part_k = 0, part_v = 0, total = 0;
@@ -279,17 +319,22 @@ Layout layout_for(const sp_attn_desc* d, const Problem& p, int op, size_t n_item
 
 // Item counts of schedule_rows with empty items included (the worst case
 // the workspace is sized for) and of schedule_keys, without building them.
+// (With the zero-fill items appended at launch.)
 size_t row_item_count(const sp_attn_desc* d, const Problem& p, int BM) {
   size_t per_head = 0;
   for (const Seg& g : p.segs) per_head += (size_t)((g.qb - g.qa) + BM - 1) / BM;
   per_head += (size_t)((d->T_q - p.q_pad) + BM - 1) / BM;
-  return per_head * (size_t)p.n_real;
+  const size_t fills =
+      (size_t)(d->H_loc - p.n_real) * (size_t)((d->T_q + spk::kFillRows - 1) / spk::kFillRows);
+  return per_head * (size_t)p.n_real + fills;
 }
 size_t key_item_count(const sp_attn_desc* d, const Problem& p, int BNK) {
   size_t per_head = 0;
   for (const Seg& g : p.segs_k) per_head += (size_t)((g.kb - g.ka) + BNK - 1) / BNK;
   per_head += (size_t)((d->T_k - p.k_pad) + BNK - 1) / BNK;
-  return per_head * (size_t)p.n_real;
+  const size_t fills =
+      (size_t)n_unread_kv(d, p) * (size_t)((d->T_k + spk::kFillRows - 1) / spk::kFillRows);
+  return per_head * (size_t)p.n_real + fills;
 }
 
 // Worst-case item counts (with empty items) for sizing.
@@ -331,17 +376,6 @@ sp_status check_ws(const Layout& L, void* ws, size_t ws_bytes) {
 }
 
 char* at(void* ws, size_t off) { return (char*)ws + off; }
-
-// Zero dummy query slots and give them LSE -inf.
-sp_status fill_dummies_fwd(const sp_attn_desc* d, const Problem& p, void* o, float* lse,
-                           hipStream_t st) {
-  if (p.n_real >= d->H_loc) return SP_OK;
-  if (o) SP_HIP(spk::launch_zero_heads_bf16(o, d->T_q, d->H_loc, p.D, p.n_real, d->H_loc, st));
-  if (lse)
-    SP_HIP(spk::launch_fill_f32(lse + (size_t)p.n_real * d->T_q,
-                                (int64_t)(d->H_loc - p.n_real) * d->T_q, -INFINITY, st));
-  return SP_OK;
-}
 
 }  // namespace
 
@@ -614,6 +648,7 @@ static sp_status fwd_common(const sp_attn_desc* d, const void* q, const void* k,
   const bool include_empty = !ring || init || o_out;
   std::vector<int32_t> items;
   schedule_rows(d, p, spk::kFwdBM, spk::kFwdBN, include_empty, items);
+  if (include_empty) prepend(row_fills(d, p), items);
   const int n_items = (int)(items.size() / kItemInts);
   hipStream_t st = (hipStream_t)stream;
   void* items_dev = nullptr;
@@ -646,16 +681,6 @@ static sp_status fwd_common(const sp_attn_desc* d, const void* q, const void* k,
     a.causal = d->causal;
     a.init = init;
     SP_HIP(spk::launch_attn_fwd(a, n_items, p.D, ring, st));
-  }
-  if (!ring) return fill_dummies_fwd(d, p, o, lse, st);
-  if (p.n_real < d->H_loc) {
-    if (init) {
-      SP_HIP(spk::launch_zero_heads_f32(o_acc, d->T_q, d->H_loc, p.D, p.n_real, d->H_loc, st));
-      SP_HIP(spk::launch_fill_f32(lse_acc + (size_t)p.n_real * d->T_q,
-                                  (int64_t)(d->H_loc - p.n_real) * d->T_q, -INFINITY, st));
-    }
-    if (o_out)
-      SP_HIP(spk::launch_zero_heads_bf16(o_out, d->T_q, d->H_loc, p.D, p.n_real, d->H_loc, st));
   }
   return SP_OK;
 }
@@ -704,19 +729,22 @@ sp_status sp_attn_bwd(const sp_attn_desc* d, const void* q, const void* k, const
   }
   std::vector<int32_t> it_dq, it_kv;
   schedule_rows(d, p, spk::kDqBM, spk::kDqBN, true, it_dq);
+  if (dq) prepend(row_fills(d, p), it_dq);  // a dq_acc's dummy slots stay untouched
   schedule_keys(d, p, spk::kDkdvBN, spk::kDkdvBQ, it_kv);
+  prepend(key_fills(d, p), it_kv);
   const size_t na = it_dq.size() / kItemInts, nb = it_kv.size() / kItemInts;
   Layout L = layout_for(d, p, SP_OP_BWD, na, nb);
   if ((s = check_ws(L, ws, ws_bytes)) != SP_OK) return s;
   hipStream_t st = (hipStream_t)stream;
   if ((s = refuse_capture(st)) != SP_OK) return s;
   const int D = p.D;
-  if (p.n_real > 0) {
+  {
     if ((s = upload(at(ws, L.items_dq), it_dq, st)) != SP_OK) return s;
     if ((s = upload(at(ws, L.items_kv), it_kv, st)) != SP_OK) return s;
     float* neg_d = (float*)at(ws, L.neg_d);
     float* lse2 = (float*)at(ws, L.lse2);
-    SP_HIP(spk::launch_rowdot(o, dout, lse, neg_d, lse2, d->T_q, d->H_loc, p.n_real, D, st));
+    if (p.n_real > 0)
+      SP_HIP(spk::launch_rowdot(o, dout, lse, neg_d, lse2, d->T_q, d->H_loc, p.n_real, D, st));
     const float sl2 = d->softmax_scale * 1.4426950408889634f;
     spk::DqArgs a{};
     a.q = (const uint16_t*)q; a.k = (const uint16_t*)k; a.v = (const uint16_t*)v;
@@ -738,7 +766,7 @@ sp_status sp_attn_bwd(const sp_attn_desc* d, const void* q, const void* k, const
     b.T_q = d->T_q; b.T_k = d->T_k; b.H = d->H_loc; b.Hkv = d->Hkv_loc;
     b.scale_log2 = sl2; b.scale = d->softmax_scale; b.causal = d->causal; b.direct = p.direct;
     SP_HIP(spk::launch_attn_dkdv(b, (int)nb, D, st));
-    if (!p.direct) {
+    if (!p.direct && p.n_real > 0) {
       spk::ReduceArgs r{};
       r.T = d->T_k; r.Hkv = d->Hkv_loc; r.D = D;
       for (int kv = 0; kv < d->Hkv_loc; ++kv) {
@@ -749,16 +777,6 @@ sp_status sp_attn_bwd(const sp_attn_desc* d, const void* q, const void* k, const
       SP_HIP(spk::launch_reduce_kv(b.part_v, dv, r, st));
     }
   }
-  // KV heads read by no real query head get zero gradients.
-  if (p.direct || p.n_real == 0) {
-    for (int kv = 0; kv < d->Hkv_loc; ++kv)
-      if (p.n_real == 0 || p.kv_hi[kv] == p.kv_lo[kv]) {
-        SP_HIP(spk::launch_zero_heads_bf16(dk, d->T_k, d->Hkv_loc, D, kv, kv + 1, st));
-        SP_HIP(spk::launch_zero_heads_bf16(dv, d->T_k, d->Hkv_loc, D, kv, kv + 1, st));
-      }
-  }
-  if (dq && p.n_real < d->H_loc)
-    SP_HIP(spk::launch_zero_heads_bf16(dq, d->T_q, d->H_loc, D, p.n_real, d->H_loc, st));
   return SP_OK;
 }
 

@@ -189,3 +189,26 @@ SP_DEV void wait_batches(int pending) {
     wait_vmcnt<0>();
   }
 }
+
+// Zero-fill work items (dummy query slots, unread KV heads): the whole
+// workgroup writes rows [r0, r1) of head h of a [T, H, D] tensor with 16-byte
+// stores, block-strided.  bf16 (zero = +0) and float32 variants.
+SP_DEV void fill_rows_bf16(uint16_t* x, int r0, int r1, int H, int h, int D, int tid, int nt) {
+  const int nch = D / 8;
+  const int64_t n = (int64_t)(r1 - r0) * nch;
+  for (int64_t e = tid; e < n; e += nt) {
+    const int64_t row = r0 + e / nch;
+    *(u32x4*)(x + (row * H + h) * D + (e % nch) * 8) = u32x4{0u, 0u, 0u, 0u};
+  }
+}
+SP_DEV void fill_rows_f32(float* x, int r0, int r1, int H, int h, int D, int tid, int nt) {
+  const int nch = D / 4;
+  const int64_t n = (int64_t)(r1 - r0) * nch;
+  for (int64_t e = tid; e < n; e += nt) {
+    const int64_t row = r0 + e / nch;
+    *(f32x4*)(x + (row * H + h) * D + (e % nch) * 4) = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+}
+SP_DEV void fill_span_f32(float* x, int n, float v, int tid, int nt) {
+  for (int e = tid; e < n; e += nt) x[e] = v;
+}

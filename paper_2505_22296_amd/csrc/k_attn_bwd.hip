@@ -64,6 +64,10 @@ __global__ __launch_bounds__(NTQ, 1) void attn_dq_kernel(DqArgs a) {
   const int q0 = it[0], q1 = it[1], k0 = it[2], k1 = it[3], delta = it[4], head = it[5],
             kvh = it[6];
   const int tid = threadIdx.x;
+  if (it[7] == kItemFillQ) {  // dummy slot of a bf16 dQ: +0
+    fill_rows_bf16(a.dq, q0, q1, a.H, head, D, tid, NTQ);
+    return;
+  }
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lane = tid & 63, hh = lane >> 5, l32 = lane & 31;
   const int row = q0 + w * 32 + l32;
@@ -485,6 +489,12 @@ SP_DEV void dkdv_body(const DkdvArgs& a, u32x4* smem, int w, int lane) {
 template <int D>
 __global__ __launch_bounds__(64 * 2 * NPF, 1) void attn_dkdv_kernel(DkdvArgs a) {
   __shared__ u32x4 smem[DkdvStage<D>::SMEM];
+  const int32_t* it = a.items + (int64_t)blockIdx.x * kItemInts;
+  if (it[7] == kItemFillKV) {  // KV head no real query head reads: dK = dV = +0
+    fill_rows_bf16(a.dk, it[0], it[1], a.Hkv, it[6], D, threadIdx.x, 64 * 2 * NPF);
+    fill_rows_bf16(a.dv, it[0], it[1], a.Hkv, it[6], D, threadIdx.x, 64 * 2 * NPF);
+    return;
+  }
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (w < NPF)

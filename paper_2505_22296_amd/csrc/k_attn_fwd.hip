@@ -66,6 +66,21 @@ __global__ __launch_bounds__(NT, 1) void attn_fwd_kernel(FwdArgs a) {
   const int q0 = it[0], q1 = it[1], k0 = it[2], k1 = it[3], delta = it[4], head = it[5],
             kvh = it[6];
   const int tid = threadIdx.x;
+  if (it[7] == kItemFillQ) {
+    // dummy slot: O = +0, LSE = -inf (ring: the accumulators' identity on the
+    // first chunk, and +0 in the bf16 copy)
+    if constexpr (!MERGE) {
+      fill_rows_bf16(a.o, q0, q1, a.H, head, D, tid, NT);
+      fill_span_f32(a.lse + (int64_t)head * a.T_q + q0, q1 - q0, neg_inf(), tid, NT);
+    } else {
+      if (a.init) {
+        fill_rows_f32(a.o_acc, q0, q1, a.H, head, D, tid, NT);
+        fill_span_f32(a.lse_acc + (int64_t)head * a.T_q + q0, q1 - q0, neg_inf(), tid, NT);
+      }
+      if (a.o_out) fill_rows_bf16(a.o_out, q0, q1, a.H, head, D, tid, NT);
+    }
+    return;
+  }
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lane = tid & 63, hh = lane >> 5, l32 = lane & 31;
   const int row = q0 + w * 32 + l32;

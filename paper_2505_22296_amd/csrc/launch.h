@@ -77,8 +77,13 @@ struct ReduceArgs {
 // Work item of the attention kernels: 8 int32.
 //   fwd / dq:  {q_begin, q_end, k_begin, k_end, delta, head, kv_head, 0}
 //   dk/dv:     {k_begin, k_end, q_begin, q_end, delta, head, kv_head, 1}
+//   zero fill of a dummy query slot (fwd / dq): {r_begin, r_end, 0, 0, 0, slot, 0, 2}
+//   zero fill of a KV head no real query head reads (dk/dv):
+//              {k_begin, k_end, 0, 0, 0, 0, kv_head, 3}
 // Causal visibility of key j from row i is j <= i + delta.
 static constexpr int kItemInts = 8;
+static constexpr int kItemFillQ = 2, kItemFillKV = 3;
+static constexpr int kFillRows = 8192;  // rows (keys) per zero-fill item
 
 struct FwdArgs {
   const uint16_t* q;   // [T_q, H, D]

@@ -314,6 +314,46 @@ def test_ring_rank_fwd_bwd(sp):
         assert_close(dvs[c], RdVs[c], f"ring dV chunk {c}")
 
 
+def test_ring_steps_with_dummy_slots(sp):
+    """Ring steps on a rank with dummy query slots (7 real heads padded to 8
+    for SP 2, rank 1: slot 3 is a dummy), the accumulators holding garbage
+    before the first chunk: after init the dummy slot is the merge identity
+    (O_acc = +0, LSE = -inf), later chunks leave it so, the bf16 copy of the
+    last chunk is +0 there, and the real slots match the oracle's ring fold.
+    The dummy fills are work items of the ring-step launch itself."""
+    import torch
+    C, r, H, D = 300, 1, 4, 64
+    base = make_shard("ring_dummy", C, C, D, H, 4, 7, 8, 7, 1, 0, [C], [C])
+    nr = base.n_real_loc
+    q = randn_bf16_bits((C, H, D), 61)
+    q[:, nr:] = 0
+    ks = [randn_bf16_bits((C, 1, D), 62 + c) for c in range(r + 1)]
+    vs = [randn_bf16_bits((C, 1, D), 64 + c) for c in range(r + 1)]
+    pos_q = r * C + np.arange(C)
+    o_acc = torch.full((C, H, D), float("nan"), dtype=torch.float32, device="cuda")
+    lse_acc = torch.full((H, C), 3.0, dtype=torch.float32, device="cuda")
+    o_bf = torch.full((C, H, D), 5.0, dtype=torch.bfloat16, device="cuda")
+    for c in range(r + 1):
+        d = lib_desc(base, pos_q=pos_q, pos_k=c * C + np.arange(C))
+        sp.sp_ring_step(d, to_dev(q), to_dev(ks[c]), to_dev(vs[c]), o_acc, lse_acc, init=(c == 0),
+                        o_out=o_bf if c == r else None)
+        if c == 0:
+            torch.cuda.synchronize()
+            assert torch.all(o_acc[:, nr:] == 0) and bool(torch.all(torch.isneginf(lse_acc[nr:])))
+    torch.cuda.synchronize()
+    assert np.all(o_acc[:, nr:].cpu().numpy().view(np.int32) == 0)
+    assert bool(torch.all(torch.isneginf(lse_acc[nr:])))
+    assert np.all(bits_from_dev(o_bf)[:, nr:] == 0)
+    common = dict(H_loc=H, head_offset=4, num_real_heads=7, gqa_group=7, kv_head_offset=0,
+                  scale=base.scale)
+    chunks = [(_dec(ks[c]), _dec(vs[c])) for c in range(r + 1)]
+    kvpos = [c * C + np.arange(C) for c in range(r + 1)]
+    RO, RL = oracle.ring_forward(_dec(q), chunks, q_pos=pos_q, kv_pos=kvpos, **common)
+    assert_close(o_acc[:, :nr].cpu().numpy().astype(np.float64), RO[:, :nr], "ring O acc")
+    assert_close(from_dev(o_bf)[:, :nr], RO[:, :nr], "ring O bf16")
+    assert np.abs(lse_acc[:nr].cpu().numpy() - RL[:nr]).max() <= LSE_MAX_ABS
+
+
 @pytest.mark.parametrize("D,Hkv", [(128, 2), (64, 4)])
 def test_zigzag_rank_fwd_bwd(sp, D, Hkv):
     """Zigzag ring (Section 3.2) with sp = 3 and 2*sp chunks of C tokens:
