@@ -115,6 +115,20 @@ enum { SP_OP_FWD = 0, SP_OP_BWD = 1, SP_OP_RING_STEP = 2 };
  * piece are padding as usual.
  */
 #define SP_DESC_SINGLE_SEQUENCE 1
+/*
+ * SP_DESC_ROWSTATS_READY (sp_attn_bwd only; ignored elsewhere): the per-row
+ * statistics of the backward -- D_i = dO_i . O_i and LSE_i log2(e) of every
+ * real query head -- are already in the workspace, left there by an earlier
+ * sp_attn_bwd on the same workspace for the same query rows (same q, o, lse
+ * and dout, same T_q, H_loc, head_offset and num_real_heads), ordered before
+ * this call on the stream; this call does not recompute them.  They sit at
+ * the start of the workspace whatever the keys, so a Ring-Attention
+ * backward (Section 2.1) forms them once: the first KV chunk's call without
+ * the flag, the other chunks' calls with it.  The library cannot check the
+ * premise: stale statistics give wrong gradients (never an out-of-bounds
+ * access).
+ */
+#define SP_DESC_ROWSTATS_READY 4
 
 typedef struct sp_attn_desc {
   int32_t T_q;              /* query tokens at this rank (rows of q, o, dq)         */
@@ -130,7 +144,7 @@ typedef struct sp_attn_desc {
   int32_t num_seqs;         /* segments (>= 0)                                       */
   int32_t causal;           /* 1 = causal by position inside a segment, 0 = full     */
   float softmax_scale;      /* multiplies q.k (callers pass 1/sqrt(D))               */
-  int32_t flags;            /* 0 or SP_DESC_SINGLE_SEQUENCE                          */
+  int32_t flags;            /* 0, SP_DESC_SINGLE_SEQUENCE | SP_DESC_ROWSTATS_READY   */
   const int32_t* cu_seqlens_q;   /* HOST, num_seqs + 1                               */
   const int32_t* cu_seqlens_k;   /* HOST, num_seqs + 1                               */
   const int32_t* position_ids_q; /* HOST, T_q, or NULL                               */

@@ -10,7 +10,8 @@ from ._lib import (Desc, SpError, load, status_string, sp_attn_workspace_size, s
                    sp_token_logprob, sp_token_logprob_bwd, sp_loss_reduce, SP_LOSS_SFT, SP_LOSS_DPO,
                    SP_KERNEL_TOKEN_LOGPROB, SP_KERNEL_TOKEN_LOGPROB_BWD,
                    SP_OK, SP_ERR_INVALID_ARG, SP_ERR_UNSUPPORTED, SP_ERR_WORKSPACE, SP_ERR_HIP,
-                   SP_OP_FWD, SP_OP_BWD, SP_OP_RING_STEP, SP_DESC_SINGLE_SEQUENCE, EXPORTED,
+                   SP_OP_FWD, SP_OP_BWD, SP_OP_RING_STEP, SP_DESC_SINGLE_SEQUENCE, SP_DESC_ROWSTATS_READY,
+                   EXPORTED,
                    LIB_PATH, SP_KERNEL_ATTN_FWD, SP_KERNEL_ATTN_DQ, SP_KERNEL_ATTN_DKDV,
                    SP_KERNEL_PACK, SP_KERNEL_UNPACK, SP_KERNEL_LSE_MERGE, SP_KERNEL_UNPACK_ADD)
 
@@ -22,7 +23,8 @@ __all__ = [
     "sp_token_logprob", "sp_token_logprob_bwd", "sp_loss_reduce", "SP_LOSS_SFT", "SP_LOSS_DPO",
     "SP_KERNEL_TOKEN_LOGPROB", "SP_KERNEL_TOKEN_LOGPROB_BWD",
     "SP_OK", "SP_ERR_INVALID_ARG", "SP_ERR_UNSUPPORTED", "SP_ERR_WORKSPACE", "SP_ERR_HIP",
-    "SP_OP_FWD", "SP_OP_BWD", "SP_OP_RING_STEP", "SP_DESC_SINGLE_SEQUENCE", "EXPORTED",
+    "SP_OP_FWD", "SP_OP_BWD", "SP_OP_RING_STEP", "SP_DESC_SINGLE_SEQUENCE",
+    "SP_DESC_ROWSTATS_READY", "EXPORTED",
     "LIB_PATH", "SP_KERNEL_ATTN_FWD", "SP_KERNEL_ATTN_DQ", "SP_KERNEL_ATTN_DKDV", "SP_KERNEL_PACK",
     "SP_KERNEL_UNPACK", "SP_KERNEL_LSE_MERGE", "SP_KERNEL_UNPACK_ADD",
 ]

@@ -103,7 +103,7 @@ sp_status single_sequence_runs(const sp_attn_desc* d, Problem& p) {
 
 sp_status validate(const sp_attn_desc* d, Problem& p) {
   if (!d) return SP_ERR_INVALID_ARG;
-  if (d->flags & ~SP_DESC_SINGLE_SEQUENCE) return SP_ERR_INVALID_ARG;
+  if (d->flags & ~(SP_DESC_SINGLE_SEQUENCE | SP_DESC_ROWSTATS_READY)) return SP_ERR_INVALID_ARG;
   const bool single = (d->flags & SP_DESC_SINGLE_SEQUENCE) != 0;
   if (d->T_q < 0 || d->T_k < 0 || d->T_q >= kMaxTokens || d->T_k >= kMaxTokens)
     return SP_ERR_INVALID_ARG;
@@ -304,10 +304,13 @@ Layout layout_for(const sp_attn_desc* d, const Problem& p, int op, size_t n_item
   if (op == SP_OP_FWD || op == SP_OP_RING_STEP) {
     L.items_dq = take(n_items_a * kItemInts * 4);
   } else {
-    L.items_dq = take(n_items_a * kItemInts * 4);
-    L.items_kv = take(n_items_b * kItemInts * 4);
+    // the row statistics first: their offsets depend on T_q and the real
+    // heads only, so calls over other KV chunks can reuse them
+    // (SP_DESC_ROWSTATS_READY)
     L.neg_d = take((size_t)std::max(p.n_real, 1) * d->T_q * 4);
     L.lse2 = take((size_t)std::max(p.n_real, 1) * d->T_q * 4);
+    L.items_dq = take(n_items_a * kItemInts * 4);
+    L.items_kv = take(n_items_b * kItemInts * 4);
     if (!p.direct) {
       L.part_k = take((size_t)p.n_real * d->T_k * D * 4);
       L.part_v = take((size_t)p.n_real * d->T_k * D * 4);
@@ -743,7 +746,7 @@ sp_status sp_attn_bwd(const sp_attn_desc* d, const void* q, const void* k, const
     if ((s = upload(at(ws, L.items_kv), it_kv, st)) != SP_OK) return s;
     float* neg_d = (float*)at(ws, L.neg_d);
     float* lse2 = (float*)at(ws, L.lse2);
-    if (p.n_real > 0)
+    if (p.n_real > 0 && !(d->flags & SP_DESC_ROWSTATS_READY))
       SP_HIP(spk::launch_rowdot(o, dout, lse, neg_d, lse2, d->T_q, d->H_loc, p.n_real, D, st));
     const float sl2 = d->softmax_scale * 1.4426950408889634f;
     spk::DqArgs a{};

@@ -3,10 +3,15 @@ bench.py times (same entry points, same tile schedule).
 
 The oracle evaluates sampled outputs one by one: O and LSE for sampled query
 rows, dQ for sampled rows, dK/dV for sampled keys near segment ends (only
-rows after them see those keys).  Over the whole arrays, properties that
-hold at any size are checked: per segment and KV head sum_j dK_j = 0 and
-sum_j dV_j = sum over the group's rows of dO_i (rows of P sum to one), and
-dummy slots are bit-zero."""
+rows after them see those keys) and for "deep" keys that ~15-16K rows see
+(the dK/dV kernel's longest accumulation: hundreds of query chunks summed in
+float32, each chunk's P exchanged as fp16).  For a deep key the oracle
+needs the full softmax row of every row that sees it, so it runs on the
+exact sub-problem that holds the key -- its segment (segments are
+independent), or one KV head's group of query heads (GQA groups are).  Over
+the whole arrays, properties that hold at any size are checked: per segment
+and KV head sum_j dK_j = 0 and sum_j dV_j = sum over the group's rows of
+dO_i (rows of P sum to one), and dummy slots are bit-zero."""
 import numpy as np
 import pytest
 
@@ -16,7 +21,7 @@ from tests.helpers import (LSE_MAX_ABS, assert_close, bits_from_dev, from_dev, l
 from workloads import (ring_chunk_positions, shard_inputs, workload, WORKLOADS, zigzag_inputs,
                        zigzag_step_positions)
 
-pytestmark = [pytest.mark.gpu, pytest.mark.timeout(300)]
+pytestmark = [pytest.mark.gpu, pytest.mark.timeout(420)]
 
 
 @pytest.fixture(scope="module")
@@ -46,6 +51,35 @@ def _tail_keys(sh, per_seg=4):
         if b - a >= 8:
             keys += [b - 1, b - 3, b - 40 if b - 40 >= a else a, b - 130 if b - 130 >= a else a][:per_seg]
     return np.array(sorted(set(keys)))
+
+
+def _deep_keys_check(sh, kw, qf, kf, vf, dof, gk, gv, nr, keys, seg):
+    """dK / dV of `keys` (all in segment `seg`, seen by many rows) against
+    the oracle on that segment alone (its rows, keys and positions)."""
+    import time
+    qa, qb = int(sh.cu_q[seg]), int(sh.cu_q[seg + 1])
+    ka, kb = int(sh.cu_k[seg]), int(sh.cu_k[seg + 1])
+    sub = dict(kw, cu_q=np.array([0, qb - qa]), cu_k=np.array([0, kb - ka]),
+               pos_q=np.asarray(kw["pos_q"])[qa:qb], pos_k=np.asarray(kw["pos_k"])[ka:kb])
+    t0 = time.perf_counter()
+    RdK, RdV = oracle.attn_dkdv_keys(qf[qa:qb], kf[ka:kb], vf[ka:kb], dof[qa:qb], keys - ka, **sub)
+    seen = [int(((np.asarray(kw["pos_k"])[k] <= sub["pos_q"]) if kw["causal"] else
+                 np.ones(qb - qa, bool)).sum()) for k in keys]
+    print(f"deep keys {keys.tolist()} seen by {seen} rows; oracle {time.perf_counter() - t0:.1f} s",
+          flush=True)
+    used = sorted({sh.kv_of(h) for h in range(nr)})
+    assert_close(from_dev(gk[keys])[:, used], RdK[:, used], "dK deep keys")
+    assert_close(from_dev(gv[keys])[:, used], RdV[:, used], "dV deep keys")
+
+
+def _deep_keys(sh):
+    """Two keys of the longest segment, at a quarter and half of it (causal:
+    the rows after them, ~3/4 and ~1/2 of the segment, see them), and the
+    segment's index."""
+    lens = np.diff(sh.cu_k)
+    seg = int(np.argmax(lens))
+    a, n = int(sh.cu_k[seg]), int(lens[seg])
+    return np.array([a + n // 4 + 3, a + n // 2 + 1]), seg
 
 
 def _grad_sums(sh, dk, dv, do, nr):
@@ -96,6 +130,9 @@ def test_fullsize_shard(sp, name):
     used = sorted({sh.kv_of(h) for h in range(nr)})
     assert_close(from_dev(gk[kidx])[:, used], RdK[:, used], "dK keys")
     assert_close(from_dev(gv[kidx])[:, used], RdV[:, used], "dV keys")
+    if sh.T_q >= 16384:
+        dkeys, seg = _deep_keys(sh)
+        _deep_keys_check(sh, kw, qf, kf, vf, dof, gk, gv, nr, dkeys, seg)
     _grad_sums(sh, from_dev(gk), from_dev(gv), dof, nr)
     if nr < sh.H_loc:
         assert torch.all(o[:, nr:].view(torch.int16) == 0)
@@ -128,8 +165,14 @@ def test_fullsize_ring_rank(sp):
                         o_out=o if c == n - 1 else None)
     dq_acc = torch.zeros((C, H, D), dtype=torch.float32, device="cuda")
     dks, dvs = [], []
+    # one workspace: the row statistics formed by chunk 0's call are reused
+    descs_b = [lib_desc(sh, pos_k=ring_chunk_positions(sh, c), rowstats_ready=c > 0)
+               for c in range(n)]
+    ws = torch.empty(max(sp.sp_attn_workspace_size(d, sp.SP_OP_BWD) for d in descs_b),
+                     dtype=torch.uint8, device="cuda")
     for c in range(n):
-        _, gk, gv = sp.sp_attn_bwd(descs[c], Q, Ks[c], Vs[c], o, lse, dO, dq_acc=dq_acc)
+        _, gk, gv = sp.sp_attn_bwd(descs_b[c], Q, Ks[c], Vs[c], o, lse, dO, dq_acc=dq_acc,
+                                   workspace=ws)
         dks.append(gk)
         dvs.append(gv)
     torch.cuda.synchronize()
@@ -155,6 +198,20 @@ def test_fullsize_ring_rank(sp):
     kl = torch.from_numpy(keys - (n - 1) * C).cuda()
     assert_close(from_dev(dks[-1][kl]), RdK, "ring dK keys")
     assert_close(from_dev(dvs[-1][kl]), RdV, "ring dV keys")
+    # deep keys: two keys of KV chunk 0, which all 16384 rows see (every row
+    # accumulates the whole chunk); the oracle on KV head 0's group of query
+    # heads (GQA groups are independent)
+    import time
+    g = sh.gqa_group
+    grp = dict(kw, H_loc=g, num_real_heads=g)
+    deep = np.array([100, C // 2 + 7])
+    t0 = time.perf_counter()
+    RdK0, RdV0 = oracle.attn_dkdv_keys(qf[:, :g], kcat[:, :1], vcat[:, :1], dof[:, :g], deep, **grp)
+    print(f"ring deep keys {deep.tolist()} (KV head 0, heads 0-{g - 1}, all {C} rows); "
+          f"oracle {time.perf_counter() - t0:.1f} s", flush=True)
+    kd = torch.from_numpy(deep).cuda()
+    assert_close(from_dev(dks[0][kd])[:, :1], RdK0, "ring dK deep keys")
+    assert_close(from_dev(dvs[0][kd])[:, :1], RdV0, "ring dV deep keys")
     # whole-array identities over all chunks
     dk_all = np.concatenate([from_dev(x) for x in dks])
     dv_all = np.concatenate([from_dev(x) for x in dvs])
@@ -193,8 +250,12 @@ def test_fullsize_zigzag_rank(sp, name):
                         o_out=o if s == n - 1 else None)
     dq_acc = torch.zeros((T, H, D), dtype=torch.float32, device="cuda")
     dks, dvs = [], []
+    descs_b = [lib_desc(sh, pos_k=pks[s], rowstats_ready=s > 0) for s in range(n)]
+    ws = torch.empty(max(sp.sp_attn_workspace_size(d, sp.SP_OP_BWD) for d in descs_b),
+                     dtype=torch.uint8, device="cuda")
     for s in range(n):
-        _, gk, gv = sp.sp_attn_bwd(descs[s], Q, Ks[s], Vs[s], o, lse, dO, dq_acc=dq_acc)
+        _, gk, gv = sp.sp_attn_bwd(descs_b[s], Q, Ks[s], Vs[s], o, lse, dO, dq_acc=dq_acc,
+                                   workspace=ws)
         dks.append(gk)
         dvs.append(gv)
     torch.cuda.synchronize()

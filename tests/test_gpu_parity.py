@@ -312,6 +312,17 @@ def test_ring_rank_fwd_bwd(sp):
     for c in range(r + 1):
         assert_close(dks[c], RdKs[c], f"ring dK chunk {c}")
         assert_close(dvs[c], RdVs[c], f"ring dV chunk {c}")
+    # the row statistics formed once (chunk 0) and reused by the other
+    # chunks' calls on one workspace: the same bits
+    ws = torch.empty(sp.sp_attn_workspace_size(lib_desc(base, pos_q=pos_q, pos_k=np.arange(C)),
+                                               sp.SP_OP_BWD), dtype=torch.uint8, device="cuda")
+    dq_acc2 = torch.zeros((C, H, D), dtype=torch.float32, device="cuda")
+    for c in range(r + 1):
+        d = lib_desc(base, pos_q=pos_q, pos_k=c * C + np.arange(C), rowstats_ready=c > 0)
+        _, gk, gv = sp.sp_attn_bwd(d, dq, to_dev(ks[c]), to_dev(vs[c]), o_bf, lse_acc, to_dev(do),
+                                   dq_acc=dq_acc2, workspace=ws)
+        assert np.array_equal(from_dev(gk), dks[c]) and np.array_equal(from_dev(gv), dvs[c])
+    assert np.array_equal(dq_acc2.cpu().numpy(), dq_acc.cpu().numpy())
 
 
 def test_ring_steps_with_dummy_slots(sp):
