@@ -8,6 +8,8 @@
 //     GQA reduction of per-query-head dK/dV partials.
 // All accesses are 16-byte vectors; consecutive lanes touch consecutive
 // 16-byte chunks of a row.
+#include <algorithm>
+
 #include "dev_common.h"
 #include "launch.h"
 
@@ -23,101 +25,199 @@ static inline int grid_for(int64_t n_threads) {
 }
 
 // ---------------------------------------------------------------- pack
-// dst[j, t, h, c] = src[t, map[j*Hd + h], c] or 0; c counts 16-byte chunks.
-__global__ __launch_bounds__(kBlock) void pack_kernel(const u32x4* __restrict__ src,
-                                                      u32x4* __restrict__ dst, PackArgs a) {
-  const int64_t n = (int64_t)a.sp * a.T * a.Hd * a.nch;
-  for (int64_t e = (int64_t)blockIdx.x * kBlock + threadIdx.x; e < n;
-       e += (int64_t)gridDim.x * kBlock) {
-    int c = (int)(e % a.nch);
-    int64_t r = e / a.nch;
-    int h = (int)(r % a.Hd);
-    r /= a.Hd;
-    int t = (int)(r % a.T);
-    int j = (int)(r / a.T);
-    int g = a.map[j * a.Hd + h];
-    u32x4 v = {0u, 0u, 0u, 0u};
-    if (g >= 0) v = src[((int64_t)t * a.Hs + g) * a.nch + c];
-    dst[e] = v;
+// The copies run one (destination slot or head) per grid row (blockIdx.y),
+// so the head map is read once per block at a uniform index; inside a block
+// thread e of the row handles 16-byte chunks e, e + kBlock, ... of the
+// T x nch (row, chunk) plane with 32-bit index arithmetic, loads issued
+// before stores.  Rows are 16 * nch bytes apart on both sides (whole cache
+// lines for D = 64 and 128).  Planes past 2^31 chunks take 64-bit indices.
+static constexpr int kPer = 4;  // 16-byte chunks per thread
+
+template <typename I>
+SP_DEV void plane_index(I e, int nch, int lg, I& t, int& c) {
+  if (lg >= 0) {
+    t = e >> lg;
+    c = (int)(e & (I)(nch - 1));
+  } else {
+    t = e / nch;
+    c = (int)(e % nch);
   }
 }
 
-// dst[t, g, c] = src[j, t, h, c] with inv[g] = j*Hs + h (every g named once).
+static inline int log2_or_neg(int n) {
+  return (n > 0 && (n & (n - 1)) == 0) ? __builtin_ctz(n) : -1;
+}
+
+// dst[j, t, h, c] = src[t, map[j*Hd + h], c] or 0 (blockIdx.y = j*Hd + h).
+template <typename I>
+__global__ __launch_bounds__(kBlock) void pack_kernel(const u32x4* __restrict__ src,
+                                                      u32x4* __restrict__ dst, PackArgs a,
+                                                      int lg) {
+  const int slot = blockIdx.y;
+  const int j = slot / a.Hd, h = slot - j * a.Hd;
+  const int g = a.map[slot];
+  const I n = (I)a.T * a.nch;
+  const I e0 = (I)blockIdx.x * (kBlock * kPer) + threadIdx.x;
+  u32x4 v[kPer];
+#pragma unroll
+  for (int k = 0; k < kPer; ++k) {
+    const I e = e0 + (I)k * kBlock;
+    v[k] = u32x4{0u, 0u, 0u, 0u};
+    if (g >= 0 && e < n) {
+      I t;
+      int c;
+      plane_index<I>(e, a.nch, lg, t, c);
+      v[k] = src[(t * a.Hs + g) * a.nch + c];
+    }
+  }
+#pragma unroll
+  for (int k = 0; k < kPer; ++k) {
+    const I e = e0 + (I)k * kBlock;
+    if (e < n) {
+      I t;
+      int c;
+      plane_index<I>(e, a.nch, lg, t, c);
+      dst[(((I)j * a.T + t) * a.Hd + h) * a.nch + c] = v[k];
+    }
+  }
+}
+
+// dst[t, g, c] = src[j, t, h, c] with map[g] = j*Hs + h (blockIdx.y = g).
+template <typename I>
 __global__ __launch_bounds__(kBlock) void unpack_kernel(const u32x4* __restrict__ src,
-                                                        u32x4* __restrict__ dst, PackArgs a) {
-  const int64_t n = (int64_t)a.T * a.Hd * a.nch;
-  for (int64_t e = (int64_t)blockIdx.x * kBlock + threadIdx.x; e < n;
-       e += (int64_t)gridDim.x * kBlock) {
-    int c = (int)(e % a.nch);
-    int64_t r = e / a.nch;
-    int g = (int)(r % a.Hd);
-    int t = (int)(r / a.Hd);
-    int s = a.map[g];
-    int j = s / a.Hs, h = s % a.Hs;
-    dst[e] = src[(((int64_t)j * a.T + t) * a.Hs + h) * a.nch + c];
+                                                        u32x4* __restrict__ dst, PackArgs a,
+                                                        int lg) {
+  const int g = blockIdx.y;
+  const int s = a.map[g];
+  const int j = s / a.Hs, h = s - j * a.Hs;
+  const I n = (I)a.T * a.nch;
+  const I e0 = (I)blockIdx.x * (kBlock * kPer) + threadIdx.x;
+  u32x4 v[kPer];
+#pragma unroll
+  for (int k = 0; k < kPer; ++k) {
+    const I e = e0 + (I)k * kBlock;
+    if (e < n) {
+      I t;
+      int c;
+      plane_index<I>(e, a.nch, lg, t, c);
+      v[k] = src[(((I)j * a.T + t) * a.Hs + h) * a.nch + c];
+    }
+  }
+#pragma unroll
+  for (int k = 0; k < kPer; ++k) {
+    const I e = e0 + (I)k * kBlock;
+    if (e < n) {
+      I t;
+      int c;
+      plane_index<I>(e, a.nch, lg, t, c);
+      dst[(t * a.Hd + g) * a.nch + c] = v[k];
+    }
   }
 }
 
 // dst[t, g, c] = sum over the slots s = j*Hs + h listed for g (ascending) of
 // src[j, t, h, c]: eight bf16 per 16-byte chunk, summed in float32 one slot
-// at a time, rounded once to bf16 (nearest-even); no slot gives +0.
+// at a time, rounded once to bf16 (nearest-even); no slot gives +0
+// (blockIdx.y = g).  Each thread has two chunks of the plane in flight and,
+// per chunk, up to eight slots' loads before the additions.
+template <typename I>
 __global__ __launch_bounds__(kBlock) void unpack_add_kernel(const u32x4* __restrict__ src,
                                                             u32x4* __restrict__ dst,
-                                                            PackAddArgs a) {
-  const int64_t n = (int64_t)a.T * a.Hd * a.nch;
-  for (int64_t e = (int64_t)blockIdx.x * kBlock + threadIdx.x; e < n;
-       e += (int64_t)gridDim.x * kBlock) {
-    const int c = (int)(e % a.nch);
-    const int64_t r = e / a.nch;
-    const int g = (int)(r % a.Hd);
-    const int t = (int)(r / a.Hd);
-    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-    auto load = [&](int i) {
-      const int s = a.slot[i];
-      const int j = s / a.Hs, h = s % a.Hs;
-      return src[(((int64_t)j * a.T + t) * a.Hs + h) * a.nch + c];
-    };
-    auto add = [&](const u32x4& v) {
+                                                            PackAddArgs a, int lg) {
+  constexpr int P = 2, NS = 8;
+  const int g = blockIdx.y;
+  const int i0 = a.start[g], i1 = a.start[g + 1];
+  const I n = (I)a.T * a.nch;
+  const I e0 = (I)blockIdx.x * (kBlock * P) + threadIdx.x;
+  auto add = [](float* acc, const u32x4& v) {
 #pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        acc[2 * k] += __uint_as_float(v[k] << 16);
-        acc[2 * k + 1] += __uint_as_float(v[k] & 0xffff0000u);
-      }
-    };
-    // the first four copies are loaded together (a KV head rarely has more),
-    // then added in slot order
-    const int i0 = a.start[g], i1 = a.start[g + 1];
-    u32x4 v[4];
+    for (int k = 0; k < 4; ++k) {
+      acc[2 * k] += __uint_as_float(v[k] << 16);
+      acc[2 * k + 1] += __uint_as_float(v[k] & 0xffff0000u);
+    }
+  };
+  float acc[P][8];
+  I t[P];
+  int c[P];
 #pragma unroll
-    for (int k = 0; k < 4; ++k)
-      if (i0 + k < i1) v[k] = load(i0 + k);
+  for (int p = 0; p < P; ++p) {
 #pragma unroll
-    for (int k = 0; k < 4; ++k)
-      if (i0 + k < i1) add(v[k]);
-    for (int i = i0 + 4; i < i1; ++i) add(load(i));
-    dst[e] = pack_bf16x8(acc[0], acc[1], acc[2], acc[3], acc[4], acc[5], acc[6], acc[7]);
+    for (int i = 0; i < 8; ++i) acc[p][i] = 0.f;
+    plane_index<I>(e0 + (I)p * kBlock, a.nch, lg, t[p], c[p]);
   }
+  for (int b = i0; b < i1; b += NS) {
+    u32x4 v[P][NS];
+#pragma unroll
+    for (int k = 0; k < NS; ++k) {
+      if (b + k < i1) {
+        const int s = a.slot[b + k];
+        const int j = s / a.Hs, h = s - j * a.Hs;
+#pragma unroll
+        for (int p = 0; p < P; ++p)
+          if (e0 + (I)p * kBlock < n)
+            v[p][k] = src[(((I)j * a.T + t[p]) * a.Hs + h) * a.nch + c[p]];
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < NS; ++k)
+      if (b + k < i1)
+#pragma unroll
+        for (int p = 0; p < P; ++p)
+          if (e0 + (I)p * kBlock < n) add(acc[p], v[p][k]);
+  }
+#pragma unroll
+  for (int p = 0; p < P; ++p)
+    if (e0 + (I)p * kBlock < n)
+      dst[(t[p] * a.Hd + g) * a.nch + c[p]] =
+          pack_bf16x8(acc[p][0], acc[p][1], acc[p][2], acc[p][3], acc[p][4], acc[p][5],
+                      acc[p][6], acc[p][7]);
 }
 
+// 32-bit indices when every chunk index of both tensors (plus a block's
+// overshoot) fits; x blocks of the grid must fit as well.
+static inline bool fits32(int64_t chunks) { return chunks + kBlock * kPer < ((int64_t)1 << 31); }
+static inline bool grid_ok(int64_t blocks) { return blocks <= 0x7fffffff; }
+
 hipError_t launch_pack(const void* src, void* dst, const PackArgs& a, hipStream_t st) {
-  int64_t n = (int64_t)a.sp * a.T * a.Hd * a.nch;
+  const int64_t n = (int64_t)a.T * a.nch;
   if (n == 0) return hipSuccess;
-  return sp_launch(kKPack, pack_kernel, dim3(grid_for(n)), dim3(kBlock), st, (const u32x4*)src,
-                   (u32x4*)dst, a);
+  const int64_t bx = (n + kBlock * kPer - 1) / (kBlock * kPer);
+  if (!grid_ok(bx)) return hipErrorInvalidValue;
+  const dim3 grid((unsigned)bx, a.sp * a.Hd);
+  const int lg = log2_or_neg(a.nch);
+  if (fits32(std::max((int64_t)a.Hs, (int64_t)a.sp * a.Hd) * n))
+    return sp_launch(kKPack, pack_kernel<int>, grid, dim3(kBlock), st, (const u32x4*)src,
+                     (u32x4*)dst, a, lg);
+  return sp_launch(kKPack, pack_kernel<int64_t>, grid, dim3(kBlock), st, (const u32x4*)src,
+                   (u32x4*)dst, a, lg);
 }
 
 hipError_t launch_unpack_add(const void* src, void* dst, const PackAddArgs& a, hipStream_t st) {
-  int64_t n = (int64_t)a.T * a.Hd * a.nch;
+  const int64_t n = (int64_t)a.T * a.nch;
   if (n == 0) return hipSuccess;
-  return sp_launch(kKUnpackAdd, unpack_add_kernel, dim3(grid_for(n)), dim3(kBlock), st,
-                   (const u32x4*)src, (u32x4*)dst, a);
+  const int64_t bx = (n + kBlock * 2 - 1) / (kBlock * 2);
+  if (!grid_ok(bx)) return hipErrorInvalidValue;
+  const dim3 grid((unsigned)bx, a.Hd);
+  const int lg = log2_or_neg(a.nch);
+  if (fits32(std::max((int64_t)a.sp * a.Hs, (int64_t)a.Hd) * n))
+    return sp_launch(kKUnpackAdd, unpack_add_kernel<int>, grid, dim3(kBlock), st,
+                     (const u32x4*)src, (u32x4*)dst, a, lg);
+  return sp_launch(kKUnpackAdd, unpack_add_kernel<int64_t>, grid, dim3(kBlock), st,
+                   (const u32x4*)src, (u32x4*)dst, a, lg);
 }
 
 hipError_t launch_unpack(const void* src, void* dst, const PackArgs& a, hipStream_t st) {
-  int64_t n = (int64_t)a.T * a.Hd * a.nch;
+  const int64_t n = (int64_t)a.T * a.nch;
   if (n == 0) return hipSuccess;
-  return sp_launch(kKUnpack, unpack_kernel, dim3(grid_for(n)), dim3(kBlock), st,
-                   (const u32x4*)src, (u32x4*)dst, a);
+  const int64_t bx = (n + kBlock * kPer - 1) / (kBlock * kPer);
+  if (!grid_ok(bx)) return hipErrorInvalidValue;
+  const dim3 grid((unsigned)bx, a.Hd);
+  const int lg = log2_or_neg(a.nch);
+  if (fits32(std::max((int64_t)a.sp * a.Hs, (int64_t)a.Hd) * n))
+    return sp_launch(kKUnpack, unpack_kernel<int>, grid, dim3(kBlock), st, (const u32x4*)src,
+                     (u32x4*)dst, a, lg);
+  return sp_launch(kKUnpack, unpack_kernel<int64_t>, grid, dim3(kBlock), st, (const u32x4*)src,
+                   (u32x4*)dst, a, lg);
 }
 
 // ---------------------------------------------------------------- merge
