@@ -591,6 +591,20 @@ def bandwidth(sp, torch, reps=24):
     return out
 
 
+def recorded_workloads(path):
+    """Workloads that already have a line in the JSONL file `path` (none if
+    the file is absent); a line cut short by an interrupted run is ignored."""
+    done = set()
+    if path and os.path.exists(path):
+        with open(path) as f:
+            for line in f:
+                try:
+                    done.add(json.loads(line)["config"]["workload"])
+                except (ValueError, KeyError, TypeError):
+                    pass
+    return done
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -607,6 +621,9 @@ def main():
                     help="run one 1 GiB device copy first (counter scaling)")
     ap.add_argument("--bandwidth", action="store_true",
                     help="only measure the pack / unpack / LSE-merge kernels (one JSON line each)")
+    ap.add_argument("--jsonl", default=None,
+                    help="also append each workload's line to this file; workloads already "
+                         "recorded there are skipped, so a rerun resumes an interrupted --all")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path "
@@ -622,7 +639,11 @@ def main():
             print(json.dumps(rec), flush=True)
         return
     names = WORKLOADS if args.all else [args.workload]
+    done = recorded_workloads(args.jsonl)
     for name in names:
+        if name in done:
+            log(f"{name}: already in {args.jsonl}, skipped")
+            continue
         kernel_steps = 10
         sh, st, ms, ks_dom, ks, per_step = measure(sp, torch, name, args.steps, args.warmup,
                                                    warmup_s=args.warmup_seconds,
@@ -682,6 +703,9 @@ def main():
             cb["gpu_speedup_at_this_rate"] = round(value / cb["value"], 1) if cb["value"] else None
             out["cpu_baseline"] = cb
         print(json.dumps(out), flush=True)
+        if args.jsonl:
+            with open(args.jsonl, "a") as f:
+                f.write(json.dumps(out) + "\n")
 
 
 def dummy_overhead(sp, torch, names=DUMMY_WORKLOADS, target_s=0.6):

@@ -95,7 +95,11 @@ enum { SP_OP_FWD = 0, SP_OP_BWD = 1, SP_OP_RING_STEP = 2 };
  * included).  Inside each segment positions must be a +1 ramp; only each
  * segment's first position matters, so ring chunks express their global
  * offsets here (Q chunk r at r*C.., KV chunk c at c*C..).  NULL means
- * positions 0,1,.. restarting at every segment.
+ * positions 0,1,.. restarting at every segment.  Every call checks the ramps
+ * (O(T) host work, SP_ERR_INVALID_ARG on a break) unless the environment
+ * holds SPATTN_VALIDATE=0 when the library first validates a descriptor;
+ * then only each segment's first position is read, and a broken ramp gives
+ * a wrong mask, never an out-of-bounds access.
  *
  * Limits.  T_q, T_k < 2^30 and, per segment, |(first key position - first
  * key index) - (first query position - first query index)| <= 2^30

@@ -15,6 +15,7 @@
 #include <atomic>
 #include <cmath>
 #include <cstdint>
+#include <cstdlib>
 #include <cstring>
 #include <mutex>
 #include <vector>
@@ -101,6 +102,18 @@ sp_status single_sequence_runs(const sp_attn_desc* d, Problem& p) {
   return SP_OK;
 }
 
+// The O(T) checks that every segment's positions form a +1 ramp run unless
+// the environment sets SPATTN_VALIDATE=0 (read once per process); without
+// them only each segment's first position is read, and a malformed ramp
+// gives a wrong mask, never an out-of-bounds access.
+bool ramp_checks() {
+  static const bool on = [] {
+    const char* e = std::getenv("SPATTN_VALIDATE");
+    return !(e && e[0] == '0' && e[1] == '\0');
+  }();
+  return on;
+}
+
 sp_status validate(const sp_attn_desc* d, Problem& p) {
   if (!d) return SP_ERR_INVALID_ARG;
   if (d->flags & ~(SP_DESC_SINGLE_SEQUENCE | SP_DESC_ROWSTATS_READY)) return SP_ERR_INVALID_ARG;
@@ -161,14 +174,16 @@ sp_status validate(const sp_attn_desc* d, Problem& p) {
       int64_t pq = g.qa, pk = g.ka;  // default: positions restart at 0 per segment
       if (d->position_ids_q && g.qb > g.qa) {
         const int32_t* pos = d->position_ids_q;
-        for (int i = g.qa + 1; i < g.qb; ++i)
-          if ((int64_t)pos[i] != (int64_t)pos[i - 1] + 1) return SP_ERR_INVALID_ARG;
+        if (ramp_checks())
+          for (int i = g.qa + 1; i < g.qb; ++i)
+            if ((int64_t)pos[i] != (int64_t)pos[i - 1] + 1) return SP_ERR_INVALID_ARG;
         pq = (int64_t)g.qa - pos[g.qa];
       }
       if (d->position_ids_k && g.kb > g.ka) {
         const int32_t* pos = d->position_ids_k;
-        for (int i = g.ka + 1; i < g.kb; ++i)
-          if ((int64_t)pos[i] != (int64_t)pos[i - 1] + 1) return SP_ERR_INVALID_ARG;
+        if (ramp_checks())
+          for (int i = g.ka + 1; i < g.kb; ++i)
+            if ((int64_t)pos[i] != (int64_t)pos[i - 1] + 1) return SP_ERR_INVALID_ARG;
         pk = (int64_t)g.ka - pos[g.ka];
       }
       // key j visible from row i iff pos_k[j] <= pos_q[i]
