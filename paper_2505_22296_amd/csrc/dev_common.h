@@ -31,6 +31,13 @@ SP_DEV f32x16 mfma32(const u32x4& a, const u32x4& b, const f32x16& c) {
 }
 
 // Round 8 floats to bf16 (RNE, v_cvt_pk_bf16_f32) and pack into 16 bytes.
+// Streaming 16-byte accesses for data a kernel touches exactly once (the
+// Ulysses copies, the logits of the loss path): non-temporal loads and
+// stores, so the lines are not kept in the caches for reuse that never
+// comes (measured 1.1-1.25x the bandwidth of plain accesses on these copies).
+SP_DEV u32x4 ld_stream(const u32x4* p) { return __builtin_nontemporal_load(p); }
+SP_DEV void st_stream(const u32x4& v, u32x4* p) { __builtin_nontemporal_store(v, p); }
+
 SP_DEV u32x4 pack_bf16x8(float a0, float a1, float a2, float a3, float a4, float a5, float a6,
                          float a7) {
   f32x8 v = {a0, a1, a2, a3, a4, a5, a6, a7};

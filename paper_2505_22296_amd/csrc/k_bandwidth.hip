@@ -28,8 +28,8 @@ static inline int grid_for(int64_t n_threads) {
 // The copies run one (destination slot or head) per grid row (blockIdx.y),
 // so the head map is read once per block at a uniform index; inside a block
 // thread e of the row handles 16-byte chunks e, e + kBlock, ... of the
-// T x nch (row, chunk) plane with 32-bit index arithmetic, loads issued
-// before stores.  Rows are 16 * nch bytes apart on both sides (whole cache
+// T x nch (row, chunk) plane with 32-bit index arithmetic, streaming loads
+// issued before streaming stores.  Rows are 16 * nch bytes apart on both sides (whole cache
 // lines for D = 64 and 128).  Planes past 2^31 chunks take 64-bit indices.
 static constexpr int kPer = 4;  // 16-byte chunks per thread
 
@@ -67,7 +67,7 @@ __global__ __launch_bounds__(kBlock) void pack_kernel(const u32x4* __restrict__ 
       I t;
       int c;
       plane_index<I>(e, a.nch, lg, t, c);
-      v[k] = src[(t * a.Hs + g) * a.nch + c];
+      v[k] = ld_stream(&src[(t * a.Hs + g) * a.nch + c]);
     }
   }
 #pragma unroll
@@ -77,7 +77,7 @@ __global__ __launch_bounds__(kBlock) void pack_kernel(const u32x4* __restrict__ 
       I t;
       int c;
       plane_index<I>(e, a.nch, lg, t, c);
-      dst[(((I)j * a.T + t) * a.Hd + h) * a.nch + c] = v[k];
+      st_stream(v[k], &dst[(((I)j * a.T + t) * a.Hd + h) * a.nch + c]);
     }
   }
 }
@@ -100,7 +100,7 @@ __global__ __launch_bounds__(kBlock) void unpack_kernel(const u32x4* __restrict_
       I t;
       int c;
       plane_index<I>(e, a.nch, lg, t, c);
-      v[k] = src[(((I)j * a.T + t) * a.Hs + h) * a.nch + c];
+      v[k] = ld_stream(&src[(((I)j * a.T + t) * a.Hs + h) * a.nch + c]);
     }
   }
 #pragma unroll
@@ -110,7 +110,7 @@ __global__ __launch_bounds__(kBlock) void unpack_kernel(const u32x4* __restrict_
       I t;
       int c;
       plane_index<I>(e, a.nch, lg, t, c);
-      dst[(t * a.Hd + g) * a.nch + c] = v[k];
+      st_stream(v[k], &dst[(t * a.Hd + g) * a.nch + c]);
     }
   }
 }
@@ -155,7 +155,7 @@ __global__ __launch_bounds__(kBlock) void unpack_add_kernel(const u32x4* __restr
 #pragma unroll
         for (int p = 0; p < P; ++p)
           if (e0 + (I)p * kBlock < n)
-            v[p][k] = src[(((I)j * a.T + t[p]) * a.Hs + h) * a.nch + c[p]];
+            v[p][k] = ld_stream(&src[(((I)j * a.T + t[p]) * a.Hs + h) * a.nch + c[p]]);
       }
     }
 #pragma unroll
@@ -168,9 +168,9 @@ __global__ __launch_bounds__(kBlock) void unpack_add_kernel(const u32x4* __restr
 #pragma unroll
   for (int p = 0; p < P; ++p)
     if (e0 + (I)p * kBlock < n)
-      dst[(t[p] * a.Hd + g) * a.nch + c[p]] =
-          pack_bf16x8(acc[p][0], acc[p][1], acc[p][2], acc[p][3], acc[p][4], acc[p][5],
-                      acc[p][6], acc[p][7]);
+      st_stream(pack_bf16x8(acc[p][0], acc[p][1], acc[p][2], acc[p][3], acc[p][4], acc[p][5],
+                            acc[p][6], acc[p][7]),
+                &dst[(t[p] * a.Hd + g) * a.nch + c[p]]);
 }
 
 // 32-bit indices when every chunk index of both tensors (plus a block's

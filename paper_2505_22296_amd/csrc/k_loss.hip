@@ -56,7 +56,7 @@ __global__ __launch_bounds__(kLB) void token_logprob_kernel(LossArgs a, const u3
   for (; c + 3 * kLB < nch; c += 4 * kLB) {  // four loads in flight
     u32x4 v[4];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) v[u] = row[c + u * kLB];
+    for (int u = 0; u < 4; ++u) v[u] = ld_stream(&row[c + u * kLB]);
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       float x[8];
@@ -148,14 +148,14 @@ __global__ __launch_bounds__(kLB) void token_logprob_bwd_kernel(LossArgs a, cons
   const float ng = -g;
   for (int c = threadIdx.x; c < nch; c += kLB) {
     float x[8];
-    decode8(logits[base + c], x);
+    decode8(ld_stream(&logits[base + c]), x);
     float d[8];
 #pragma unroll
     for (int k = 0; k < 8; ++k) {
       d[k] = ng * __builtin_amdgcn_exp2f(__builtin_fmaf(x[k], kLog2e, -b));
       if (c * 8 + k == lab) d[k] += g;
     }
-    dlogits[base + c] = pack_bf16x8(d[0], d[1], d[2], d[3], d[4], d[5], d[6], d[7]);
+    st_stream(pack_bf16x8(d[0], d[1], d[2], d[3], d[4], d[5], d[6], d[7]), &dlogits[base + c]);
   }
 }
 
