@@ -74,12 +74,12 @@ class KernelTimers:
             b.record()
             self.pool.append((a, b))
 
-    def arm(self, kid, flops):
+    def arm(self, kid, flops, nbytes=0.0):
         if not self.on or (self.only is not None and kid not in self.only):
             return
         self.reserve(len(self.used) + 1)
         pair = self.pool[len(self.used)]
-        self.used.append((kid, flops, pair))
+        self.used.append((kid, flops, nbytes, pair))
         self.sp.sp_profile_events(kid, *pair)
 
     def disarm(self):
@@ -88,12 +88,13 @@ class KernelTimers:
 
     def summary(self):
         out = {}
-        for kid, flops, (a, b) in self.used:
+        for kid, flops, nbytes, (a, b) in self.used:
             ms = a.elapsed_time(b)
-            s = out.setdefault(kid, {"ms": 0.0, "n": 0, "flops": 0.0, "all": []})
+            s = out.setdefault(kid, {"ms": 0.0, "n": 0, "flops": 0.0, "bytes": 0.0, "all": []})
             s["ms"] += ms
             s["n"] += 1
             s["flops"] += flops
+            s["bytes"] += nbytes
             s["all"].append(ms)
         return out
 
@@ -215,6 +216,14 @@ class Step:
             self.mha = sh.hkv == sh.hs
             self.kmap = self.qmap if self.mha else ulysses_kv_head_map(sh.hs, sh.hkv, sh.sp)
             self.kw = len(self.kmap) // sh.sp
+            # algorithmic bytes of each copy: named slots read, every slot
+            # (dummies as zeros) written; the unpacks read named slots only
+            row = Tl * D * 2
+            named_q, named_kv = int(np.sum(self.qmap >= 0)), int(np.sum(self.kmap >= 0))
+            self.bytes_pack_q = row * (named_q + len(self.qmap))
+            self.bytes_pack_kv = row * (named_kv + len(self.kmap))
+            self.bytes_unpack_q = row * 2 * named_q
+            self.bytes_unpack_add = row * (named_kv + sh.hkv)
             self.send_q = torch.empty((sh.sp, Tl, sh.H_loc, D), dtype=torch.bfloat16, device=dev)
             self.send_do = torch.empty_like(self.send_q)
             self.send_k = torch.empty((sh.sp, Tl, self.kw, D), dtype=torch.bfloat16, device=dev)
@@ -233,11 +242,11 @@ class Step:
     def run(self):
         sp, t, sh = self.sp, self.t, self.sh
         if self.ulysses:
-            t.arm(sp.SP_KERNEL_PACK, 0.0)
+            t.arm(sp.SP_KERNEL_PACK, 0.0, self.bytes_pack_q)
             sp.sp_ulysses_pack(self.q_pre, sh.sp, sh.H_loc, self.qmap, dst=self.send_q)
-            t.arm(sp.SP_KERNEL_PACK, 0.0)
+            t.arm(sp.SP_KERNEL_PACK, 0.0, self.bytes_pack_kv)
             sp.sp_ulysses_pack(self.k_pre, sh.sp, self.kw, self.kmap, dst=self.send_k)
-            t.arm(sp.SP_KERNEL_PACK, 0.0)
+            t.arm(sp.SP_KERNEL_PACK, 0.0, self.bytes_pack_kv)
             sp.sp_ulysses_pack(self.v_pre, sh.sp, self.kw, self.kmap, dst=self.send_v)
         if self.ring:
             n = len(self.descs)
@@ -251,10 +260,10 @@ class Step:
             sp.sp_attn_fwd(self.desc, self.q, self.k, self.v, self.o, self.lse,
                            workspace=self.ws_f)
         if self.ulysses:
-            t.arm(sp.SP_KERNEL_UNPACK, 0.0)
+            t.arm(sp.SP_KERNEL_UNPACK, 0.0, self.bytes_unpack_q)
             sp.sp_ulysses_unpack(self.o.view(sh.sp, self.Tl, sh.H_loc, sh.D), self.qmap, sh.hs,
                                  dst=self.o_pre)
-            t.arm(sp.SP_KERNEL_PACK, 0.0)
+            t.arm(sp.SP_KERNEL_PACK, 0.0, self.bytes_pack_q)
             sp.sp_ulysses_pack(self.do_pre, sh.sp, sh.H_loc, self.qmap, dst=self.send_do)
         if self.ring:
             self.dq_acc.zero_()
@@ -271,20 +280,20 @@ class Step:
             sp.sp_attn_bwd(self.desc, self.q, self.k, self.v, self.o, self.lse, self.do,
                            dq=self.dq, dk=self.dk, dv=self.dv, workspace=self.ws_b)
         if self.ulysses:
-            t.arm(sp.SP_KERNEL_UNPACK, 0.0)
+            t.arm(sp.SP_KERNEL_UNPACK, 0.0, self.bytes_unpack_q)
             sp.sp_ulysses_unpack(self.dq.view(sh.sp, self.Tl, sh.H_loc, sh.D), self.qmap, sh.hs,
                                  dst=self.dq_pre)
             if self.mha and not self.ring:
-                t.arm(sp.SP_KERNEL_UNPACK, 0.0)
+                t.arm(sp.SP_KERNEL_UNPACK, 0.0, self.bytes_unpack_q)
                 sp.sp_ulysses_unpack(self.dk.view(sh.sp, self.Tl, sh.H_loc, sh.D), self.qmap,
                                      sh.hkv, dst=self.dk_pre)
-                t.arm(sp.SP_KERNEL_UNPACK, 0.0)
+                t.arm(sp.SP_KERNEL_UNPACK, 0.0, self.bytes_unpack_q)
                 sp.sp_ulysses_unpack(self.dv.view(sh.sp, self.Tl, sh.H_loc, sh.D), self.qmap,
                                      sh.hkv, dst=self.dv_pre)
             elif not self.mha:
-                t.arm(sp.SP_KERNEL_UNPACK_ADD, 0.0)
+                t.arm(sp.SP_KERNEL_UNPACK_ADD, 0.0, self.bytes_unpack_add)
                 sp.sp_ulysses_unpack_add(self.recv_dk, self.kmap, sh.hkv, dst=self.dk_pre)
-                t.arm(sp.SP_KERNEL_UNPACK_ADD, 0.0)
+                t.arm(sp.SP_KERNEL_UNPACK_ADD, 0.0, self.bytes_unpack_add)
                 sp.sp_ulysses_unpack_add(self.recv_dv, self.kmap, sh.hkv, dst=self.dv_pre)
 
 
@@ -481,7 +490,7 @@ def bandwidth(sp, torch, reps=24):
     previous call); the single-call event median, which adds one dispatch
     gap per call, is reported beside it."""
     out = []
-    HBM_PEAK = 8000.0  # GB/s
+    HBM_PEAK = PEAK_HBM_GBS
 
     def run(label, nbytes, sets, call, batch=16):
         n = max(4, -(-(1 << 30) // max(nbytes, 1)) + 1)
@@ -661,8 +670,10 @@ def main():
                                  "tflops": round(s["flops"] / s["n"] / (avg * 1e-3) / 1e12, 1)
                                  if s["flops"] else None,
                                  "tflops_at_median": round(s["flops"] / s["n"] / (med * 1e-3) / 1e12, 1)
-                                 if s["flops"] else None}
-        if dom:
+                                 if s["flops"] else None,
+                                 "gb_per_s": round(s["bytes"] / s["n"] / (avg * 1e-3) / 1e9, 1)
+                                 if s["bytes"] else None}
+        if dom and dom[1]["flops"] > 0:
             kid, s = dom
             avg_s = s["ms"] / s["n"] * 1e-3
             ach = s["flops"] / s["n"] / avg_s / 1e12
@@ -672,6 +683,15 @@ def main():
                     "traffic": measured_traffic(KNAMES[kid], name),
                     "avg_launch_ms": round(s["ms"] / s["n"], 4),
                     "flops_per_launch": s["flops"] / s["n"]}
+        elif dom:  # a copy kernel dominates (launch-bound shapes): HBM roofline
+            kid, s = dom
+            avg_s = s["ms"] / s["n"] * 1e-3
+            ach = s["bytes"] / s["n"] / avg_s / 1e9
+            roof = {"bound": "hbm", "kernel": KNAMES[kid], "achieved": round(ach, 1),
+                    "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBS, 4),
+                    "traffic": measured_traffic(KNAMES[kid], name),
+                    "avg_launch_ms": round(s["ms"] / s["n"], 4),
+                    "bytes_per_launch": s["bytes"] / s["n"]}
         out = {
             "metric": METRIC, "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1,
             "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
