@@ -480,10 +480,10 @@ def copy_calibration(torch, nbytes=1 << 30):
 
 def bandwidth(sp, torch, reps=24):
     """GB/s of the bandwidth kernels at the workloads' shapes: the Ulysses
-    pack/unpack and the summing K/V-gradient unpack of the 7B-like (c1) and
-    long (c4) shards, the loss path's token log-probs and their backward
-    (4096 tokens x 152064 vocabulary), and the fp32 LSE
-    merge of the ring shard (c3).  Buffer sets rotate (>= 4 sets, > 1 GB in
+    pack/unpack and the summing K/V-gradient unpack of the 7B-like and the
+    long Ulysses shards, the loss path's token log-probs and their backward
+    (4096 tokens x 152064 vocabulary), and the fp32 LSE merge of the ring
+    rank's Q chunk.  Buffer sets rotate (>= 4 sets, > 1 GB in
     total) so that the 256 MB last-level cache cannot serve repeats.  GB/s
     comes from batches of back-to-back calls between one HIP event pair (as
     the calls run inside a step, each launch's dispatch overlapping the
