@@ -757,8 +757,15 @@ sp_status sp_attn_bwd(const sp_attn_desc* d, const void* q, const void* k, const
   if ((s = refuse_capture(st)) != SP_OK) return s;
   const int D = p.D;
   {
-    if ((s = upload(at(ws, L.items_dq), it_dq, st)) != SP_OK) return s;
-    if ((s = upload(at(ws, L.items_kv), it_kv, st)) != SP_OK) return s;
+    // both work lists in one copy (they are adjacent in the workspace): every
+    // host-to-device copy sits between two kernels on the stream
+    {
+      const size_t gap = (L.items_kv - L.items_dq) / sizeof(int32_t);
+      std::vector<int32_t> both(gap + it_kv.size(), 0);
+      std::copy(it_dq.begin(), it_dq.end(), both.begin());
+      std::copy(it_kv.begin(), it_kv.end(), both.begin() + gap);
+      if ((s = upload(at(ws, L.items_dq), both, st)) != SP_OK) return s;
+    }
     float* neg_d = (float*)at(ws, L.neg_d);
     float* lse2 = (float*)at(ws, L.lse2);
     if (p.n_real > 0 && !(d->flags & SP_DESC_ROWSTATS_READY))
