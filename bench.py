@@ -103,8 +103,9 @@ KNAMES = {1: "attn_fwd_kernel", 2: "attn_dq_kernel", 3: "attn_dkdv_kernel", 4: "
           5: "unpack_kernel", 6: "merge_kernel", 7: "unpack_add_kernel"}
 
 
-def lib_desc(sp, sh, pos_k=None, rowstats_ready=False):
-    return sp.Desc(rowstats_ready=rowstats_ready, T_q=sh.T_q, T_k=sh.T_k, head_dim=sh.D, H_loc=sh.H_loc,
+def lib_desc(sp, sh, pos_k=None, rowstats_ready=False, dq_acc_init=False):
+    return sp.Desc(rowstats_ready=rowstats_ready, dq_acc_init=dq_acc_init, T_q=sh.T_q, T_k=sh.T_k,
+                   head_dim=sh.D, H_loc=sh.H_loc,
                    head_offset=sh.head_offset, num_real_heads=sh.num_real_heads,
                    num_padded_heads=sh.num_padded_heads, gqa_group=sh.gqa_group,
                    Hkv_loc=sh.Hkv_loc, kv_head_offset=sh.kv_head_offset,
@@ -130,8 +131,10 @@ class Step:
             # zigzag ring: the rank's two chunks against the two chunks of each step
             self.descs = [lib_desc(sp, sh, zigzag_step_positions(sh, s))
                           for s in range(sh.ring_chunks)]
-            # backward: the row statistics formed by step 0's call are reused
-            self.descs_b = [lib_desc(sp, sh, zigzag_step_positions(sh, s), rowstats_ready=s > 0)
+            # backward: the row statistics formed by step 0's call are reused;
+            # step 0 starts the dQ accumulator
+            self.descs_b = [lib_desc(sp, sh, zigzag_step_positions(sh, s), rowstats_ready=s > 0,
+                                     dq_acc_init=s == 0)
                             for s in range(sh.ring_chunks)]
             self.pairs = [allowed_pairs(sh.cu_q, sh.cu_k, sh.pos_q, zigzag_step_positions(sh, s),
                                         single_sequence=True) for s in range(sh.ring_chunks)]
@@ -144,7 +147,8 @@ class Step:
                 self.v.append(to_dev(torch, v))
         elif self.ring:
             self.descs = [lib_desc(sp, sh, ring_chunk_positions(sh, c)) for c in range(sh.ring_chunks)]
-            self.descs_b = [lib_desc(sp, sh, ring_chunk_positions(sh, c), rowstats_ready=c > 0)
+            self.descs_b = [lib_desc(sp, sh, ring_chunk_positions(sh, c), rowstats_ready=c > 0,
+                                     dq_acc_init=c == 0)
                             for c in range(sh.ring_chunks)]
             self.pairs = [allowed_pairs(sh.cu_q, sh.cu_k, sh.pos_q, ring_chunk_positions(sh, c))
                           for c in range(sh.ring_chunks)]
@@ -266,14 +270,14 @@ class Step:
             t.arm(sp.SP_KERNEL_PACK, 0.0, self.bytes_pack_q)
             sp.sp_ulysses_pack(self.do_pre, sh.sp, sh.H_loc, self.qmap, dst=self.send_do)
         if self.ring:
-            self.dq_acc.zero_()
+            # the first chunk starts the fp32 dQ accumulator, the last one
+            # writes the bf16 dQ from it (no clearing, no separate cast)
             for c in range(n):
                 t.arm(sp.SP_KERNEL_ATTN_DQ, self.flops_dq[c])
                 t.arm(sp.SP_KERNEL_ATTN_DKDV, self.flops_dkdv[c])
                 sp.sp_attn_bwd(self.descs_b[c], self.q, self.k[c], self.v[c], self.o, self.lse_acc,
-                               self.do, dq_acc=self.dq_acc, dk=self.dk[c], dv=self.dv[c],
-                               workspace=self.ws_b)
-            sp.sp_f32_to_bf16(self.dq_acc, self.dq)
+                               self.do, dq=self.dq if c == n - 1 else None, dq_acc=self.dq_acc,
+                               dk=self.dk[c], dv=self.dv[c], workspace=self.ws_b)
         else:
             t.arm(sp.SP_KERNEL_ATTN_DQ, self.flops_dq[0])
             t.arm(sp.SP_KERNEL_ATTN_DKDV, self.flops_dkdv[0])

@@ -133,6 +133,14 @@ enum { SP_OP_FWD = 0, SP_OP_BWD = 1, SP_OP_RING_STEP = 2 };
  * access).
  */
 #define SP_DESC_ROWSTATS_READY 4
+/*
+ * SP_DESC_DQ_ACC_INIT (sp_attn_bwd with dq_acc only; ignored elsewhere): the
+ * call starts the dQ accumulator instead of adding to it -- dq_acc is
+ * written with this call's dQ (or, with dq too, taken as zero), so it needs
+ * no clearing before the first KV chunk of a ring backward.  Dummy slots of
+ * dq_acc stay untouched either way.
+ */
+#define SP_DESC_DQ_ACC_INIT 8
 
 typedef struct sp_attn_desc {
   int32_t T_q;              /* query tokens at this rank (rows of q, o, dq)         */
@@ -148,7 +156,7 @@ typedef struct sp_attn_desc {
   int32_t num_seqs;         /* segments (>= 0)                                       */
   int32_t causal;           /* 1 = causal by position inside a segment, 0 = full     */
   float softmax_scale;      /* multiplies q.k (callers pass 1/sqrt(D))               */
-  int32_t flags;            /* 0, SP_DESC_SINGLE_SEQUENCE | SP_DESC_ROWSTATS_READY   */
+  int32_t flags;            /* 0 or an OR of the SP_DESC_* flags above               */
   const int32_t* cu_seqlens_q;   /* HOST, num_seqs + 1                               */
   const int32_t* cu_seqlens_k;   /* HOST, num_seqs + 1                               */
   const int32_t* position_ids_q; /* HOST, T_q, or NULL                               */
@@ -273,9 +281,18 @@ sp_status sp_attn_fwd_static(const sp_attn_desc* desc, const void* q, const void
  *
  * o, lse: the forward's outputs (for ring: the FINAL merged O and LSE).
  * dout: [T_q, H_loc, D] bf16.
- * dq: bf16 [T_q, H_loc, D], written; or NULL when dq_acc is given.
+ * dq: bf16 [T_q, H_loc, D], written; or NULL.
  * dq_acc: float32 [T_q, H_loc, D], dQ is ADDED to it (ring: accumulate over
- *         KV chunks); or NULL.  Exactly one of dq / dq_acc must be non-NULL.
+ *         KV chunks, Section 2.1); or NULL.  At least one of dq / dq_acc must
+ *         be non-NULL:
+ *           dq only:         dq = bf16(dQ);
+ *           dq_acc only:     dq_acc += dQ (with SP_DESC_DQ_ACC_INIT in the
+ *                            flags: dq_acc = dQ, nothing read -- the first KV
+ *                            chunk of a ring backward);
+ *           both:            dq = bf16(dq_acc + dQ) (dq_acc = dQ's own value
+ *                            under SP_DESC_DQ_ACC_INIT), dq_acc not written --
+ *                            the last KV chunk: the accumulator's final sum goes
+ *                            straight to bf16, with no separate cast.
  * dk, dv: bf16 [T_k, Hkv_loc, D], written.
  * Dummy slots: dq = +0.0 (dq_acc untouched); KV heads read by no real query
  * head get dk = dv = +0.0.  Deterministic: no atomics.

@@ -11,6 +11,7 @@ from ._lib import (Desc, SpError, load, status_string, sp_attn_workspace_size, s
                    SP_KERNEL_TOKEN_LOGPROB, SP_KERNEL_TOKEN_LOGPROB_BWD,
                    SP_OK, SP_ERR_INVALID_ARG, SP_ERR_UNSUPPORTED, SP_ERR_WORKSPACE, SP_ERR_HIP,
                    SP_OP_FWD, SP_OP_BWD, SP_OP_RING_STEP, SP_DESC_SINGLE_SEQUENCE, SP_DESC_ROWSTATS_READY,
+                   SP_DESC_DQ_ACC_INIT,
                    EXPORTED,
                    LIB_PATH, SP_KERNEL_ATTN_FWD, SP_KERNEL_ATTN_DQ, SP_KERNEL_ATTN_DKDV,
                    SP_KERNEL_PACK, SP_KERNEL_UNPACK, SP_KERNEL_LSE_MERGE, SP_KERNEL_UNPACK_ADD)
@@ -24,7 +25,7 @@ __all__ = [
     "SP_KERNEL_TOKEN_LOGPROB", "SP_KERNEL_TOKEN_LOGPROB_BWD",
     "SP_OK", "SP_ERR_INVALID_ARG", "SP_ERR_UNSUPPORTED", "SP_ERR_WORKSPACE", "SP_ERR_HIP",
     "SP_OP_FWD", "SP_OP_BWD", "SP_OP_RING_STEP", "SP_DESC_SINGLE_SEQUENCE",
-    "SP_DESC_ROWSTATS_READY", "EXPORTED",
+    "SP_DESC_ROWSTATS_READY", "SP_DESC_DQ_ACC_INIT", "EXPORTED",
     "LIB_PATH", "SP_KERNEL_ATTN_FWD", "SP_KERNEL_ATTN_DQ", "SP_KERNEL_ATTN_DKDV", "SP_KERNEL_PACK",
     "SP_KERNEL_UNPACK", "SP_KERNEL_LSE_MERGE", "SP_KERNEL_UNPACK_ADD",
 ]

@@ -21,6 +21,7 @@ SP_OK, SP_ERR_INVALID_ARG, SP_ERR_UNSUPPORTED, SP_ERR_WORKSPACE, SP_ERR_HIP = ra
 SP_OP_FWD, SP_OP_BWD, SP_OP_RING_STEP = 0, 1, 2
 SP_DESC_SINGLE_SEQUENCE = 1
 SP_DESC_ROWSTATS_READY = 4
+SP_DESC_DQ_ACC_INIT = 8
 SCHED_ITEM_INTS = 8
 
 _i32p = ctypes.POINTER(ctypes.c_int32)
@@ -114,7 +115,8 @@ class Desc:
     def __init__(self, *, T_q, T_k, head_dim, H_loc, head_offset, num_real_heads,
                  num_padded_heads, gqa_group, Hkv_loc, kv_head_offset, cu_seqlens_q,
                  cu_seqlens_k, position_ids_q=None, position_ids_k=None, causal=True,
-                 softmax_scale=None, single_sequence=False, rowstats_ready=False):
+                 softmax_scale=None, single_sequence=False, rowstats_ready=False,
+                 dq_acc_init=False):
         self._keep = []
 
         def arr(x):
@@ -139,7 +141,8 @@ class Desc:
             num_seqs=max(0, len(cq) - 1), causal=1 if causal else 0,
             softmax_scale=(1.0 / math.sqrt(head_dim)) if softmax_scale is None else softmax_scale,
             flags=((SP_DESC_SINGLE_SEQUENCE if single_sequence else 0)
-                   | (SP_DESC_ROWSTATS_READY if rowstats_ready else 0)),
+                   | (SP_DESC_ROWSTATS_READY if rowstats_ready else 0)
+                   | (SP_DESC_DQ_ACC_INIT if dq_acc_init else 0)),
             cu_seqlens_q=arr(cu_seqlens_q), cu_seqlens_k=arr(cu_seqlens_k),
             position_ids_q=arr(position_ids_q), position_ids_k=arr(position_ids_k))
 

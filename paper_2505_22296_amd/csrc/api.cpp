@@ -116,7 +116,8 @@ bool ramp_checks() {
 
 sp_status validate(const sp_attn_desc* d, Problem& p) {
   if (!d) return SP_ERR_INVALID_ARG;
-  if (d->flags & ~(SP_DESC_SINGLE_SEQUENCE | SP_DESC_ROWSTATS_READY)) return SP_ERR_INVALID_ARG;
+  if (d->flags & ~(SP_DESC_SINGLE_SEQUENCE | SP_DESC_ROWSTATS_READY | SP_DESC_DQ_ACC_INIT))
+    return SP_ERR_INVALID_ARG;
   const bool single = (d->flags & SP_DESC_SINGLE_SEQUENCE) != 0;
   if (d->T_q < 0 || d->T_k < 0 || d->T_q >= kMaxTokens || d->T_k >= kMaxTokens)
     return SP_ERR_INVALID_ARG;
@@ -731,10 +732,8 @@ sp_status sp_attn_bwd(const sp_attn_desc* d, const void* q, const void* k, const
   sp_status s = validate(d, p);
   if (s != SP_OK) return s;
   // pointers are required for tensors that have elements
-  if (d->T_q > 0 && (!q || !o || !lse || !dout || (dq == nullptr) == (dq_acc == nullptr)))
-    return SP_ERR_INVALID_ARG;
+  if (d->T_q > 0 && (!q || !o || !lse || !dout || (!dq && !dq_acc))) return SP_ERR_INVALID_ARG;
   if (d->T_k > 0 && (!k || !v || !dk || !dv)) return SP_ERR_INVALID_ARG;
-  if (dq && dq_acc) return SP_ERR_INVALID_ARG;
   for (const void* ptr : {q, k, v, o, dout, (const void*)dk, (const void*)dv})
     if (!aligned16(ptr)) return SP_ERR_INVALID_ARG;
   if ((dq && !aligned16(dq)) || (dq_acc && !aligned16(dq_acc))) return SP_ERR_INVALID_ARG;
@@ -775,6 +774,7 @@ sp_status sp_attn_bwd(const sp_attn_desc* d, const void* q, const void* k, const
     a.q = (const uint16_t*)q; a.k = (const uint16_t*)k; a.v = (const uint16_t*)v;
     a.dout = (const uint16_t*)dout;
     a.lse = lse; a.neg_d = neg_d; a.dq = (uint16_t*)dq; a.dq_acc = dq_acc;
+    a.dq_init = dq_acc && (d->flags & SP_DESC_DQ_ACC_INIT) ? 1 : 0;
     a.items = (const int32_t*)at(ws, L.items_dq);
     a.T_q = d->T_q; a.T_k = d->T_k; a.H = d->H_loc; a.Hkv = d->Hkv_loc;
     a.scale_log2 = sl2; a.scale = d->softmax_scale; a.causal = d->causal;

@@ -230,10 +230,17 @@ __global__ __launch_bounds__(NTQ, 1) void attn_dq_kernel(DqArgs a) {
     for (int j = 0; j < 4; ++j) {
       float x0 = acc[d][j * 4] * sc, x1 = acc[d][j * 4 + 1] * sc;
       float x2 = acc[d][j * 4 + 2] * sc, x3 = acc[d][j * 4 + 3] * sc;
-      if (a.dq_acc) {
+      if (a.dq_acc) {  // ring: accumulate; the last chunk emits bf16 instead
         float4* p = (float4*)(a.dq_acc + base + d * 32 + j * 8);
-        float4 o = *p;
-        *p = make_float4(o.x + x0, o.y + x1, o.z + x2, o.w + x3);
+        float4 t = make_float4(x0, x1, x2, x3);
+        if (!a.dq_init) {
+          const float4 o = *p;
+          t = make_float4(o.x + x0, o.y + x1, o.z + x2, o.w + x3);
+        }
+        if (a.dq)
+          *(u32x2*)(a.dq + base + d * 32 + j * 8) = pack_bf16x4(t.x, t.y, t.z, t.w);
+        else
+          *p = t;
       } else {
         *(u32x2*)(a.dq + base + d * 32 + j * 8) = pack_bf16x4(x0, x1, x2, x3);
       }

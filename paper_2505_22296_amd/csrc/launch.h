@@ -108,7 +108,9 @@ struct DqArgs {
   const float* lse;      // [H, T_q]
   const float* neg_d;    // -D = -(dO . O) per row: [n_real, T_q]
   uint16_t* dq;          // bf16 [T_q, H, D] or null
-  float* dq_acc;         // float32 [T_q, H, D] (+=) or null
+  float* dq_acc;         // float32 [T_q, H, D] or null: with dq, read only
+                         // (dq = bf16(dq_acc + dQ)); without, dq_acc += dQ
+  int dq_init;           // dq_acc taken as zero (not read)
   const int32_t* items;
   int T_q, T_k, H, Hkv;
   float scale_log2, scale;

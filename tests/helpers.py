@@ -39,7 +39,8 @@ def oracle_kw(sh: Shard, pos_q=None, pos_k=None, causal=None):
                 causal=sh.causal if causal is None else causal)
 
 
-def lib_desc(sh: Shard, pos_q=None, pos_k=None, causal=None, T_k=None, rowstats_ready=False):
+def lib_desc(sh: Shard, pos_q=None, pos_k=None, causal=None, T_k=None, rowstats_ready=False,
+             dq_acc_init=False):
     from paper_2505_22296_amd import Desc
     return Desc(T_q=sh.T_q, T_k=sh.T_k if T_k is None else T_k, head_dim=sh.D, H_loc=sh.H_loc,
                 head_offset=sh.head_offset, num_real_heads=sh.num_real_heads,
@@ -48,7 +49,8 @@ def lib_desc(sh: Shard, pos_q=None, pos_k=None, causal=None, T_k=None, rowstats_
                 cu_seqlens_k=sh.cu_k, position_ids_q=sh.pos_q if pos_q is None else pos_q,
                 position_ids_k=sh.pos_k if pos_k is None else pos_k,
                 causal=sh.causal if causal is None else causal, softmax_scale=sh.scale,
-                single_sequence=sh.single_sequence, rowstats_ready=rowstats_ready)
+                single_sequence=sh.single_sequence, rowstats_ready=rowstats_ready,
+                dq_acc_init=dq_acc_init)
 
 
 def to_dev(bits: np.ndarray):

@@ -163,16 +163,19 @@ def test_fullsize_ring_rank(sp):
     for c in range(n):
         sp.sp_ring_step(descs[c], Q, Ks[c], Vs[c], o_acc, lse, init=(c == 0),
                         o_out=o if c == n - 1 else None)
-    dq_acc = torch.zeros((C, H, D), dtype=torch.float32, device="cuda")
+    # the benchmark's flow: one workspace (the row statistics formed by chunk
+    # 0's call are reused), the dQ accumulator started by chunk 0 (its NaN
+    # start never read) and turned into bf16 dQ by the last chunk
+    dq_acc = torch.full((C, H, D), float("nan"), dtype=torch.float32, device="cuda")
+    dq = torch.empty((C, H, D), dtype=torch.bfloat16, device="cuda")
     dks, dvs = [], []
-    # one workspace: the row statistics formed by chunk 0's call are reused
-    descs_b = [lib_desc(sh, pos_k=ring_chunk_positions(sh, c), rowstats_ready=c > 0)
-               for c in range(n)]
+    descs_b = [lib_desc(sh, pos_k=ring_chunk_positions(sh, c), rowstats_ready=c > 0,
+                        dq_acc_init=c == 0) for c in range(n)]
     ws = torch.empty(max(sp.sp_attn_workspace_size(d, sp.SP_OP_BWD) for d in descs_b),
                      dtype=torch.uint8, device="cuda")
     for c in range(n):
-        _, gk, gv = sp.sp_attn_bwd(descs_b[c], Q, Ks[c], Vs[c], o, lse, dO, dq_acc=dq_acc,
-                                   workspace=ws)
+        _, gk, gv = sp.sp_attn_bwd(descs_b[c], Q, Ks[c], Vs[c], o, lse, dO,
+                                   dq=dq if c == n - 1 else None, dq_acc=dq_acc, workspace=ws)
         dks.append(gk)
         dvs.append(gv)
     torch.cuda.synchronize()
@@ -190,8 +193,7 @@ def test_fullsize_ring_rank(sp):
     assert_close(o_acc[ridx].cpu().numpy().astype(np.float64), RO, "ring O acc rows")
     assert np.abs(lse[:, ridx].cpu().numpy() - RL).max() <= LSE_MAX_ABS
     RdQ, _, _ = oracle.attn_dq_rows(qf, kcat, vcat, dof, rows[::2], **kw)
-    assert_close(dq_acc[torch.from_numpy(rows[::2]).cuda()].cpu().numpy().astype(np.float64), RdQ,
-                 "ring dQ rows")
+    assert_close(from_dev(dq[torch.from_numpy(rows[::2]).cuda()]), RdQ, "ring dQ rows")
     # keys near the end of the diagonal chunk: few rows see them
     keys = np.array([n * C - 1, n * C - 5, n * C - 70])
     RdK, RdV = oracle.attn_dkdv_keys(qf, kcat, vcat, dof, keys, **kw)
@@ -248,14 +250,16 @@ def test_fullsize_zigzag_rank(sp, name):
     for s in range(n):
         sp.sp_ring_step(descs[s], Q, Ks[s], Vs[s], o_acc, lse, init=(s == 0),
                         o_out=o if s == n - 1 else None)
-    dq_acc = torch.zeros((T, H, D), dtype=torch.float32, device="cuda")
+    dq_acc = torch.full((T, H, D), float("nan"), dtype=torch.float32, device="cuda")
+    dq = torch.empty((T, H, D), dtype=torch.bfloat16, device="cuda")
     dks, dvs = [], []
-    descs_b = [lib_desc(sh, pos_k=pks[s], rowstats_ready=s > 0) for s in range(n)]
+    descs_b = [lib_desc(sh, pos_k=pks[s], rowstats_ready=s > 0, dq_acc_init=s == 0)
+               for s in range(n)]
     ws = torch.empty(max(sp.sp_attn_workspace_size(d, sp.SP_OP_BWD) for d in descs_b),
                      dtype=torch.uint8, device="cuda")
     for s in range(n):
-        _, gk, gv = sp.sp_attn_bwd(descs_b[s], Q, Ks[s], Vs[s], o, lse, dO, dq_acc=dq_acc,
-                                   workspace=ws)
+        _, gk, gv = sp.sp_attn_bwd(descs_b[s], Q, Ks[s], Vs[s], o, lse, dO,
+                                   dq=dq if s == n - 1 else None, dq_acc=dq_acc, workspace=ws)
         dks.append(gk)
         dvs.append(gv)
     torch.cuda.synchronize()
@@ -275,8 +279,7 @@ def test_fullsize_zigzag_rank(sp, name):
     assert_close(from_dev(o[ridx]), RO, "zigzag O rows")
     assert np.abs(lse[:, ridx].cpu().numpy() - RL).max() <= LSE_MAX_ABS
     RdQ, _, _ = oracle.attn_dq_rows(qf, kcat, vcat, dof, rows[::2], **kw)
-    assert_close(dq_acc[torch.from_numpy(rows[::2]).cuda()].cpu().numpy().astype(np.float64), RdQ,
-                 "zigzag dQ rows")
+    assert_close(from_dev(dq[torch.from_numpy(rows[::2]).cuda()]), RdQ, "zigzag dQ rows")
     # keys at the end of the rank's own second chunk (step 0): only the last
     # rows see them, so the oracle evaluates few rows
     loc = np.array([2 * C - 1, 2 * C - 3, 2 * C - 40])

@@ -323,6 +323,23 @@ def test_ring_rank_fwd_bwd(sp):
                                    dq_acc=dq_acc2, workspace=ws)
         assert np.array_equal(from_dev(gk), dks[c]) and np.array_equal(from_dev(gv), dvs[c])
     assert np.array_equal(dq_acc2.cpu().numpy(), dq_acc.cpu().numpy())
+    # the accumulator started by the first chunk (SP_DESC_DQ_ACC_INIT: its
+    # NaN start is never read) and finished by the last, which writes bf16
+    # dQ directly and leaves the accumulator at the other chunks' sum: the
+    # same values as the cleared accumulator and the separate cast
+    dq_acc3 = torch.full((C, H, D), float("nan"), dtype=torch.float32, device="cuda")
+    dq_bf3 = torch.empty((C, H, D), dtype=torch.bfloat16, device="cuda")
+    for c in range(r + 1):
+        d = lib_desc(base, pos_q=pos_q, pos_k=c * C + np.arange(C), rowstats_ready=c > 0,
+                     dq_acc_init=c == 0)
+        sp.sp_attn_bwd(d, dq, to_dev(ks[c]), to_dev(vs[c]), o_bf, lse_acc, to_dev(do),
+                       dq=dq_bf3 if c == r else None, dq_acc=dq_acc3, workspace=ws)
+    assert np.array_equal(from_dev(dq_bf3), from_dev(gq_bf))
+    partial = torch.zeros((C, H, D), dtype=torch.float32, device="cuda")
+    for c in range(r):
+        sp.sp_attn_bwd(lib_desc(base, pos_q=pos_q, pos_k=c * C + np.arange(C)), dq,
+                       to_dev(ks[c]), to_dev(vs[c]), o_bf, lse_acc, to_dev(do), dq_acc=partial)
+    assert np.array_equal(dq_acc3.cpu().numpy(), partial.cpu().numpy())
 
 
 def test_ring_steps_with_dummy_slots(sp):
