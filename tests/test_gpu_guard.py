@@ -62,7 +62,15 @@ def _attn_guarded(sp, sh, dq_acc_mode=False):
     dk = Guarded((sh.T_k, sh.Hkv_loc, D), bf)
     dv = Guarded((sh.T_k, sh.Hkv_loc, D), bf)
     wsb = Guarded((sp.sp_attn_workspace_size(d, sp.SP_OP_BWD),), torch.uint8)
-    if dq_acc_mode:
+    if dq_acc_mode == "both":  # the last ring chunk's mode: bf16 dQ from the accumulator
+        dq = Guarded((sh.T_q, sh.H_loc, D), bf)
+        acc = Guarded((sh.T_q, sh.H_loc, D), f32)
+        acc.t.zero_()
+        sp.sp_attn_bwd(d, Q, K, V, o.t, lse.t, dO, dq=dq.t, dq_acc=acc.t, dk=dk.t, dv=dv.t,
+                       workspace=wsb.t)
+        assert bool((acc.t == 0).all()), "the accumulator is read, not written, with dq given"
+        assert acc.intact()
+    elif dq_acc_mode:
         dq = Guarded((sh.T_q, sh.H_loc, D), f32)
         dq.t.zero_()
         sp.sp_attn_bwd(d, Q, K, V, o.t, lse.t, dO, dq_acc=dq.t, dk=dk.t, dv=dv.t, workspace=wsb.t)
@@ -79,7 +87,7 @@ def _attn_guarded(sp, sh, dq_acc_mode=False):
 def test_attention_guard_bands(sp, seed):
     sh = random_shard(seed)
     print(f"guard {sh.name}", flush=True)
-    _attn_guarded(sp, sh, dq_acc_mode=(seed % 2 == 1))
+    _attn_guarded(sp, sh, dq_acc_mode=("both" if seed % 4 == 0 else seed % 2 == 1))
 
 
 def test_attention_guard_gqa_partials(sp):
