@@ -798,8 +798,7 @@ sp_status sp_attn_bwd(const sp_attn_desc* d, const void* q, const void* k, const
         r.head_lo[kv] = p.kv_lo[kv];
         r.head_hi[kv] = p.kv_hi[kv];
       }
-      SP_HIP(spk::launch_reduce_kv(b.part_k, dk, r, st));
-      SP_HIP(spk::launch_reduce_kv(b.part_v, dv, r, st));
+      SP_HIP(spk::launch_reduce_kv(b.part_k, b.part_v, dk, dv, r, st));
     }
   }
   return SP_OK;

@@ -429,10 +429,15 @@ hipError_t launch_rowdot(const void* o, const void* dout, const float* lse, floa
 }
 
 // ------------------------------------------------------- GQA dK/dV reduce
-// out[t][kv][d] = bf16( sum_{y in heads of kv} part[y][t][d] ), ascending y.
-__global__ __launch_bounds__(kBlock) void reduce_kv_kernel(const float* __restrict__ part,
-                                                           uint16_t* __restrict__ out,
+// out[t][kv][d] = bf16( sum_{y in heads of kv} part[y][t][d] ), ascending y;
+// dK (blockIdx.y = 0) and dV (blockIdx.y = 1) in one launch.
+__global__ __launch_bounds__(kBlock) void reduce_kv_kernel(const float* __restrict__ part_k,
+                                                           const float* __restrict__ part_v,
+                                                           uint16_t* __restrict__ dk,
+                                                           uint16_t* __restrict__ dv,
                                                            ReduceArgs a) {
+  const float* part = blockIdx.y ? part_v : part_k;
+  uint16_t* out = blockIdx.y ? dv : dk;
   const int n8 = a.D >> 3;
   const int64_t n = (int64_t)a.T * a.Hkv * n8;
   for (int64_t e = (int64_t)blockIdx.x * kBlock + threadIdx.x; e < n;
@@ -453,11 +458,12 @@ __global__ __launch_bounds__(kBlock) void reduce_kv_kernel(const float* __restri
   }
 }
 
-hipError_t launch_reduce_kv(const float* part, void* out, const ReduceArgs& a, hipStream_t st) {
+hipError_t launch_reduce_kv(const float* part_k, const float* part_v, void* dk, void* dv,
+                            const ReduceArgs& a, hipStream_t st) {
   int64_t n = (int64_t)a.T * a.Hkv * (a.D / 8);
   if (n == 0) return hipSuccess;
-  hipLaunchKernelGGL(reduce_kv_kernel, dim3(grid_for(n)), dim3(kBlock), 0, st, part,
-                     (uint16_t*)out, a);
+  hipLaunchKernelGGL(reduce_kv_kernel, dim3(grid_for(n), 2), dim3(kBlock), 0, st, part_k, part_v,
+                     (uint16_t*)dk, (uint16_t*)dv, a);
   return hipGetLastError();
 }
 

@@ -152,7 +152,8 @@ hipError_t launch_fill_f32(float* x, int64_t n, float v, hipStream_t st);
 hipError_t launch_f32_to_bf16(const float* s, void* d, int64_t n, hipStream_t st);
 hipError_t launch_rowdot(const void* o, const void* dout, const float* lse, float* neg_d,
                          float* lse2, int T, int H, int nh, int D, hipStream_t st);
-hipError_t launch_reduce_kv(const float* part, void* out, const ReduceArgs& a, hipStream_t st);
+hipError_t launch_reduce_kv(const float* part_k, const float* part_v, void* dk, void* dv,
+                            const ReduceArgs& a, hipStream_t st);
 
 hipError_t launch_attn_fwd(const FwdArgs& a, int n_items, int D, bool merge, hipStream_t st);
 hipError_t launch_attn_dq(const DqArgs& a, int n_items, int D, hipStream_t st);
