@@ -132,3 +132,72 @@ def test_random_shard_parity(sp, seed):
     if nr < sh.H_loc:
         assert np.all(bits_from_dev(o)[:, nr:] == 0) and np.all(bits_from_dev(gq)[:, nr:] == 0)
         assert np.all(np.isneginf(GL[nr:]))
+
+
+@pytest.mark.parametrize("seed", [s for s in SEEDS if s % 3 == 2])
+def test_random_ring_split(sp, seed):
+    """The same random shards (pieces of one sequence) with their keys cut
+    into 2-3 contiguous chunks and run as ring steps: the forward merged by
+    log-sum-exp (first chunk initialises, last writes bf16 O), the backward
+    with the row statistics formed once, the dQ accumulator started by the
+    first chunk (from NaN, never read) and turned into bf16 dQ by the last.
+    Everything must match the monolithic oracle at the parity bars."""
+    import torch
+    sh = random_shard(seed)
+    rng = np.random.default_rng(4100 + seed)
+    n_ch = int(rng.integers(2, 4))
+    cuts = np.sort(rng.choice(np.arange(1, sh.T_k), size=min(n_ch - 1, sh.T_k - 1), replace=False))
+    bounds = [0, *[int(c) for c in cuts], sh.T_k]
+    print(f"{sh.name}: T_q={sh.T_q} T_k={sh.T_k} chunks={bounds} D={sh.D} H_loc={sh.H_loc} "
+          f"real={sh.n_real_loc} g={sh.gqa_group} causal={sh.causal}", flush=True)
+    q, k, v, do = shard_inputs(sh)
+    Q, K, V, dO = (to_dev(x) for x in (q, k, v, do))
+
+    # a chunk's keys are the pieces it cuts from the sequence's key pieces
+    def desc(a, b, **flags):
+        L = b - a
+        return sp.Desc(T_q=sh.T_q, T_k=L, head_dim=sh.D, H_loc=sh.H_loc, head_offset=sh.head_offset,
+                       num_real_heads=sh.num_real_heads, num_padded_heads=sh.num_padded_heads,
+                       gqa_group=sh.gqa_group, Hkv_loc=sh.Hkv_loc,
+                       kv_head_offset=sh.kv_head_offset, cu_seqlens_q=sh.cu_q,
+                       cu_seqlens_k=np.clip(sh.cu_k, a, b) - a, position_ids_q=sh.pos_q,
+                       position_ids_k=sh.pos_k[a:b], causal=sh.causal, softmax_scale=sh.scale,
+                       single_sequence=True, **flags)
+
+    H, D = sh.H_loc, sh.D
+    o_acc = torch.full((sh.T_q, H, D), float("nan"), dtype=torch.float32, device="cuda")
+    lse = torch.full((H, sh.T_q), float("nan"), dtype=torch.float32, device="cuda")
+    o = torch.empty((sh.T_q, H, D), dtype=torch.bfloat16, device="cuda")
+    n = len(bounds) - 1
+    for c in range(n):
+        a, b = bounds[c], bounds[c + 1]
+        sp.sp_ring_step(desc(a, b), Q, K[a:b], V[a:b], o_acc, lse, init=(c == 0),
+                        o_out=o if c == n - 1 else None)
+    dq_acc = torch.full((sh.T_q, H, D), float("nan"), dtype=torch.float32, device="cuda")
+    dq = torch.empty((sh.T_q, H, D), dtype=torch.bfloat16, device="cuda")
+    dk, dv = torch.empty_like(K), torch.empty_like(V)
+    ws = torch.empty(max(sp.sp_attn_workspace_size(desc(bounds[c], bounds[c + 1]), sp.SP_OP_BWD)
+                         for c in range(n)), dtype=torch.uint8, device="cuda")
+    for c in range(n):
+        a, b = bounds[c], bounds[c + 1]
+        sp.sp_attn_bwd(desc(a, b, rowstats_ready=c > 0, dq_acc_init=c == 0), Q, K[a:b], V[a:b], o,
+                       lse, dO, dq=dq if c == n - 1 else None, dq_acc=dq_acc, dk=dk[a:b],
+                       dv=dv[a:b], workspace=ws)
+    torch.cuda.synchronize()
+    qf, kf, vf, dof = (oracle.bf16_bits_to_f64(x) for x in (q, k, v, do))
+    kw = oracle_kw(sh)
+    RO, RL = oracle.attn_forward(qf, kf, vf, **kw)
+    RdQ, RdK, RdV = oracle.attn_backward(qf, kf, vf, dof, **kw)
+    nr = sh.n_real_loc
+    GL = lse.cpu().numpy().astype(np.float64)
+    if nr:
+        assert_close(from_dev(o)[:, :nr], RO[:, :nr], "O", max_abs=scaled_max_abs(RO[:, :nr]))
+        fin = np.isfinite(RL[:nr])
+        assert np.array_equal(np.isfinite(GL[:nr]), fin)
+        if fin.any():
+            assert np.abs(GL[:nr][fin] - RL[:nr][fin]).max() <= LSE_MAX_ABS
+        assert_close(from_dev(dq)[:, :nr], RdQ[:, :nr], "dQ", max_abs=scaled_max_abs(RdQ[:, :nr]))
+    assert_close(from_dev(dk), RdK, "dK", max_abs=scaled_max_abs(RdK))
+    assert_close(from_dev(dv), RdV, "dV", max_abs=scaled_max_abs(RdV))
+    if nr < sh.H_loc:
+        assert np.all(bits_from_dev(o)[:, nr:] == 0) and np.all(bits_from_dev(dq)[:, nr:] == 0)
