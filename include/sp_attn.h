@@ -134,11 +134,12 @@ enum { SP_OP_FWD = 0, SP_OP_BWD = 1, SP_OP_RING_STEP = 2 };
  */
 #define SP_DESC_ROWSTATS_READY 4
 /*
- * SP_DESC_DQ_ACC_INIT (sp_attn_bwd with dq_acc only; ignored elsewhere): the
- * call starts the dQ accumulator instead of adding to it -- dq_acc is
- * written with this call's dQ (or, with dq too, taken as zero), so it needs
- * no clearing before the first KV chunk of a ring backward.  Dummy slots of
- * dq_acc stay untouched either way.
+ * SP_DESC_DQ_ACC_INIT (sp_attn_bwd when dq_acc is given; ignored otherwise):
+ * the call starts the dQ accumulator instead of adding to it -- dq_acc is not
+ * read, and is written with this call's dQ (with dq given too, dq = bf16(dQ)
+ * and dq_acc is not touched at all), so it needs no clearing before the
+ * first KV chunk of a ring backward.  Dummy slots of dq_acc stay untouched
+ * either way.
  */
 #define SP_DESC_DQ_ACC_INIT 8
 
@@ -289,9 +290,9 @@ sp_status sp_attn_fwd_static(const sp_attn_desc* desc, const void* q, const void
  *           dq_acc only:     dq_acc += dQ (with SP_DESC_DQ_ACC_INIT in the
  *                            flags: dq_acc = dQ, nothing read -- the first KV
  *                            chunk of a ring backward);
- *           both:            dq = bf16(dq_acc + dQ) (dq_acc = dQ's own value
- *                            under SP_DESC_DQ_ACC_INIT), dq_acc not written --
- *                            the last KV chunk: the accumulator's final sum goes
+ *           both:            dq = bf16(dq_acc + dQ) (bf16(dQ) under
+ *                            SP_DESC_DQ_ACC_INIT), dq_acc not written -- the
+ *                            last KV chunk: the accumulator's final sum goes
  *                            straight to bf16, with no separate cast.
  * dk, dv: bf16 [T_k, Hkv_loc, D], written.
  * Dummy slots: dq = +0.0 (dq_acc untouched); KV heads read by no real query
