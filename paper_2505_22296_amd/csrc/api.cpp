@@ -205,17 +205,41 @@ struct Item {
   int64_t cost;
 };
 
-void sort_items(std::vector<Item>& items, std::vector<int32_t>& out) {
+// Launch order: longest first (items are enumerated head by head, and the
+// sort keeps that order among equal costs).  Within a run of equal costs --
+// where the order does not change how the work divides over the CUs -- the
+// items are arranged for the XCDs: MI355X hands workgroup i of a launch to
+// XCD i % 8, each with its own L2, so the run's positions that fall on one
+// XCD take one contiguous share of the run, i.e. a few neighbouring heads,
+// whose tiles that XCD's L2 then serves to all its workgroups.  `n_front`
+// items (zero fills) precede these in the launch and shift the map.
+constexpr int kXcds = 8;
+
+void sort_items(std::vector<Item>& items, std::vector<int32_t>& out, size_t n_front) {
   std::stable_sort(items.begin(), items.end(),
                    [](const Item& a, const Item& b) { return a.cost > b.cost; });
-  out.resize(items.size() * kItemInts);
-  for (size_t i = 0; i < items.size(); ++i)
-    std::memcpy(&out[i * kItemInts], items[i].v, sizeof(int) * kItemInts);
+  const size_t N = items.size();
+  std::vector<const Item*> order(N);
+  for (size_t s = 0; s < N;) {
+    size_t e = s + 1;
+    while (e < N && items[e].cost == items[s].cost) ++e;
+    size_t next[kXcds] = {};
+    for (size_t p = s; p < e; ++p) ++next[(n_front + p) % kXcds];  // positions per XCD
+    for (size_t x = 0, at = s; x < kXcds; ++x) {                   // -> first item of its share
+      const size_t n = next[x];
+      next[x] = at;
+      at += n;
+    }
+    for (size_t p = s; p < e; ++p) order[p] = &items[next[(n_front + p) % kXcds]++];
+    s = e;
+  }
+  out.resize(N * kItemInts);
+  for (size_t i = 0; i < N; ++i) std::memcpy(&out[i * kItemInts], order[i]->v, sizeof(int) * kItemInts);
 }
 
 // Row-tile items (forward, ring step, dQ).
 void schedule_rows(const sp_attn_desc* d, const Problem& p, int BM, int BN, bool include_empty,
-                   std::vector<int32_t>& out) {
+                   std::vector<int32_t>& out, size_t n_front) {
   std::vector<Item> items;
   for (int y = 0; y < p.n_real; ++y) {
     for (const Seg& g : p.segs) {
@@ -235,12 +259,12 @@ void schedule_rows(const sp_attn_desc* d, const Problem& p, int BM, int BN, bool
       for (int a = p.q_pad; a < d->T_q; a += BM)
         items.push_back(Item{{a, std::min(a + BM, d->T_q), 0, 0, 0, y, p.kv_of[y], 0}, 0});
   }
-  sort_items(items, out);
+  sort_items(items, out, n_front);
 }
 
 // Key-tile items (dK / dV).  Every key of every real head gets exactly one item.
 void schedule_keys(const sp_attn_desc* d, const Problem& p, int BNK, int BQ,
-                   std::vector<int32_t>& out) {
+                   std::vector<int32_t>& out, size_t n_front) {
   std::vector<Item> items;
   for (int y = 0; y < p.n_real; ++y) {
     for (const Seg& g : p.segs_k) {
@@ -257,7 +281,7 @@ void schedule_keys(const sp_attn_desc* d, const Problem& p, int BNK, int BQ,
     for (int a = p.k_pad; a < d->T_k; a += BNK)
       items.push_back(Item{{a, std::min(a + BNK, d->T_k), 0, 0, 0, y, p.kv_of[y], 1}, 0});
   }
-  sort_items(items, out);
+  sort_items(items, out, n_front);
 }
 
 // Zero fills as work items of the same launch (no extra kernels): dummy
@@ -585,10 +609,13 @@ sp_status sp_attn_schedule(const sp_attn_desc* desc, int32_t op, int32_t* items,
   sp_status s = validate(desc, p);
   if (s != SP_OK) return s;
   std::vector<int32_t> v;
+  // in launch order: the fill items that precede the listed ones there
+  // shift the workgroup -> XCD map
   if (op == SP_OP_FWD || op == SP_OP_RING_STEP)
-    schedule_rows(desc, p, spk::kFwdBM, spk::kFwdBN, true, v);
+    schedule_rows(desc, p, spk::kFwdBM, spk::kFwdBN, true, v,
+                  row_fills(desc, p).size() / kItemInts);
   else if (op == SP_OP_BWD)
-    schedule_keys(desc, p, spk::kDkdvBN, spk::kDkdvBQ, v);
+    schedule_keys(desc, p, spk::kDkdvBN, spk::kDkdvBQ, v, key_fills(desc, p).size() / kItemInts);
   else
     return SP_ERR_INVALID_ARG;
   const int32_t n = (int32_t)(v.size() / kItemInts);
@@ -666,8 +693,9 @@ static sp_status fwd_common(const sp_attn_desc* d, const void* q, const void* k,
   if (d->T_q == 0) return SP_OK;
   const bool include_empty = !ring || init || o_out;
   std::vector<int32_t> items;
-  schedule_rows(d, p, spk::kFwdBM, spk::kFwdBN, include_empty, items);
-  if (include_empty) prepend(row_fills(d, p), items);
+  const std::vector<int32_t> fills = include_empty ? row_fills(d, p) : std::vector<int32_t>();
+  schedule_rows(d, p, spk::kFwdBM, spk::kFwdBN, include_empty, items, fills.size() / kItemInts);
+  prepend(fills, items);
   const int n_items = (int)(items.size() / kItemInts);
   hipStream_t st = (hipStream_t)stream;
   void* items_dev = nullptr;
@@ -745,10 +773,13 @@ sp_status sp_attn_bwd(const sp_attn_desc* d, const void* q, const void* k, const
     return SP_OK;
   }
   std::vector<int32_t> it_dq, it_kv;
-  schedule_rows(d, p, spk::kDqBM, spk::kDqBN, true, it_dq);
-  if (dq) prepend(row_fills(d, p), it_dq);  // a dq_acc's dummy slots stay untouched
-  schedule_keys(d, p, spk::kDkdvBN, spk::kDkdvBQ, it_kv);
-  prepend(key_fills(d, p), it_kv);
+  // a dq_acc's dummy slots stay untouched
+  const std::vector<int32_t> fq = dq ? row_fills(d, p) : std::vector<int32_t>();
+  const std::vector<int32_t> fkv = key_fills(d, p);
+  schedule_rows(d, p, spk::kDqBM, spk::kDqBN, true, it_dq, fq.size() / kItemInts);
+  prepend(fq, it_dq);
+  schedule_keys(d, p, spk::kDkdvBN, spk::kDkdvBQ, it_kv, fkv.size() / kItemInts);
+  prepend(fkv, it_kv);
   const size_t na = it_dq.size() / kItemInts, nb = it_kv.size() / kItemInts;
   Layout L = layout_for(d, p, SP_OP_BWD, na, nb);
   if ((s = check_ws(L, ws, ws_bytes)) != SP_OK) return s;

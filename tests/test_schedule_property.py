@@ -97,3 +97,71 @@ def test_schedule_matches_the_mask(sh):
         cost = np.array([-(-(int(it[b]) - (int(it[a]) & ~7)) // step) if it[b] > it[a] else 0
                          for it in items])
         assert np.all(np.diff(cost) <= 0), (op, cost[:20])
+
+
+def _runs(cost):
+    s = 0
+    for e in range(1, len(cost) + 1):
+        if e == len(cost) or cost[e] != cost[s]:
+            yield s, e
+            s = e
+
+
+@settings(max_examples=200, deadline=None, derandomize=True,
+          suppress_health_check=[HealthCheck.too_slow, HealthCheck.data_too_large])
+@given(shards())
+def test_equal_cost_runs_are_cut_per_xcd(sh):
+    """Within a run of equal cost the launch positions of one XCD (position
+    mod 8, whatever the number of fill items in front) hold one contiguous
+    share of the run taken head by head, rows (keys) ascending; the shares
+    follow each other in XCD order."""
+    d = lib_desc(sh)
+    for op, (a, b, step) in ((sp.SP_OP_FWD, (2, 3, 64)), (sp.SP_OP_BWD, (2, 3, 32))):
+        items = sp.sp_attn_schedule(d, op)
+        cost = [-(-(int(it[b]) - (int(it[a]) & ~7)) // step) if it[b] > it[a] else 0
+                for it in items]
+        for s, e in _runs(cost):
+            run = [tuple(int(x) for x in it) for it in items[s:e]]
+            enum = sorted(run, key=lambda it: (it[5], it[0], it[2]))
+            groups = [[run[p] for p in range(r, len(run), 8)] for r in range(min(8, len(run)))]
+            # each group is a slice of the enumeration
+            start = {it: i for i, it in enumerate(enum)}
+            for g in groups:
+                i0 = start[g[0]]
+                assert g == enum[i0:i0 + len(g)], (op, s, e)
+            # the slices tile it, in a rotation of XCD order
+            firsts = sorted(range(len(groups)), key=lambda r: start[groups[r][0]])
+            assert sum(len(g) for g in groups) == len(enum)
+            assert all((firsts[i + 1] - firsts[i]) % 8 == 1 or len(groups) < 8
+                       for i in range(len(firsts) - 1)), (op, firsts)
+
+
+@pytest.mark.parametrize("causal", [False, True])
+@pytest.mark.parametrize("n_dummy", [0, 1])
+def test_xcd_shares_large(causal, n_dummy):
+    """A ring-sized chunk (8192 rows and keys, 28 slots, n_dummy of them
+    dummies): with the fills in front counted, launch position P runs on XCD
+    P % 8, and XCD x's positions of a run take share x of it (head by head),
+    the shares differing in size by at most one item."""
+    T, H, sp_n = 8192, 28, 4  # the last of 4 ranks (fewer dummies than ranks)
+    real = H - n_dummy
+    off = (sp_n - 1) * H
+    sh = make_shard("xcd", T, T, 128, H, off, off + real, sp_n * H, 1, real, off, [T],
+                    causal=causal)
+    d = lib_desc(sh)
+    n_front = n_dummy * -(-T // 8192)
+    items = sp.sp_attn_schedule(d, sp.SP_OP_FWD)
+    cost = [-(-(int(it[3]) - (int(it[2]) & ~7)) // 64) for it in items]
+    n_long = 0
+    for s, e in _runs(cost):
+        run = [tuple(int(x) for x in it) for it in items[s:e]]
+        enum = sorted(run, key=lambda it: (it[5], it[0]))
+        shares = [[run[p - s] for p in range(s, e) if (n_front + p) % 8 == x] for x in range(8)]
+        assert sum(shares, []) == enum
+        sizes = [len(g) for g in shares]
+        assert max(sizes) - min(sizes) <= 1
+        n_long += (e - s) >= 8
+    assert n_long >= (1 if not causal else 8)
+    if not causal:  # one run: XCD x holds heads x*real/8 .. about (x+1)*real/8
+        heads = [sorted({it[5] for it in g}) for g in shares]
+        assert all(len(h) <= -(-real // 8) + 1 for h in heads), heads
