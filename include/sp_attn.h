@@ -350,7 +350,9 @@ sp_status sp_f32_to_bf16(const float* src, void* dst, int64_t n, void* stream);
  *   SP_OP_FWD / SP_OP_RING_STEP (init=1): {q_begin, q_end, k_begin, k_end,
  *       delta, head, kv_head, 0} -- query rows [q_begin, q_end) of local
  *       head `head` against keys [k_begin, k_end); causal visibility is
- *       key <= row + delta.
+ *       key <= row + delta.  Row tiles hold 256 rows; under a causal mask
+ *       they end at the segment's end, so a partial tile is the segment's
+ *       first (its rows see the fewest keys).
  *   SP_OP_BWD, dK/dV items: {k_begin, k_end, q_begin, q_end, delta, head,
  *       kv_head, 1}.
  * Writes at most `capacity` items to `items` (may be NULL) and the total

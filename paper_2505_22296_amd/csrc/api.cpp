@@ -243,8 +243,14 @@ void schedule_rows(const sp_attn_desc* d, const Problem& p, int BM, int BN, bool
   std::vector<Item> items;
   for (int y = 0; y < p.n_real; ++y) {
     for (const Seg& g : p.segs) {
-      for (int a = g.qa; a < g.qb; a += BM) {
-        const int b = std::min(a + BM, g.qb);
+      // Causal row tiles end at the segment's end, so a partial tile is the
+      // segment's first: its rows see the fewest keys.  (Aligned to the
+      // start, the partial tile would be the last -- the segment's longest
+      // item -- with most of its wavefronts idle.)
+      const int len = g.qb - g.qa;
+      const int first = d->causal && len % BM ? len % BM : BM;
+      for (int a = g.qa, b = g.qa + std::min(first, len); a < g.qb;
+           a = b, b = std::min(b + BM, g.qb)) {
         int k1 = g.kb;
         if (d->causal) k1 = (int)std::min<int64_t>(g.kb, (int64_t)b + g.delta);
         const int k0 = g.ka;

@@ -165,3 +165,56 @@ def test_xcd_shares_large(causal, n_dummy):
     if not causal:  # one run: XCD x holds heads x*real/8 .. about (x+1)*real/8
         heads = [sorted({it[5] for it in g}) for g in shares]
         assert all(len(h) <= -(-real // 8) + 1 for h in heads), heads
+
+
+@settings(max_examples=200, deadline=None, derandomize=True,
+          suppress_health_check=[HealthCheck.too_slow, HealthCheck.data_too_large])
+@given(shards())
+def test_causal_row_tiles_end_at_the_segment_end(sh):
+    """Forward row tiles of a causal segment end at its end: every tile has
+    the full 256 rows except the segment's first, which holds the remainder
+    (its rows see the fewest keys); non-causal tiles start at the segment's
+    start."""
+    if sh.single_sequence:
+        return
+    d = lib_desc(sh)
+    items = sp.sp_attn_schedule(d, sp.SP_OP_FWD)
+    real = [h for h in range(sh.H_loc) if sh.head_offset + h < sh.num_real_heads]
+    for h in real:
+        mine = items[items[:, 5] == h]
+        for s in range(len(sh.cu_q) - 1):
+            a, b = int(sh.cu_q[s]), int(sh.cu_q[s + 1])
+            tiles = sorted((int(it[0]), int(it[1])) for it in mine if a <= it[0] < b)
+            n = b - a
+            if n == 0:
+                assert tiles == []
+                continue
+            first = n % 256 if (sh.causal and n % 256) else min(256, n)
+            expect, at = [], a
+            while at < b:
+                end = min(b, at + (first if at == a else 256))
+                expect.append((at, end))
+                at = end
+            assert tiles == expect, (s, tiles[:3], expect[:3])
+
+
+@pytest.mark.parametrize("causal", [True, False])
+def test_row_tiles_of_long_segments(causal):
+    """The same property on segments longer than a tile (the drawn shards'
+    segments are shorter than one): 300, 700, 256, 1000 and 5 rows."""
+    lens = [300, 700, 256, 1000, 5]
+    T = sum(lens) + 40
+    sh = make_shard("long_segs", T, T, 128, 2, 0, 2, 2, 1, 2, 0, lens, causal=causal)
+    items = sp.sp_attn_schedule(lib_desc(sh), sp.SP_OP_FWD)
+    starts = np.concatenate([[0], np.cumsum(lens)])
+    for h in range(2):
+        got = sorted((int(it[0]), int(it[1])) for it in items[items[:, 5] == h])
+        want = []
+        for a, n in zip(starts[:-1], lens):
+            first = n % 256 if causal and n % 256 else 256
+            bounds = [0] + list(range(first, n, 256)) + [n]
+            want += [(int(a + x), int(a + y)) for x, y in zip(bounds[:-1], bounds[1:])]
+        want.append((int(starts[-1]), T))  # the padding rows: one item, rows see no key
+        assert got == sorted(want), (h, got, want)
+    if causal:  # the partial tiles are the segments' first
+        assert (300, 300 + 188) in got and (0, 44) in got
