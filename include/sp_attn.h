@@ -341,12 +341,16 @@ sp_status sp_f32_to_bf16(const float* src, void* dst, int64_t n, void* stream);
 /*
  * Introspection of the block-skip scheduler (host only, no GPU work): the
  * work items `op` would launch, SP_SCHED_ITEM_INTS int32 each, in launch
- * order.  That order is longest first; within a run of equal cost, whose
- * order leaves the balance over the CUs unchanged, it is arranged for the
- * eight XCDs (workgroup i of a launch runs on XCD i % 8, counting the fill
- * items below): the run's items, taken head by head, are cut into eight
- * contiguous shares, and the positions that fall on one XCD take one share,
- * so each XCD's L2 serves a few neighbouring heads.
+ * order, which is laid out per XCD (workgroup i of a launch runs on XCD
+ * i % 8, counting the fill items below; an XCD feeds its four shader
+ * engines in turn, in order): every XCD's share (positions x, x + 8, ...)
+ * is longest first.  Row items (SP_OP_FWD / SP_OP_RING_STEP) are dealt to
+ * the XCDs in groups of four consecutive items of the longest-first order,
+ * eight groups a round, the rounds alternately forwards and backwards over
+ * the XCDs (the rest item by item); dK/dV items one by one in list order.
+ * Within each cost the items an XCD gets are a contiguous share of that
+ * cost's items taken head by head, so each XCD's L2 serves a few
+ * neighbouring heads.
  *   SP_OP_FWD / SP_OP_RING_STEP (init=1): {q_begin, q_end, k_begin, k_end,
  *       delta, head, kv_head, 0} -- query rows [q_begin, q_end) of local
  *       head `head` against keys [k_begin, k_end); causal visibility is

@@ -247,11 +247,13 @@ def test_schedule_covers_exactly_the_mask(sh):
         cov = _coverage_from_schedule(sh, items, kind)
         for h in real:
             assert np.array_equal(cov[h], mask.astype(np.int32)), (op, h)
-        # longest first: tile counts never increase along the list
+        # longest first on every XCD (list positions 8 apart): tile counts
+        # never increase along an XCD's share
         a, b, step = (2, 3, 64) if kind == "rows" else (2, 3, 32)
         cost = np.array([-(-(int(it[b]) - (int(it[a]) & ~7)) // step) if it[b] > it[a] else 0
                          for it in items])
-        assert np.all(np.diff(cost) <= 0), (op, cost[:20])
+        for r in range(8):
+            assert np.all(np.diff(cost[r::8]) <= 0), (op, r, cost[r::8][:20])
 
 
 def test_schedule_rows_cover_every_row_once():

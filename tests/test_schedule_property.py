@@ -96,75 +96,125 @@ def test_schedule_matches_the_mask(sh):
         a, b, step = (2, 3, 64) if kind == "rows" else (2, 3, 32)
         cost = np.array([-(-(int(it[b]) - (int(it[a]) & ~7)) // step) if it[b] > it[a] else 0
                          for it in items])
-        assert np.all(np.diff(cost) <= 0), (op, cost[:20])
+        for r in range(8):  # longest first on every XCD (positions 8 apart)
+            assert np.all(np.diff(cost[r::8]) <= 0), (op, r, cost[r::8][:20])
+        if kind == "keys":  # dealt in list order: longest first along the whole list
+            assert np.all(np.diff(cost) <= 0), (op, cost[:20])
 
 
-def _runs(cost):
-    s = 0
-    for e in range(1, len(cost) + 1):
-        if e == len(cost) or cost[e] != cost[s]:
-            yield s, e
-            s = e
+def _costs(items, kind):
+    a, b, step = (2, 3, 64) if kind == "rows" else (2, 3, 32)
+    return np.array([-(-(int(it[b]) - (int(it[a]) & ~7)) // step) if it[b] > it[a] else 0
+                     for it in items])
+
+
+def _check_cost_shares(items, cost, n_front=None):
+    """For every cost value: the items of that cost on one XCD (list
+    positions p with (n_front + p) % 8 == x) are one contiguous slice of that
+    cost's items taken head by head, rows (keys) ascending, and the slices
+    follow each other in XCD order (from XCD 0 when n_front is given, else
+    from some XCD)."""
+    for c in sorted(set(cost.tolist())):
+        idx = np.nonzero(cost == c)[0]
+        run = [tuple(int(x) for x in items[i]) for i in idx]
+        enum = sorted(run, key=lambda it: (it[5], it[0], it[2]))
+        slot = {it: k for k, it in enumerate(enum)}
+        by_x = {}
+        for i, it in zip(idx, run):
+            by_x.setdefault(int(i) % 8 if n_front is None else (n_front + int(i)) % 8, []).append(it)
+        order = sorted(by_x, key=lambda x: slot[by_x[x][0]])
+        tiles = []
+        for x in order:
+            g = by_x[x]
+            k0 = slot[g[0]]
+            assert g == enum[k0:k0 + len(g)], (c, x)
+            tiles += g
+        assert tiles == enum, c
+        if n_front is not None:
+            assert order == sorted(order), (c, order)
+        else:  # a rotation of XCD order
+            assert all((order[i + 1] - order[i]) % 8 >= 1 for i in range(len(order) - 1))
+            assert sum((order[i + 1] - order[i]) % 8 for i in range(len(order) - 1)) < 8
 
 
 @settings(max_examples=200, deadline=None, derandomize=True,
           suppress_health_check=[HealthCheck.too_slow, HealthCheck.data_too_large])
 @given(shards())
-def test_equal_cost_runs_are_cut_per_xcd(sh):
-    """Within a run of equal cost the launch positions of one XCD (position
-    mod 8, whatever the number of fill items in front) hold one contiguous
-    share of the run taken head by head, rows (keys) ascending; the shares
-    follow each other in XCD order."""
+def test_equal_costs_are_cut_per_xcd(sh):
+    """Within each cost the items one XCD receives are one contiguous share
+    of that cost's items, head by head (whatever the number of fill items in
+    front)."""
     d = lib_desc(sh)
-    for op, (a, b, step) in ((sp.SP_OP_FWD, (2, 3, 64)), (sp.SP_OP_BWD, (2, 3, 32))):
+    for op, kind in ((sp.SP_OP_FWD, "rows"), (sp.SP_OP_BWD, "keys")):
         items = sp.sp_attn_schedule(d, op)
-        cost = [-(-(int(it[b]) - (int(it[a]) & ~7)) // step) if it[b] > it[a] else 0
-                for it in items]
-        for s, e in _runs(cost):
-            run = [tuple(int(x) for x in it) for it in items[s:e]]
-            enum = sorted(run, key=lambda it: (it[5], it[0], it[2]))
-            groups = [[run[p] for p in range(r, len(run), 8)] for r in range(min(8, len(run)))]
-            # each group is a slice of the enumeration
-            start = {it: i for i, it in enumerate(enum)}
-            for g in groups:
-                i0 = start[g[0]]
-                assert g == enum[i0:i0 + len(g)], (op, s, e)
-            # the slices tile it, in a rotation of XCD order
-            firsts = sorted(range(len(groups)), key=lambda r: start[groups[r][0]])
-            assert sum(len(g) for g in groups) == len(enum)
-            assert all((firsts[i + 1] - firsts[i]) % 8 == 1 or len(groups) < 8
-                       for i in range(len(firsts) - 1)), (op, firsts)
+        _check_cost_shares(items, _costs(items, kind))
+
+
+def _xcd_shard(T, causal, n_dummy, H=28, sp_n=4):
+    real = H - n_dummy
+    off = (sp_n - 1) * H  # the last of sp_n ranks (fewer dummies than ranks)
+    return make_shard("xcd", T, T, 128, H, off, off + real, sp_n * H, 1, real, off, [T],
+                      causal=causal)
 
 
 @pytest.mark.parametrize("causal", [False, True])
 @pytest.mark.parametrize("n_dummy", [0, 1])
 def test_xcd_shares_large(causal, n_dummy):
     """A ring-sized chunk (8192 rows and keys, 28 slots, n_dummy of them
-    dummies): with the fills in front counted, launch position P runs on XCD
-    P % 8, and XCD x's positions of a run take share x of it (head by head),
-    the shares differing in size by at most one item."""
-    T, H, sp_n = 8192, 28, 4  # the last of 4 ranks (fewer dummies than ranks)
-    real = H - n_dummy
-    off = (sp_n - 1) * H
-    sh = make_shard("xcd", T, T, 128, H, off, off + real, sp_n * H, 1, real, off, [T],
-                    causal=causal)
+    dummies): with the fill items in front counted, list position p runs on
+    XCD (n_front + p) % 8; within each cost, XCD x holds share x of that
+    cost's items (head by head); every XCD runs its share longest first."""
+    T = 8192
+    sh = _xcd_shard(T, causal, n_dummy)
     d = lib_desc(sh)
+    # fills in front: one per dummy slot (rows); none for the keys (every
+    # KV head here is read by a real head)
+    for op, kind, n_front in ((sp.SP_OP_FWD, "rows", n_dummy), (sp.SP_OP_BWD, "keys", 0)):
+        items = sp.sp_attn_schedule(d, op)
+        cost = _costs(items, kind)
+        _check_cost_shares(items, cost, n_front)
+        for x in range(8):
+            mine = cost[[p for p in range(len(cost)) if (n_front + p) % 8 == x]]
+            assert np.all(np.diff(mine) <= 0), (op, x)
+    if not causal:  # one cost: XCD x holds heads about x*real/8 .. (x+1)*real/8
+        real = 28 - n_dummy
+        items = sp.sp_attn_schedule(d, sp.SP_OP_FWD)
+        for x in range(8):
+            heads = {int(items[p, 5]) for p in range(len(items)) if (n_dummy + p) % 8 == x}
+            assert len(heads) <= -(-real // 8) + 1, (x, heads)
+
+
+@pytest.mark.parametrize("n_dummy", [0, 1])
+def test_row_items_dealt_in_groups_of_four(n_dummy):
+    """Row work lists (forward, dQ) go to each XCD in groups of four near-equal
+    items -- one per shader engine, which an XCD feeds in turn -- rounds of
+    eight groups alternating direction: on every XCD each full round's four
+    costs are four consecutive costs of the longest-first order, and the
+    XCDs' totals differ by less than the longest item.  A plain round-robin
+    deal would give one XCD's engine the longest of each round."""
+    T = 32768  # a 7B-like rank: 4 query slots on one causal sequence
+    if n_dummy:  # rank 1 of 2: slots 4..7 of 8, slot 7 a dummy (MHA)
+        sh = make_shard("g4", T, T, 128, 4, 4, 7, 8, 1, 3, 4, [T], causal=True)
+    else:  # 4 query heads on one KV head
+        sh = make_shard("g4", T, T, 128, 4, 0, 4, 4, 4, 1, 0, [T], causal=True)
+    items = sp.sp_attn_schedule(lib_desc(sh), sp.SP_OP_FWD)
     n_front = n_dummy * -(-T // 8192)
-    items = sp.sp_attn_schedule(d, sp.SP_OP_FWD)
-    cost = [-(-(int(it[3]) - (int(it[2]) & ~7)) // 64) for it in items]
-    n_long = 0
-    for s, e in _runs(cost):
-        run = [tuple(int(x) for x in it) for it in items[s:e]]
-        enum = sorted(run, key=lambda it: (it[5], it[0]))
-        shares = [[run[p - s] for p in range(s, e) if (n_front + p) % 8 == x] for x in range(8)]
-        assert sum(shares, []) == enum
-        sizes = [len(g) for g in shares]
-        assert max(sizes) - min(sizes) <= 1
-        n_long += (e - s) >= 8
-    assert n_long >= (1 if not causal else 8)
-    if not causal:  # one run: XCD x holds heads x*real/8 .. about (x+1)*real/8
-        heads = [sorted({it[5] for it in g}) for g in shares]
-        assert all(len(h) <= -(-real // 8) + 1 for h in heads), heads
+    cost = _costs(items, "rows")
+    srt = np.sort(cost)[::-1]
+    spread4 = max(srt[i] - srt[i + 3] for i in range(len(srt) - 3))
+    full_rounds = len(cost) // 32
+    assert full_rounds >= 8
+    totals = []
+    for x in range(8):
+        mine = cost[[p for p in range(len(cost)) if (n_front + p) % 8 == x]]
+        totals.append(int(mine.sum()))
+        for r in range(full_rounds):
+            grp = mine[4 * r:4 * r + 4]
+            assert grp.max() - grp.min() <= spread4, (x, r, grp)
+    assert max(totals) - min(totals) < cost.max(), totals
+    # and it matters: under round-robin the first four of an XCD are 8 apart
+    plain = srt[0:32:8]
+    assert plain.max() - plain.min() > spread4
 
 
 @settings(max_examples=200, deadline=None, derandomize=True,
