@@ -224,27 +224,36 @@ __global__ __launch_bounds__(NTQ, 1) void attn_dq_kernel(DqArgs a) {
   if (!row_ok) return;
   const float sc = a.scale;
   const int64_t base = ((int64_t)row * a.H + head) * D + hh * 4;
+  if (a.dq_acc) {  // ring: accumulate; the last chunk emits bf16 instead
+    // every accumulator value is loaded before the first store: the stores
+    // (through dq or dq_acc) could alias later loads for all the compiler
+    // knows, which would serialize one memory round trip per 16 bytes
+    float4 old[DB * 4];
 #pragma unroll
-  for (int d = 0; d < DB; ++d)
+    for (int i = 0; i < DB * 4; ++i)
+      old[i] = a.dq_init ? make_float4(0.f, 0.f, 0.f, 0.f)
+                         : *(const float4*)(a.dq_acc + base + (i >> 2) * 32 + (i & 3) * 8);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      float x0 = acc[d][j * 4] * sc, x1 = acc[d][j * 4 + 1] * sc;
-      float x2 = acc[d][j * 4 + 2] * sc, x3 = acc[d][j * 4 + 3] * sc;
-      if (a.dq_acc) {  // ring: accumulate; the last chunk emits bf16 instead
-        float4* p = (float4*)(a.dq_acc + base + d * 32 + j * 8);
-        float4 t = make_float4(x0, x1, x2, x3);
-        if (!a.dq_init) {
-          const float4 o = *p;
-          t = make_float4(o.x + x0, o.y + x1, o.z + x2, o.w + x3);
-        }
+    for (int d = 0; d < DB; ++d)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const float4 o = old[d * 4 + j];
+        const float4 t = make_float4(o.x + acc[d][j * 4] * sc, o.y + acc[d][j * 4 + 1] * sc,
+                                     o.z + acc[d][j * 4 + 2] * sc, o.w + acc[d][j * 4 + 3] * sc);
         if (a.dq)
           *(u32x2*)(a.dq + base + d * 32 + j * 8) = pack_bf16x4(t.x, t.y, t.z, t.w);
         else
-          *p = t;
-      } else {
-        *(u32x2*)(a.dq + base + d * 32 + j * 8) = pack_bf16x4(x0, x1, x2, x3);
+          *(float4*)(a.dq_acc + base + d * 32 + j * 8) = t;
       }
-    }
+  } else {
+#pragma unroll
+    for (int d = 0; d < DB; ++d)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        *(u32x2*)(a.dq + base + d * 32 + j * 8) =
+            pack_bf16x4(acc[d][j * 4] * sc, acc[d][j * 4 + 1] * sc, acc[d][j * 4 + 2] * sc,
+                        acc[d][j * 4 + 3] * sc);
+  }
 }
 
 // ---------------------------------------------------------------- dK / dV

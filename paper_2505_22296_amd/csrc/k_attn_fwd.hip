@@ -308,15 +308,22 @@ __global__ __launch_bounds__(NT, 1) void attn_fwd_kernel(FwdArgs a) {
       wa = ea / ssum;
       wb = eb / ssum * inv;  // folds the chunk's 1/l normalisation
     }
+    // every accumulator value is loaded before the first store (the stores
+    // could alias later loads for all the compiler knows, which would
+    // serialize one memory round trip per 16 bytes)
+    float4 old[DB * 4];
+#pragma unroll
+    for (int i = 0; i < DB * 4; ++i)
+      old[i] = a.init ? make_float4(0.f, 0.f, 0.f, 0.f)
+                      : *(const float4*)(a.o_acc + obase + (i >> 2) * 32 + (i & 3) * 8);
 #pragma unroll
     for (int d = 0; d < DB; ++d)
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        float4* po = (float4*)(a.o_acc + obase + d * 32 + j * 8);
-        float4 old = a.init ? make_float4(0.f, 0.f, 0.f, 0.f) : *po;
-        float4 nv = make_float4(wa * old.x + wb * oacc[d][j * 4], wa * old.y + wb * oacc[d][j * 4 + 1],
-                                wa * old.z + wb * oacc[d][j * 4 + 2], wa * old.w + wb * oacc[d][j * 4 + 3]);
-        *po = nv;
+        const float4 o = old[d * 4 + j];
+        float4 nv = make_float4(wa * o.x + wb * oacc[d][j * 4], wa * o.y + wb * oacc[d][j * 4 + 1],
+                                wa * o.z + wb * oacc[d][j * 4 + 2], wa * o.w + wb * oacc[d][j * 4 + 3]);
+        *(float4*)(a.o_acc + obase + d * 32 + j * 8) = nv;
         if (a.o_out) *(u32x2*)(a.o_out + obase + d * 32 + j * 8) = pack_bf16x4(nv.x, nv.y, nv.z, nv.w);
       }
     if (hh == 0) a.lse_acc[li] = L;
