@@ -197,6 +197,17 @@ SP_DEV void wait_batches(int pending) {
   }
 }
 
+// The 8 int32 of work item `pos`, read through the scalar cache (the list is
+// not written during a launch).  A plain read can become a vector load with a
+// full wait per field when the compiler cannot prove that no store of the
+// kernel precedes it.
+SP_DEV void load_item(const int32_t* items, int64_t pos, int32_t (&v)[8]) {
+  typedef const __attribute__((address_space(4))) int32_t cint;
+  cint* p = (cint*)(items + pos * 8);
+#pragma unroll
+  for (int j = 0; j < 8; ++j) v[j] = p[j];
+}
+
 // Zero-fill work items (dummy query slots, unread KV heads): the whole
 // workgroup writes rows [r0, r1) of head h of a [T, H, D] tensor with 16-byte
 // stores, block-strided.  bf16 (zero = +0) and float32 variants.

@@ -290,11 +290,11 @@ struct DkdvStage {
 };
 
 template <int D, bool PWAVE>
-SP_DEV void dkdv_body(const DkdvArgs& a, u32x4* smem, int w, int lane) {
+SP_DEV void dkdv_body(const DkdvArgs& a, const int32_t (&it)[kItemInts], u32x4* smem, int w,
+                      int lane) {
   using S = DkdvStage<D>;
   constexpr int BQ = S::BQ, KS = D / 16, DB = D / 32, SUB = S::SUB, NBW = S::NBW;
   constexpr int STAGE = S::STAGE;
-  const int32_t* it = a.items + (int64_t)blockIdx.x * kItemInts;
   const int k0 = it[0], k1 = it[1], qb = it[2], qe = it[3], delta = it[4], head = it[5],
             kvh = it[6];
   const int hh = lane >> 5, l32 = lane & 31;
@@ -505,7 +505,8 @@ SP_DEV void dkdv_body(const DkdvArgs& a, u32x4* smem, int w, int lane) {
 template <int D>
 __global__ __launch_bounds__(64 * 2 * NPF, 1) void attn_dkdv_kernel(DkdvArgs a) {
   __shared__ u32x4 smem[DkdvStage<D>::SMEM];
-  const int32_t* it = a.items + (int64_t)blockIdx.x * kItemInts;
+  int32_t it[kItemInts];
+  load_item(a.items, blockIdx.x, it);
   if (it[7] == kItemFillKV) {  // KV head no real query head reads: dK = dV = +0
     fill_rows_bf16(a.dk, it[0], it[1], a.Hkv, it[6], D, threadIdx.x, 64 * 2 * NPF);
     fill_rows_bf16(a.dv, it[0], it[1], a.Hkv, it[6], D, threadIdx.x, 64 * 2 * NPF);
@@ -514,9 +515,9 @@ __global__ __launch_bounds__(64 * 2 * NPF, 1) void attn_dkdv_kernel(DkdvArgs a) 
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (w < NPF)
-    dkdv_body<D, true>(a, smem, w, lane);
+    dkdv_body<D, true>(a, it, smem, w, lane);
   else
-    dkdv_body<D, false>(a, smem, w, lane);
+    dkdv_body<D, false>(a, it, smem, w, lane);
 }
 
 }  // namespace

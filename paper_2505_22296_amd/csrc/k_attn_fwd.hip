@@ -297,6 +297,15 @@ __global__ __launch_bounds__(NT, 1) void attn_fwd_kernel(FwdArgs a) {
       }
     if (hh == 0) a.lse[(int64_t)head * a.T_q + row] = lse_v;
   } else {
+    // every accumulator value is loaded before the first store (the stores
+    // could alias later loads for all the compiler knows, which would
+    // serialize one memory round trip per 16 bytes), together with the
+    // accumulated LSE
+    float4 old[DB * 4];
+#pragma unroll
+    for (int i = 0; i < DB * 4; ++i)
+      old[i] = a.init ? make_float4(0.f, 0.f, 0.f, 0.f)
+                      : *(const float4*)(a.o_acc + obase + (i >> 2) * 32 + (i & 3) * 8);
     const int64_t li = (int64_t)head * a.T_q + row;
     const float la = a.init ? neg_inf() : a.lse_acc[li];
     float wa = 0.f, wb = 0.f, L = neg_inf();
@@ -308,14 +317,6 @@ __global__ __launch_bounds__(NT, 1) void attn_fwd_kernel(FwdArgs a) {
       wa = ea / ssum;
       wb = eb / ssum * inv;  // folds the chunk's 1/l normalisation
     }
-    // every accumulator value is loaded before the first store (the stores
-    // could alias later loads for all the compiler knows, which would
-    // serialize one memory round trip per 16 bytes)
-    float4 old[DB * 4];
-#pragma unroll
-    for (int i = 0; i < DB * 4; ++i)
-      old[i] = a.init ? make_float4(0.f, 0.f, 0.f, 0.f)
-                      : *(const float4*)(a.o_acc + obase + (i >> 2) * 32 + (i & 3) * 8);
 #pragma unroll
     for (int d = 0; d < DB; ++d)
 #pragma unroll
