@@ -214,12 +214,14 @@ struct Item {
 // So the list is built per XCD:
 //  (1) items sorted longest first (enumerated head by head; the sort keeps
 //      that order among equal costs);
-//  (2) dealt to the XCDs in groups of four consecutive items -- equal or
-//      near-equal costs, which the XCD then runs one per shader engine, so
-//      its engines free CUs in step -- eight groups a round, the rounds
-//      alternately forwards and backwards over the XCDs so that no XCD
-//      always takes the round's longest group; what is left after the last
-//      full round goes item by item in list order;
+//  (2) with `grouped` (row items: forward, dQ), dealt to the XCDs in groups
+//      of four consecutive items -- equal or near-equal costs, which the
+//      XCD then runs one per shader engine, so its engines free CUs in
+//      step -- eight groups a round, the rounds alternately forwards and
+//      backwards over the XCDs so that no XCD always takes the round's
+//      longest group; what is left after the last full round, and every
+//      dK/dV item list (measured better that way), goes item by item in
+//      list order;
 //  (3) within each cost, the items an XCD was dealt are replaced by a
 //      contiguous share of that cost's items, taken head by head, so each
 //      XCD's L2 serves a few neighbouring heads (the costs per XCD stay);
